@@ -1,0 +1,148 @@
+"""Literal-loop twin of the fp64 oracle, for inputs of at most a few dozen tokens.
+
+TEST INFRASTRUCTURE ONLY (same rule as ``stlite_oracle``: the compression library
+never imports it).  Every quantity is written with explicit Python loops over
+tokens, neighbours, rows and dimensions, straight from the paper's definitions,
+so that a vectorisation slip in the NumPy oracle shows up as a disagreement:
+
+  A_base^(i) = (1/G) sum_g sum_{p in window} exp(z_{g,p,i}) / sum_{j<=p} exp(z_{g,p,j}),
+      z = q . k / sqrt(d)                               (Eq. base_attention; readings R1, R2)
+  H_{u,v}   = (1/|N|) sum_{n in N(u,v)} cos(h_{u,v}, h_n), Phi = 1 - H   (Eq. css_calc)
+  rho_i     = max_{j in current frame} cos(h_i, h_j)  (Sec. TSG)
+  gate      = the m = min(B, |pool|) smallest rho by (rho, index)       (Eqs. budget_threshold,
+                                                                        temporal_mask; R7)
+  S         = A (text) | M (A + alpha Phi) (visual)  (Eq. modal_scoring)
+  I_keep    = first B by (S descending, index ascending), ascending  (Top_B; R16)
+
+It reuses nothing from the NumPy oracle except the bf16 widening rule, which it
+restates with ``struct``.
+"""
+from __future__ import annotations
+
+import math
+import struct
+
+
+def bf16(bits: int) -> float:
+    return struct.unpack("<f", struct.pack("<I", (int(bits) & 0xFFFF) << 16))[0]
+
+
+def f32(x: float) -> float:
+    """Round a Python float to the nearest float32 (ranking precision, R-dec)."""
+    return struct.unpack("<f", struct.pack("<f", x))[0]
+
+
+def dot(a, b):
+    s = 0.0
+    for x, y in zip(a, b):
+        s += x * y
+    return s
+
+
+def cos(a, b):
+    na = math.sqrt(dot(a, a))
+    nb = math.sqrt(dot(b, b))
+    if na == 0.0 or nb == 0.0:
+        return 0.0
+    return dot(a, b) / (na * nb)
+
+
+def base_score(Q, K):
+    """Q: list[G][delta][d] floats, K: list[L][d]."""
+    G = len(Q)
+    delta = len(Q[0])
+    L = len(K)
+    d = len(K[0])
+    A = [0.0] * L
+    for g in range(G):
+        for w in range(delta):
+            p = L - delta + w
+            z = [dot(Q[g][w], K[i]) / math.sqrt(d) for i in range(p + 1)]
+            zm = max(z)
+            den = 0.0
+            for i in range(p + 1):
+                den += math.exp(z[i] - zm)
+            for i in range(p + 1):
+                A[i] += math.exp(z[i] - zm) / den
+    return [a / G for a in A]
+
+
+def css(K, frames):
+    L = len(K)
+    phi = [0.0] * L
+    for off, rows, cols in frames:
+        for u in range(rows):
+            for v in range(cols):
+                centre = K[off + u * cols + v]
+                total = 0.0
+                count = 0
+                for du in (-1, 0, 1):
+                    for dv in (-1, 0, 1):
+                        if du == 0 and dv == 0:
+                            continue
+                        uu, vv = u + du, v + dv
+                        if 0 <= uu < rows and 0 <= vv < cols:
+                            total += cos(centre, K[off + uu * cols + vv])
+                            count += 1
+                phi[off + u * cols + v] = 0.0 if count == 0 else 1.0 - total / count
+    return phi
+
+
+def partition(L, frames):
+    hist, cur = [], []
+    visual = [False] * L
+    for f, (off, rows, cols) in enumerate(frames):
+        ids = list(range(off, off + rows * cols))
+        for i in ids:
+            visual[i] = True
+        if f == len(frames) - 1:
+            cur = ids
+        else:
+            hist.extend(ids)
+    return hist, cur, visual
+
+
+def rho(K, hist, cur, snap=1e-4):
+    out = {}
+    for i in hist:
+        best = -2.0
+        for j in cur:
+            c = cos(K[i], K[j])
+            if c > best:
+                best = c
+        best = min(1.0, max(-1.0, best))
+        if best >= 1.0 - snap:
+            best = 1.0
+        out[i] = best
+    return out
+
+
+def gate(rho_of, hist, L, B):
+    g = [1] * L
+    m = min(B, len(hist))
+    ranked = sorted(hist, key=lambda i: (f32(rho_of[i]), i))
+    for i in hist:
+        g[i] = 0
+    for i in ranked[:m]:
+        g[i] = 1
+    return g
+
+
+def scores(A, phi, g, visual, alpha):
+    return [g[i] * (A[i] + alpha * phi[i]) if visual[i] else A[i] for i in range(len(A))]
+
+
+def top_b(S, B):
+    ranked = sorted(range(len(S)), key=lambda i: (-f32(S[i]), i))
+    return sorted(ranked[:B])
+
+
+def compress(Q, K, frames, B, alpha=1.0, use_css=True, use_tsg=True):
+    L = len(K)
+    A = base_score(Q, K)
+    hist, cur, visual = partition(L, frames)
+    phi = css(K, frames) if use_css else [0.0] * L
+    r = rho(K, hist, cur)
+    g = gate(r, hist, L, B) if use_tsg else [1] * L
+    S = scores(A, phi, g, visual, alpha if use_css else 0.0)
+    return dict(A=A, phi=phi, rho=r, gate=g, S=S, kept=top_b(S, B))

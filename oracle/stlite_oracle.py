@@ -1,0 +1,300 @@
+"""fp64 CPU oracle of the ST-Lite prefill-time KV-cache compression pass.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the package smoke check and the
+benchmark's CPU-baseline leg may import or call this module; the compression
+library never does, and this module imports nothing from it.
+
+The oracle is plain and slow on purpose: each function writes out one
+definition of the paper in float64 (NumPy; fp64 matmul is used as a library
+primitive for dot products), in the order the paper's compression procedure
+(the algorithm "ST-Lite Compression Procedure", appendix "Algorithm Details")
+takes them:
+
+  budget           B = floor(beta * L)                      (problem setup)
+  base_score       A_base, window voting of softmax rows      (Eq. base_attention)
+  css_saliency     H = mean Moore-neighbour cosine, Phi = 1-H (Eq. css_calc, Sec. CSS)
+  tsg_rho          rho_i = max cosine to the current frame    (Sec. TSG)
+  tsg_gate         tau_red = min(B,|pool|)-th smallest rho,
+                   M_time = 1[rho <= tau_red]                 (Eqs. budget_threshold, temporal_mask)
+  integrate        S = A (text), M (A + alpha Phi) (visual)   (Eq. modal_scoring)
+  select_topk      I_keep = Top_B(S)                          (Sec. integrated scoring)
+  compact          K' = K[I_keep], V' = V[I_keep]             (algorithm's return value)
+
+Readings where the paper is silent (each is also listed in the design notes):
+
+  R1  causal window: window query at position p only sees keys 0..p;
+  R2  GQA: A_base of a kv head is the mean over its G query heads of the
+      single-head window sum;
+  R3  CSS and TSG use the key vectors of each kv head separately (d = 128);
+  R5  grid borders: only in-grid Moore neighbours count (8/5/3); no neighbour
+      (1x1 grid) gives Phi = 0;
+  R6  cosine with a zero-norm vector is 0;
+  R7  ties at tau_red: the gate admits exactly m = min(B, |pool|) historical
+      tokens, taken in (rho ascending, index ascending) order;
+  R8  rho >= 1 - 1e-4 is snapped to exactly 1 (duplicate class);
+  R9  beta is a rational num/den and B = floor(L*num/den) in integers;
+  R11 no forced keep of the window; R13 gated-out visual tokens score 0;
+  R16 I_keep is emitted in ascending token order;
+  R-dec ranking decisions (gate admission, top-B) are taken on the scores
+      rounded to float32, the precision the GPU kernels compute them in; ties
+      go to the lowest token index.
+
+Parity unpinned (by the paper): readings R1, R2, R3, R8 and R11 are choices the
+paper does not arbitrate -- it prints no numeric A_base, Phi, rho or S for any
+input -- so the tests pin the oracle under these readings (closed forms,
+invariants, the literal twin), not against printed values.
+
+Arrays: keys/values/queries arrive as bf16 bit patterns (uint16) exactly as
+stored; ``bf16_to_f64`` widens them exactly.  Token indices inside one
+sequence are local (0..L-1); ``compress_sequence`` adds the sequence offset.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+SNAP_EPS = 1e-4          # reading R8
+DECIDE_DTYPE = np.float32  # reading R-dec
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns (uint16) to float64."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Budget (problem setup: B = floor(beta * L); Alg. initialisation)
+# ---------------------------------------------------------------------------
+
+def budget(L: int, beta_num: int, beta_den: int) -> int:
+    """B = floor(beta * L) with beta = beta_num / beta_den, in exact integers."""
+    if L < 0 or beta_num <= 0 or beta_den <= 0 or beta_num > beta_den:
+        raise ValueError("need L >= 0 and 0 < beta <= 1")
+    return (int(L) * int(beta_num)) // int(beta_den)
+
+
+# ---------------------------------------------------------------------------
+# Window base score (Eq. base_attention)
+# ---------------------------------------------------------------------------
+
+def base_score(Q: np.ndarray, K: np.ndarray, row_chunk: int = 64) -> np.ndarray:
+    """A_base for one kv head of one sequence.
+
+    Q: [G, delta, d] float64 -- the group's window queries; window position w
+       sits at token p = L - delta + w.
+    K: [L, d] float64.
+    Returns A [L]: (1/G) * sum_g sum_w softmax_{i <= p}(q_{g,w} . k_i / sqrt(d)).
+    """
+    G, delta, d = Q.shape
+    L = K.shape[0]
+    if delta > L:
+        raise ValueError("window longer than the sequence")
+    rows = Q.reshape(G * delta, d)
+    pos = np.tile(np.arange(L - delta, L), G)           # token position of every row
+    A = np.zeros(L, dtype=np.float64)
+    scale = 1.0 / math.sqrt(d)
+    keys = np.arange(L)
+    for r0 in range(0, rows.shape[0], row_chunk):
+        z = (rows[r0:r0 + row_chunk] @ K.T) * scale      # [r, L] logits
+        visible = keys[None, :] <= pos[r0:r0 + row_chunk, None]   # R1 causal
+        z = np.where(visible, z, -np.inf)
+        zmax = z.max(axis=1, keepdims=True)
+        e = np.exp(z - zmax)
+        P = e / e.sum(axis=1, keepdims=True)              # softmax over visible keys
+        A += P.sum(axis=0)
+    return A / G                                          # R2
+
+
+# ---------------------------------------------------------------------------
+# Cosine helper (R6)
+# ---------------------------------------------------------------------------
+
+def _cos_matrix(X: np.ndarray, Y: np.ndarray) -> np.ndarray:
+    nx = np.sqrt((X * X).sum(axis=1))
+    ny = np.sqrt((Y * Y).sum(axis=1))
+    dots = X @ Y.T
+    den = nx[:, None] * ny[None, :]
+    return np.where(den > 0, dots / np.where(den > 0, den, 1.0), 0.0)
+
+
+def _cos_rows(X: np.ndarray, Y: np.ndarray) -> np.ndarray:
+    """Row-wise cosine of equally shaped [n, d] arrays."""
+    nx = np.sqrt((X * X).sum(axis=1))
+    ny = np.sqrt((Y * Y).sum(axis=1))
+    den = nx * ny
+    dots = (X * Y).sum(axis=1)
+    return np.where(den > 0, dots / np.where(den > 0, den, 1.0), 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Component-centric Spatial Saliency (Eq. css_calc and Phi_space = 1 - H)
+# ---------------------------------------------------------------------------
+
+MOORE = [(-1, -1), (-1, 0), (-1, 1), (0, -1), (0, 1), (1, -1), (1, 0), (1, 1)]
+
+
+def css_frame(X: np.ndarray, rows: int, cols: int) -> np.ndarray:
+    """Phi for one frame.  X: [rows*cols, d] keys in row-major grid order."""
+    d = X.shape[1]
+    grid = X.reshape(rows, cols, d)
+    acc = np.zeros((rows, cols))
+    cnt = np.zeros((rows, cols))
+    for du, dv in MOORE:
+        # centre cells whose neighbour (u+du, v+dv) is inside the grid (R5)
+        u0, u1 = max(0, -du), min(rows, rows - du)
+        v0, v1 = max(0, -dv), min(cols, cols - dv)
+        if u1 <= u0 or v1 <= v0:
+            continue
+        c = grid[u0:u1, v0:v1].reshape(-1, d)
+        n = grid[u0 + du:u1 + du, v0 + dv:v1 + dv].reshape(-1, d)
+        acc[u0:u1, v0:v1] += _cos_rows(c, n).reshape(u1 - u0, v1 - v0)
+        cnt[u0:u1, v0:v1] += 1
+    H = np.where(cnt > 0, acc / np.where(cnt > 0, cnt, 1), 1.0)   # no neighbour -> Phi = 0
+    return (1.0 - H).reshape(-1)
+
+
+def css_saliency(K: np.ndarray, frames: Sequence[Tuple[int, int, int]]) -> np.ndarray:
+    """Phi_space over one sequence (0 on text tokens).  frames: local (offset, rows, cols)."""
+    phi = np.zeros(K.shape[0])
+    for off, r, c in frames:
+        phi[off:off + r * c] = css_frame(K[off:off + r * c], r, c)
+    return phi
+
+
+# ---------------------------------------------------------------------------
+# Trajectory-aware Semantic Gating (Sec. TSG; Eqs. budget_threshold, temporal_mask)
+# ---------------------------------------------------------------------------
+
+def split_tokens(L: int, frames: Sequence[Tuple[int, int, int]]):
+    """(historical visual, current-frame visual, text) local token indices."""
+    hist: List[np.ndarray] = []
+    cur = np.zeros(0, dtype=np.int64)
+    visual = np.zeros(L, dtype=bool)
+    for f, (off, r, c) in enumerate(frames):
+        idx = np.arange(off, off + r * c)
+        visual[idx] = True
+        if f == len(frames) - 1:
+            cur = idx
+        else:
+            hist.append(idx)
+    h = np.concatenate(hist) if hist else np.zeros(0, dtype=np.int64)
+    return h, cur, np.flatnonzero(~visual)
+
+
+def tsg_rho(K: np.ndarray, hist: np.ndarray, cur: np.ndarray, chunk: int = 4096) -> np.ndarray:
+    """rho_i = max over current-frame j of cos(k_i, k_j), clamped to [-1, 1], snapped (R8)."""
+    rho = np.zeros(len(hist))
+    if len(hist) == 0:
+        return rho
+    if len(cur) == 0:
+        raise ValueError("historical tokens need a current frame")
+    Kc = K[cur]
+    for a in range(0, len(hist), chunk):
+        rho[a:a + chunk] = _cos_matrix(K[hist[a:a + chunk]], Kc).max(axis=1)
+    rho = np.clip(rho, -1.0, 1.0)
+    return np.where(rho >= 1.0 - SNAP_EPS, 1.0, rho)
+
+
+def tsg_gate(rho: np.ndarray, hist: np.ndarray, L: int, B: int):
+    """M_time over all L tokens (1 for text and the current frame) and tau_red.
+
+    m = min(B, |pool|) historical tokens are admitted, those first in
+    (rho ascending, index ascending) order, decided on float32 rho (R7, R-dec).
+    tau_red is the rho of the m-th admitted token (NaN when m = 0).
+    """
+    gate = np.ones(L, dtype=np.uint8)
+    m = min(B, len(hist))
+    if len(hist) == 0:
+        return gate, float("nan")
+    r32 = rho.astype(DECIDE_DTYPE)
+    order = np.lexsort((hist, r32))          # primary rho asc, secondary index asc
+    gate[hist] = 0
+    gate[hist[order[:m]]] = 1
+    tau = float(r32[order[m - 1]]) if m > 0 else float("nan")
+    return gate, tau
+
+
+# ---------------------------------------------------------------------------
+# Integrated score and flat top-B (Eq. modal_scoring; Sec. integrated scoring)
+# ---------------------------------------------------------------------------
+
+def integrate(A: np.ndarray, phi: np.ndarray, gate: np.ndarray, visual: np.ndarray,
+              alpha: float) -> np.ndarray:
+    """S = A on text; S = M (A + alpha Phi) on visual tokens."""
+    return np.where(visual, gate * (A + alpha * phi), A)
+
+
+def select_topk(S: np.ndarray, B: int) -> np.ndarray:
+    """The B tokens first in (S descending, index ascending) order, emitted ascending.
+
+    The ranking is decided on float32 S (R-dec)."""
+    s32 = S.astype(DECIDE_DTYPE)
+    order = np.lexsort((np.arange(len(S)), -s32.astype(np.float64)))
+    return np.sort(order[:B])
+
+
+def compact(K_bits: np.ndarray, V_bits: np.ndarray, kept: np.ndarray):
+    """K' = K[I_keep], V' = V[I_keep]: exact copies of the stored rows."""
+    return K_bits[kept].copy(), V_bits[kept].copy()
+
+
+# ---------------------------------------------------------------------------
+# One (sequence, layer, kv head) unit, and whole packed batches
+# ---------------------------------------------------------------------------
+
+def compress_unit(Q_bits: np.ndarray, K_bits: np.ndarray, V_bits: np.ndarray,
+                  frames: Sequence[Tuple[int, int, int]], beta: Tuple[int, int],
+                  alpha: float = 1.0, use_css: bool = True, use_tsg: bool = True) -> Dict:
+    """Run the whole procedure for one unit; local indices.
+
+    Q_bits [G, delta, d], K_bits/V_bits [L, d] (bf16 bits); frames local.
+    use_css=False drops the Phi term (alpha = 0); use_tsg=False sets M = 1.
+    """
+    K = bf16_to_f64(K_bits)
+    Q = bf16_to_f64(Q_bits)
+    L = K.shape[0]
+    B = budget(L, *beta)
+    A = base_score(Q, K)
+    hist, cur, text = split_tokens(L, frames)
+    visual = np.zeros(L, dtype=bool)
+    visual[hist] = True
+    visual[cur] = True
+    phi = css_saliency(K, frames) if use_css else np.zeros(L)
+    rho = tsg_rho(K, hist, cur)
+    if use_tsg:
+        gate, tau = tsg_gate(rho, hist, L, B)
+    else:
+        gate, tau = np.ones(L, dtype=np.uint8), float("nan")
+    S = integrate(A, phi, gate, visual, alpha if use_css else 0.0)
+    kept = select_topk(S, B)
+    k_out, v_out = compact(K_bits, V_bits, kept)
+    return dict(B=B, A=A, phi=phi, hist=hist, cur=cur, rho=rho, gate=gate, tau=tau,
+                S=S, kept=kept, k_out=k_out, v_out=v_out, visual=visual)
+
+
+def seq_frames_local(cu_seqlens, cu_frames, frame_meta, s: int):
+    """Frames of sequence s with offsets made local to the sequence."""
+    base = int(cu_seqlens[s])
+    return [(int(o) - base, int(r), int(c))
+            for o, r, c in frame_meta[cu_frames[s]:cu_frames[s + 1]]]
+
+
+def compress_sequence(q_bits, k_bits, v_bits, cu_seqlens, cu_frames, frame_meta, s: int,
+                      layer: int, kv: int, group: int, beta, alpha=1.0,
+                      use_css=True, use_tsg=True) -> Dict:
+    """One unit of a packed batch.
+
+    q_bits [layers, seqs, Hq, delta, d]; k_bits, v_bits [layers, Hkv, L_total, d].
+    Kept indices are returned both local and absolute.
+    """
+    a, b = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
+    frames = seq_frames_local(cu_seqlens, cu_frames, frame_meta, s)
+    Qg = q_bits[layer, s, kv * group:(kv + 1) * group]
+    out = compress_unit(Qg, k_bits[layer, kv, a:b], v_bits[layer, kv, a:b], frames, beta,
+                        alpha, use_css, use_tsg)
+    out["kept_abs"] = out["kept"] + a
+    out["offset"] = a
+    return out

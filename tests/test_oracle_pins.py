@@ -1,0 +1,400 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: numbers the
+paper prints, closed forms worked by hand (fixtures under tests/golden/),
+invariants, library routines for special cases, and the literal-loop twin.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+
+from oracle import literal as O1
+from oracle import stlite_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def frac(s):
+    return float(Fraction(s)) if isinstance(s, str) else float(s)
+
+
+# ---------------------------------------------------------------- budget ----
+
+def test_budget_paper_instantiation():
+    g = golden("f1_instantiation.json")
+    assert O.budget(g["W"], *g["rho"]) == g["floor_rho_W"]          # floor(0.76 * 2592) = 1969
+    assert O.budget(g["N"], *g["beta"]) == g["B"]                   # 20% of 12000 = 2400
+
+
+def test_budget_rational_not_float():
+    # 0.29 * 100 is 28.999999999999996 in binary floating point; the rational budget is 29.
+    assert math.floor(0.29 * 100) == 28
+    assert O.budget(100, 29, 100) == 29
+    assert O.budget(912, 1, 5) == 182
+    assert O.budget(150528, 1, 5) == 30105
+    assert O.budget(77, 1, 1) == 77
+    with pytest.raises(ValueError):
+        O.budget(10, 3, 2)
+
+
+def test_f1_marginal_rate_paper_numbers():
+    """Part (iii) of the F1 proposition with the paper's numbers: when the floor(rho W)
+    redundant tokens outrank all others, top-B keeps exactly B - floor(rho W) of the
+    N - floor(rho W) non-redundant ones: 431 / 10031 (printed as about 4.3%)."""
+    g = golden("f1_instantiation.json")
+    N, B, nred = g["N"], g["B"], g["floor_rho_W"]
+    rng = np.random.default_rng(5)
+    S = rng.uniform(0.0, 1.0, N)
+    red = rng.choice(N, nred, replace=False)
+    S[red] += 2.0
+    kept = O.select_topk(S, B)
+    nonred = np.setdiff1d(np.arange(N), red)
+    got = Fraction(len(np.intersect1d(kept, nonred)), len(nonred))
+    assert got == Fraction(g["marginal_num"], g["marginal_den"])
+    assert round(100 * float(got), 1) == g["marginal_percent"]
+
+
+# ------------------------------------------------------------ base score ----
+
+def _q_k_for_logits(z, d=128):
+    """One query and keys along e1 so that q . k_i / sqrt(d) = z_i."""
+    L = len(z)
+    K = np.zeros((L, d))
+    K[:, 0] = z
+    Q = np.zeros((1, 1, d))
+    Q[0, 0, 0] = math.sqrt(d)
+    return Q, K
+
+
+def test_base_score_worked_example():
+    g = golden("base_score_example.json")
+    z = [{"0": 0.0, "ln2": math.log(2), "ln3": math.log(3)}[s] for s in g["logits"]]
+    Q, K = _q_k_for_logits(z)
+    np.testing.assert_allclose(O.base_score(Q, K), [frac(a) for a in g["A"]], rtol=1e-14)
+
+
+def test_base_score_uniform_logits_closed_form():
+    """All logits equal: each window row spreads 1/(p+1) over keys 0..p, so
+    A_i = sum_{p >= max(i, L-delta)} 1/(p+1) (causal window, reading R1)."""
+    L, delta, G, d = 37, 6, 3, 128
+    Q = np.zeros((G, delta, d))
+    K = np.random.default_rng(1).standard_normal((L, d))
+    want = np.array([sum(1.0 / (p + 1) for p in range(max(i, L - delta), L)) for i in range(L)])
+    np.testing.assert_allclose(O.base_score(Q, K), want, rtol=1e-13)
+
+
+def test_base_score_single_row_is_library_softmax():
+    rng = np.random.default_rng(2)
+    L, d = 50, 128
+    Q = rng.standard_normal((1, 1, d))
+    K = rng.standard_normal((L, d))
+    want = scipy.special.softmax(K @ Q[0, 0] / math.sqrt(d))
+    np.testing.assert_allclose(O.base_score(Q, K), want, rtol=1e-12)
+
+
+def test_base_score_mass_equals_window():
+    rng = np.random.default_rng(3)
+    for (L, delta, G) in [(40, 8, 7), (100, 1, 2), (9, 9, 1)]:
+        A = O.base_score(rng.standard_normal((G, delta, 128)), rng.standard_normal((L, 128)))
+        assert abs(A.sum() - delta) < 1e-11
+        assert (A > 0).all()
+
+
+def test_base_score_gqa_mean_of_heads():
+    """Reading R2: a group's A_base is the mean of its heads' single-head scores."""
+    rng = np.random.default_rng(4)
+    Q = rng.standard_normal((3, 4, 128))
+    K = rng.standard_normal((30, 128))
+    per = [O.base_score(Q[g:g + 1], K) for g in range(3)]
+    np.testing.assert_allclose(O.base_score(Q, K), np.mean(per, axis=0), rtol=1e-13)
+
+
+def test_f1_part_i_bound_and_part_ii_eviction():
+    """F1 proposition, Part (i): the window query gives i* at most
+    1/(1 + floor(rho W) e^Delta) when floor(rho W) keys beat it by Delta; the bound
+    is reached when every other key is negligible.  Part (ii): with B <= floor(rho W)
+    a plain top-B (SnapKV mode) evicts i*."""
+    g = golden("f1_instantiation.json")
+    delta_gap = g["Delta"]
+    n_red = 40
+    L = 300
+    z = np.full(L, -60.0)
+    istar = 17
+    z[istar] = 0.0
+    red = np.arange(L - n_red, L)
+    z[red] = delta_gap
+    Q, K = _q_k_for_logits(z)
+    A = O.base_score(Q, K)
+    bound = 1.0 / (1.0 + n_red * math.exp(delta_gap))
+    assert A[istar] <= bound * (1 + 1e-12)
+    assert A[istar] == pytest.approx(bound, rel=1e-12)   # the other keys add < 1e-20
+    # Part (ii), at B = floor(rho W) and below.
+    for B in (n_red, n_red - 7):
+        S = O.integrate(A, np.zeros(L), np.ones(L, np.uint8), np.zeros(L, bool), 0.0)
+        assert istar not in set(O.select_topk(S, B))
+    # The printed instantiation: 1 / (1 + 1969 e^2.1) is 6.2e-5.
+    inst = 1.0 / (1.0 + g["floor_rho_W"] * math.exp(g["Delta"]))
+    assert float(f"{inst:.{g['attn_bound_sig_digits'] - 1}e}") == g["attn_bound"]
+
+
+# ------------------------------------------------------------------- CSS ----
+
+def _grid(cells, d=128):
+    e = np.eye(d)
+    return np.array([[c(e) for c in row] for row in cells]).reshape(-1, d)
+
+
+def test_css_golden_patterns():
+    g = golden("css_patterns.json")["patterns"]
+    e1 = lambda e: e[0]
+    e2 = lambda e: e[1]
+    ne1 = lambda e: -e[0]
+    grids = {
+        "identical": [[e1] * 3] * 3,
+        "centre_e1_ring_e2": [[e2, e2, e2], [e2, e1, e2], [e2, e2, e2]],
+        "checkerboard": [[e1, ne1, e1], [ne1, e1, ne1], [e1, ne1, e1]],
+    }
+    for name, cells in grids.items():
+        want = np.array([[frac(x) for x in row] for row in g[name]["phi"]]).reshape(-1)
+        got = O.css_frame(_grid(cells), 3, 3)
+        np.testing.assert_allclose(got, want, atol=1e-15, err_msg=name)
+
+
+def test_css_border_counts_and_degenerate_grids():
+    rng = np.random.default_rng(6)
+    assert O.css_frame(rng.standard_normal((1, 128)), 1, 1).tolist() == [0.0]
+    X = rng.standard_normal((2, 128))
+    c = X[0] @ X[1] / np.linalg.norm(X[0]) / np.linalg.norm(X[1])
+    np.testing.assert_allclose(O.css_frame(X, 1, 2), [1 - c, 1 - c], rtol=1e-14)
+    # a zero key has cosine 0 with everything (R6)
+    X = rng.standard_normal((9, 128))
+    X[4] = 0
+    phi = O.css_frame(X, 3, 3)
+    assert phi[4] == 1.0
+
+
+def test_css_range_and_scale_invariance():
+    rng = np.random.default_rng(7)
+    X = rng.standard_normal((5 * 7, 128))
+    phi = O.css_frame(X, 5, 7)
+    assert (phi >= 0).all() and (phi <= 2).all()
+    scales = rng.uniform(0.1, 10.0, size=(35, 1))
+    np.testing.assert_allclose(O.css_frame(X * scales, 5, 7), phi, rtol=1e-12, atol=1e-14)
+
+
+# ------------------------------------------------------------------- TSG ----
+
+def test_tsg_golden_example():
+    g = golden("tsg_example.json")
+    e = np.eye(128)
+    hist_vecs = [e[0], (e[0] + e[1]) / math.sqrt(2), -e[0], e[2]]
+    K = np.array(hist_vecs + [e[0], e[1]])
+    hist = np.arange(4)
+    cur = np.array([4, 5])
+    rho = O.tsg_rho(K, hist, cur)
+    want = [{"1": 1.0, "1/sqrt2": 1 / math.sqrt(2), "0": 0.0}[s] for s in g["rho"]]
+    np.testing.assert_allclose(rho, want, atol=1e-15)
+    for B, gate in g["gate_by_budget"].items():
+        got, tau = O.tsg_gate(rho, hist, 6, int(B))
+        assert got[:4].tolist() == gate, B
+        assert got[4:].tolist() == [1, 1]            # current frame exempt
+
+
+def test_tsg_count_invariant_and_threshold():
+    rng = np.random.default_rng(8)
+    L = 200
+    K = rng.standard_normal((L, 128))
+    hist = np.arange(0, 150)
+    cur = np.arange(150, 190)
+    rho = O.tsg_rho(K, hist, cur)
+    for B in (0, 1, 37, 149, 150, 500):
+        gate, tau = O.tsg_gate(rho, hist, L, B)
+        m = min(B, len(hist))
+        assert gate[hist].sum() == m
+        assert gate[150:].all()
+        if 0 < m:
+            r32 = rho.astype(np.float32)
+            assert (r32[gate[hist] == 1] <= np.float32(tau)).all()
+            assert (r32[gate[hist] == 0] >= np.float32(tau)).all()
+
+
+def test_tsg_rho_brute_force_and_snap():
+    rng = np.random.default_rng(9)
+    K = rng.standard_normal((30, 128))
+    K[3] = K[25] * 2.5            # exact duplicate direction of a current-frame key
+    K[4] = K[26] + 1e-3 * rng.standard_normal(128)  # near duplicate: cos > 1 - 1e-4
+    hist = np.arange(0, 20)
+    cur = np.arange(20, 30)
+    rho = O.tsg_rho(K, hist, cur)
+    for t, i in enumerate(hist):
+        best = max(K[i] @ K[j] / np.linalg.norm(K[i]) / np.linalg.norm(K[j]) for j in cur)
+        if best < 1 - 1e-4:
+            assert rho[t] == pytest.approx(best, abs=1e-14)
+    assert rho[3] == 1.0 and rho[4] == 1.0
+
+
+def _frames_seq(rng, n_frames, rows, cols, text, dup_of_last=None):
+    """Build a small sequence (keys fp32-representable as bf16) with frames+text."""
+    d = 128
+    frames, chunks, off = [], [], 0
+    for f in range(n_frames):
+        chunks.append(rng.standard_normal((rows * cols, d)))
+        frames.append((off, rows, cols))
+        off += rows * cols
+        chunks.append(rng.standard_normal((text, d)))
+        off += text
+    K = np.concatenate(chunks)
+    if dup_of_last is not None:   # historical frame dup_of_last becomes a copy of the current frame
+        o, r, c = frames[dup_of_last]
+        oc = frames[-1][0]
+        K[o:o + r * c] = K[oc:oc + r * c]
+    return K, frames
+
+
+def test_duplicate_frame_gated_out_and_never_kept():
+    """A historical frame equal to the current frame has rho = 1 everywhere; with at
+    least m other historical tokens below the snap band it is gated out entirely,
+    so none of its tokens can be kept."""
+    rng = np.random.default_rng(10)
+    K, frames = _frames_seq(rng, 4, 4, 5, 6, dup_of_last=1)
+    L = K.shape[0]
+    hist, cur, text = O.split_tokens(L, frames)
+    rho = O.tsg_rho(K, hist, cur)
+    o, r, c = frames[1]
+    dup_tokens = np.arange(o, o + r * c)
+    in_dup = np.isin(hist, dup_tokens)
+    assert (rho[in_dup] == 1.0).all()
+    B = O.budget(L, 1, 5)
+    m = min(B, len(hist))
+    assert (rho[~in_dup] < 1 - 1e-4).sum() >= m
+    gate, _ = O.tsg_gate(rho, hist, L, B)
+    assert gate[dup_tokens].sum() == 0
+    A = np.full(L, 1.0 / L)
+    visual = np.zeros(L, bool)
+    visual[hist] = True
+    visual[cur] = True
+    S = O.integrate(A, O.css_saliency(K, frames), gate, visual, 1.0)
+    assert not np.isin(O.select_topk(S, B), dup_tokens).any()
+
+
+def test_single_frame_tsg_is_noop():
+    rng = np.random.default_rng(11)
+    L, d = 60, 128
+    Kb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(L, d)), np.uint16)
+    Kb[::2] |= 0x8000
+    Vb = np.asarray(rng.integers(0, 0xFFFF, size=(L, d)), np.uint16)
+    Qb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(2, 4, d)), np.uint16)
+    frames = [(0, 5, 8)]
+    on = O.compress_unit(Qb, Kb, Vb, frames, (1, 5))
+    off = O.compress_unit(Qb, Kb, Vb, frames, (1, 5), use_tsg=False)
+    assert on["kept"].tolist() == off["kept"].tolist()
+    assert on["gate"].all()
+
+
+# ------------------------------------------------------- integrate/select ----
+
+def test_select_properties_brute_force():
+    rng = np.random.default_rng(12)
+    for trial in range(30):
+        L = int(rng.integers(1, 40))
+        S = rng.choice([0.0, 0.25, 0.5, 1.0], size=L) if trial % 2 else rng.uniform(0, 1, L)
+        B = int(rng.integers(0, L + 1))
+        kept = O.select_topk(S, B)
+        assert len(kept) == B and (np.diff(kept) > 0).all()
+        ks = set(kept.tolist())
+        for i in ks:
+            for j in range(L):
+                if j not in ks:
+                    assert S[i] > S[j] or (S[i] == S[j] and i < j)
+
+
+def test_beta_one_keeps_everything_and_snapkv_mode():
+    rng = np.random.default_rng(13)
+    L, d = 48, 128
+    Kb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(L, d)), np.uint16)
+    Kb[1::3] |= 0x8000
+    Vb = np.asarray(rng.integers(0, 0xFFFF, size=(L, d)), np.uint16)
+    Qb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(1, 3, d)), np.uint16)
+    frames = [(0, 3, 4), (16, 3, 4)]
+    full = O.compress_unit(Qb, Kb, Vb, frames, (1, 1))
+    assert full["kept"].tolist() == list(range(L))
+    assert (full["k_out"] == Kb).all() and (full["v_out"] == Vb).all()
+    # SnapKV mode (alpha = 0, TSG off) keeps the B largest A_base.
+    snap = O.compress_unit(Qb, Kb, Vb, frames, (1, 4), use_css=False, use_tsg=False)
+    A = snap["A"].astype(np.float32)
+    thr = np.sort(A)[::-1][snap["B"] - 1]
+    assert (A[snap["kept"]] >= thr).all()
+    assert (A[np.setdiff1d(np.arange(L), snap["kept"])] <= thr).all()
+
+
+def test_integrate_modal_cases():
+    A = np.array([0.1, 0.2, 0.3, 0.4])
+    phi = np.array([0.5, 0.6, 0.7, 0.8])
+    gate = np.array([1, 0, 1, 0], np.uint8)
+    visual = np.array([False, False, True, True])
+    S = O.integrate(A, phi, gate, visual, 2.0)
+    np.testing.assert_allclose(S, [0.1, 0.2, 0.3 + 1.4, 0.0])
+
+
+# --------------------------------------------------- literal twin (O1 = O2) --
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_literal_twin_agrees(seed):
+    rng = np.random.default_rng(100 + seed)
+    d = 128
+    rows, cols = [(2, 3), (3, 3), (1, 4), (4, 2)][seed]
+    nfr = [3, 2, 1, 3][seed]
+    text = [4, 3, 7, 2][seed]
+    chunks, frames, off = [], [], 0
+    for f in range(nfr):
+        frames.append((off, rows, cols))
+        chunks.append(rng.standard_normal((rows * cols, d)) / math.sqrt(d))
+        off += rows * cols
+        chunks.append(rng.standard_normal((text, d)) / math.sqrt(d))
+        off += text
+    K = np.concatenate(chunks)
+    if nfr > 1:   # one exact copy of a current-frame key in the history (snap class)
+        K[frames[0][0]] = K[frames[-1][0] + 1]
+    L = K.shape[0]
+    Kb = np.asarray(np.round(K * 64), np.int64)   # coarse values: exact in bf16
+    K = Kb / 64.0
+    G, delta = [2, 7, 1, 3][seed], [3, 2, 4, 1][seed]
+    Q = np.round(rng.standard_normal((G, delta, d)) * 8) / 64.0
+    B = O.budget(L, [1, 1, 2, 3][seed], [5, 3, 5, 4][seed])
+    alpha = [1.0, 0.5, 2.0, 1.0][seed]
+    lit = O1.compress([[list(map(float, r)) for r in g] for g in Q],
+                      [list(map(float, r)) for r in K], frames, B, alpha)
+    A = O.base_score(Q, K)
+    np.testing.assert_allclose(A, lit["A"], rtol=1e-12, atol=0)
+    hist, cur, text_idx = O.split_tokens(L, frames)
+    phi = O.css_saliency(K, frames)
+    np.testing.assert_allclose(phi, lit["phi"], rtol=1e-12, atol=1e-13)
+    rho = O.tsg_rho(K, hist, cur)
+    np.testing.assert_allclose(rho, [lit["rho"][int(i)] for i in hist], atol=1e-13)
+    gate, _ = O.tsg_gate(rho, hist, L, B)
+    assert gate.tolist() == lit["gate"]
+    visual = np.zeros(L, bool)
+    visual[hist] = True
+    visual[cur] = True
+    S = O.integrate(A, phi, gate, visual, alpha)
+    np.testing.assert_allclose(S, lit["S"], rtol=1e-12, atol=1e-14)
+    assert O.select_topk(S, B).tolist() == lit["kept"]
+
+
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")
+def test_bf16_widening_matches_torch():
+    torch = pytest.importorskip("torch")
+    bits = np.arange(0, 1 << 16, dtype=np.uint16)
+    finite = ((bits >> 7) & 0xFF) != 0xFF
+    want = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(O.bf16_to_f64(bits)[finite], want[finite])
