@@ -1,0 +1,212 @@
+/*
+ * stlite.h -- C ABI of the MI355X (gfx950) ST-Lite KV-cache compression pass.
+ *
+ * ST-Lite compresses the prefill KV cache of a GUI-agent trajectory, per layer
+ * and kv head, to a flat budget B = floor(beta * L) tokens (problem setup and
+ * the algorithm "ST-Lite Compression Procedure" of the paper).  The pass is
+ * five asynchronous calls, each one batched over all layers, kv heads and
+ * packed sequences:
+ *
+ *   stlite_score_window  A_base, window voting of softmax rows  (Eq. base_attention)
+ *   stlite_tsg_gate      rho, tau_red and the hard gate M_time    (Sec. TSG; Eqs.
+ *                        budget_threshold, temporal_mask)
+ *   stlite_css_saliency  Phi_space = 1 - mean Moore cosine        (Eq. css_calc)
+ *   stlite_select_topk   S and the retained set I_keep = Top_B(S) (Eq. modal_scoring)
+ *   stlite_compact_kv    K' = K[I_keep], V' = V[I_keep]           (the algorithm's result)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Pointers are DEVICE pointers unless their name starts with h_ (host).  bf16
+ * tensors are passed as their 16-bit patterns (uint16_t).  `stream` is a
+ * hipStream_t passed as void* (NULL = the default stream); every call only
+ * enqueues work on it and never synchronises the host.
+ *
+ * Units and layouts (innermost dimension contiguous, head_dim d = 128):
+ *   unit u = layer * n_kv_heads + kv_head; query head g belongs to kv head g / G,
+ *   G = n_q_heads / n_kv_heads.
+ *   q_win    bf16  [n_layers][n_seqs][n_q_heads][window][d]  queries of the last
+ *                  `window` tokens of every sequence (window position w is token
+ *                  L_s - window + w of sequence s)
+ *   k, v     bf16  [n_layers][n_kv_heads][total_tokens][d]
+ *   a_base, phi, rho, score   fp32  [n_layers][n_kv_heads][total_tokens]
+ *   gate     uint8 [n_layers][n_kv_heads][total_tokens]   1 = eligible
+ *   tau      fp32  [n_layers][n_kv_heads][n_seqs]
+ *   kept     int32 [n_layers][n_kv_heads][total_budget]   absolute token indices;
+ *                  sequence s owns entries cu_budget[s] .. cu_budget[s+1]-1, in
+ *                  ascending token order
+ *   k_out, v_out bf16 [n_layers][n_kv_heads][total_budget][d]
+ *
+ * Sequences are packed back to back (cu_seqlens).  Each sequence lists its
+ * frames (screenshots) in temporal order; a frame is a row-major rows x cols
+ * patch grid of consecutive visual tokens.  The LAST frame of a sequence is its
+ * current frame; the visual tokens of its other frames are historical; every
+ * token in no frame is text.
+ *
+ * Ownership and errors: the caller allocates every buffer, including the
+ * workspace sized by stlite_workspace_size; the library allocates nothing and
+ * keeps no state between calls (calls are re-entrant; calls that share a
+ * workspace must be ordered on one stream).  Inputs are never written; outputs
+ * must not alias inputs; every element of every output is written.  Host-side
+ * arguments (the h_ mirrors, sizes, pointers) are validated before anything is
+ * enqueued: a failing call returns STLITE_ERR_INVALID_ARG / _UNSUPPORTED /
+ * _WORKSPACE with nothing enqueued and a message for stlite_last_error().  A
+ * failed kernel launch returns STLITE_ERR_HIP.  The device metadata arrays must
+ * hold the same values as their host mirrors; kernels read them without
+ * re-validating.
+ */
+#ifndef STLITE_H
+#define STLITE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define STLITE_ABI_VERSION 1
+
+typedef enum stlite_status {
+  STLITE_OK = 0,
+  STLITE_ERR_INVALID_ARG = 1, /* malformed argument or layout */
+  STLITE_ERR_UNSUPPORTED = 2, /* well formed, but outside what the kernels implement */
+  STLITE_ERR_WORKSPACE = 3,   /* workspace missing or too small */
+  STLITE_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} stlite_status;
+
+/* Which call a workspace size is asked for. */
+typedef enum stlite_call {
+  STLITE_CALL_SCORE_WINDOW = 0,
+  STLITE_CALL_TSG_GATE = 1,
+  STLITE_CALL_CSS_SALIENCY = 2,
+  STLITE_CALL_SELECT_TOPK = 3,
+  STLITE_CALL_COMPACT_KV = 4,
+  STLITE_CALL_TSG_THRESHOLD = 5
+} stlite_call;
+
+/*
+ * The packed problem: model shape, window and the varlen layout.
+ *
+ * Limits: head_dim == 128; n_q_heads % n_kv_heads == 0; 1 <= window <= L_s for
+ * every sequence; G * window <= 512 (the window queries of one kv head stay
+ * resident in registers); total_tokens < 2^31.  Budgets are per sequence
+ * (the same for every layer and head: the paper's flat budget) and must satisfy
+ * 0 <= B_s <= L_s; stlite_budget computes floor(beta * L_s).
+ */
+typedef struct stlite_problem {
+  int32_t n_layers;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t n_seqs;
+  int32_t n_frames;      /* frames over all sequences */
+  int32_t window;        /* delta: observation window length */
+  int32_t reserved;      /* must be 0 */
+  int64_t total_tokens;  /* = cu_seqlens[n_seqs] */
+  int64_t total_budget;  /* = cu_budget[n_seqs] */
+  /* device arrays */
+  const int32_t* cu_seqlens;  /* [n_seqs+1] token prefix sums, cu_seqlens[0] = 0 */
+  const int32_t* cu_frames;   /* [n_seqs+1] frame prefix sums, cu_frames[0] = 0 */
+  const int32_t* frame_meta;  /* [n_frames][3] = {absolute token offset, rows, cols} */
+  const int32_t* cu_budget;   /* [n_seqs+1] budget prefix sums, cu_budget[0] = 0 */
+  /* host mirrors of the same four arrays (validation and launch sizing) */
+  const int32_t* h_cu_seqlens;
+  const int32_t* h_cu_frames;
+  const int32_t* h_frame_meta;
+  const int32_t* h_cu_budget;
+} stlite_problem;
+
+/* ABI version of the loaded library (STLITE_ABI_VERSION it was built with). */
+int32_t stlite_abi_version(void);
+
+/* Human-readable name of a status code (static string). */
+const char* stlite_status_string(stlite_status status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* stlite_last_error(void);
+
+/*
+ * Flat per-layer budget B = floor(L * beta_num / beta_den) in exact integer
+ * arithmetic (problem setup; beta = beta_num / beta_den in (0, 1]).  Returns -1
+ * when L < 0, beta_num <= 0, beta_den <= 0 or beta_num > beta_den.
+ */
+int64_t stlite_budget(int64_t L, int64_t beta_num, int64_t beta_den);
+
+/* Checks every host-visible field of `p` (STLITE_OK or the reason it fails). */
+stlite_status stlite_validate(const stlite_problem* p);
+
+/* Bytes of device workspace `call` needs for problem `p` (0 is possible). */
+stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, size_t* bytes);
+
+/*
+ * Window base score (Eq. base_attention), per unit and sequence:
+ *   A_i = (1/G) sum_{g in group} sum_{w < window} softmax_{j <= p_w}(q_{g,w} . k_j / sqrt(d))_i
+ * with p_w = L_s - window + w (a window query sees the keys up to its own
+ * position) and A_i = 0 for keys no window query sees.  bf16 operands, fp32
+ * accumulation.  Writes a_base [units][total_tokens].
+ */
+stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win,
+                                  const uint16_t* k, float* a_base, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/*
+ * Component-centric Spatial Saliency (Eq. css_calc): for every visual token,
+ * H = mean over its in-grid Moore neighbours (8, 5 or 3 of them) of the key
+ * cosine, and phi = 1 - H; phi = 0 for a 1x1 frame and for text tokens.  A
+ * cosine with a zero key is 0.  Writes phi [units][total_tokens].
+ */
+stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, float* phi,
+                                  void* stream);
+
+/*
+ * Trajectory-aware Semantic Gating (Sec. TSG): for every historical visual
+ * token i, rho_i = max over the current frame j of cos(k_i, k_j), clamped to
+ * [-1, 1] and snapped to 1 when >= 1 - 1e-4.  Then, with m = min(B_s, |hist|),
+ * the gate admits the m historical tokens first in (rho ascending, index
+ * ascending) order -- the rank form of M_time = 1[rho <= tau_red] -- and
+ * tau_red is the rho of the last admitted token (NaN if m = 0).  Text and
+ * current-frame tokens get gate 1.
+ * rho (nullable) receives rho on historical tokens and 0 elsewhere; tau
+ * (nullable) receives tau_red per [unit][seq]; gate is required.
+ */
+stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float* rho,
+                              float* tau, uint8_t* gate, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
+ * The threshold-and-gate half of stlite_tsg_gate on a caller-supplied rho
+ * [units][total_tokens] (only its historical entries are read).  Same gate and
+ * tau semantics.  Lets a caller gate on another similarity signal.
+ */
+stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, float* tau,
+                                   uint8_t* gate, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/*
+ * Integrated score and flat top-B (Eq. modal_scoring; Sec. integrated scoring):
+ *   S_i = A_i on text;  S_i = M_i * (A_i + alpha * phi_i) on visual tokens,
+ * then the B_s tokens of each sequence first in (S descending, index
+ * ascending) order are kept and written to `kept` in ascending order.
+ * phi == NULL drops the CSS term; gate == NULL means M = 1 everywhere
+ * (a_base alone with both NULL is SnapKV's voting with a flat budget).
+ * alpha must be finite and >= 0.  score (nullable) receives S [units][total_tokens].
+ */
+stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base,
+                                 const float* phi, const uint8_t* gate, float alpha,
+                                 int32_t* kept, float* score, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/*
+ * Cache compaction: k_out[u][j] = k[u][kept[u][j]] and likewise for v, as exact
+ * 256-byte row copies.  kept must hold valid token indices of the owning
+ * sequence (as written by stlite_select_topk).
+ */
+stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                const int32_t* kept, uint16_t* k_out, uint16_t* v_out,
+                                void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STLITE_H */

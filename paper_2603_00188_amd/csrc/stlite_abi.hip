@@ -1,0 +1,348 @@
+// Host layer of libstlite: argument validation, workspace sizing, launch
+// configuration and status codes for the C ABI declared in include/stlite.h.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "stlite.h"
+#include "stlite_internal.h"
+
+using namespace stlite;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+stlite_status fail(stlite_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+stlite_status ok() {
+  g_last_error[0] = '\0';
+  return STLITE_OK;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Host-side facts derived from the validated mirrors.
+struct Facts {
+  int64_t units;
+  int64_t max_seq;
+  int64_t total_hist_blocks;
+  int64_t max_cur;
+  int32_t rows, rows_pad, waves, row_blocks, chunk;
+  int64_t total_chunks;
+};
+
+Facts derive(const stlite_problem* p) {
+  Facts f{};
+  f.units = int64_t(p->n_layers) * p->n_kv_heads;
+  const int32_t G = p->n_q_heads / p->n_kv_heads;
+  f.rows = G * p->window;
+  const int nb = (f.rows + 15) / 16;
+  f.waves = (nb + 7) / 8;  // <= 4 waves of <= 8 resident 16-row blocks
+  f.row_blocks = (nb + f.waves - 1) / f.waves;
+  f.rows_pad = f.waves * f.row_blocks * 16;
+  // Key chunk per work-group: aim for >= 2048 work-groups so that all 256 CUs
+  // stay busy, while keeping each chunk long enough to amortise the Q load.
+  const int64_t work = f.units * p->total_tokens;
+  int64_t ch = ceil_div(work, 2048);
+  ch = ceil_div(ch, 64) * 64;
+  f.chunk = int32_t(std::min<int64_t>(4096, std::max<int64_t>(256, ch)));
+  for (int s = 0; s < p->n_seqs; ++s) {
+    const int64_t L = p->h_cu_seqlens[s + 1] - p->h_cu_seqlens[s];
+    f.max_seq = std::max(f.max_seq, L);
+    f.total_chunks += ceil_div(L, f.chunk);
+    const int32_t f0 = p->h_cu_frames[s], f1 = p->h_cu_frames[s + 1];
+    int64_t hist = 0;
+    for (int32_t fi = f0; fi < f1; ++fi) {
+      const int64_t n = int64_t(p->h_frame_meta[3 * fi + 1]) * p->h_frame_meta[3 * fi + 2];
+      if (fi + 1 < f1)
+        hist += n;
+      else
+        f.max_cur = std::max(f.max_cur, n);
+    }
+    f.total_hist_blocks += ceil_div(hist, 256);
+  }
+  return f;
+}
+
+Layout make_layout(const stlite_problem* p) {
+  Layout l;
+  l.cu_seqlens = p->cu_seqlens;
+  l.cu_frames = p->cu_frames;
+  l.frame_meta = p->frame_meta;
+  l.cu_budget = p->cu_budget;
+  l.n_seqs = p->n_seqs;
+  l.n_frames = p->n_frames;
+  l.n_units = p->n_layers * p->n_kv_heads;
+  l.n_kv_heads = p->n_kv_heads;
+  l.total_tokens = p->total_tokens;
+  l.total_budget = p->total_budget;
+  return l;
+}
+
+stlite_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(STLITE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+stlite_status check_ws(const stlite_problem* p, stlite_call call, const void* ws, size_t bytes) {
+  size_t need = 0;
+  stlite_status st = stlite_workspace_size(p, call, &need);
+  if (st != STLITE_OK) return st;
+  if (need > 0 && ws == nullptr) return fail(STLITE_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (bytes < need) return fail(STLITE_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0) return fail(STLITE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return STLITE_OK;
+}
+
+bool aligned16(const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t stlite_abi_version(void) { return STLITE_ABI_VERSION; }
+
+const char* stlite_status_string(stlite_status s) {
+  switch (s) {
+    case STLITE_OK: return "STLITE_OK";
+    case STLITE_ERR_INVALID_ARG: return "STLITE_ERR_INVALID_ARG";
+    case STLITE_ERR_UNSUPPORTED: return "STLITE_ERR_UNSUPPORTED";
+    case STLITE_ERR_WORKSPACE: return "STLITE_ERR_WORKSPACE";
+    case STLITE_ERR_HIP: return "STLITE_ERR_HIP";
+  }
+  return "STLITE_ERR_UNKNOWN";
+}
+
+const char* stlite_last_error(void) { return g_last_error; }
+
+int64_t stlite_budget(int64_t L, int64_t beta_num, int64_t beta_den) {
+  if (L < 0 || beta_num <= 0 || beta_den <= 0 || beta_num > beta_den) return -1;
+  const __int128 prod = static_cast<__int128>(L) * beta_num;
+  return static_cast<int64_t>(prod / beta_den);
+}
+
+stlite_status stlite_validate(const stlite_problem* p) {
+  if (!p) return fail(STLITE_ERR_INVALID_ARG, "problem is NULL");
+  if (p->reserved != 0) return fail(STLITE_ERR_INVALID_ARG, "reserved field must be 0");
+  if (p->n_layers < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1)
+    return fail(STLITE_ERR_INVALID_ARG, "n_layers, n_q_heads and n_kv_heads must be >= 1");
+  if (p->n_q_heads % p->n_kv_heads != 0)
+    return fail(STLITE_ERR_INVALID_ARG, "n_q_heads (%d) is not a multiple of n_kv_heads (%d)",
+                p->n_q_heads, p->n_kv_heads);
+  if (p->head_dim != kHeadDim)
+    return fail(STLITE_ERR_UNSUPPORTED, "head_dim %d: only %d is implemented", p->head_dim, kHeadDim);
+  if (p->n_seqs < 1) return fail(STLITE_ERR_INVALID_ARG, "n_seqs must be >= 1");
+  if (p->n_frames < 0) return fail(STLITE_ERR_INVALID_ARG, "n_frames must be >= 0");
+  if (p->window < 1) return fail(STLITE_ERR_INVALID_ARG, "window must be >= 1");
+  const int64_t G = p->n_q_heads / p->n_kv_heads;
+  if (G * p->window > kMaxWindowRows)
+    return fail(STLITE_ERR_UNSUPPORTED, "G * window = %lld exceeds %d", (long long)(G * p->window),
+                kMaxWindowRows);
+  if (!p->h_cu_seqlens || !p->h_cu_frames || !p->h_cu_budget || (p->n_frames > 0 && !p->h_frame_meta))
+    return fail(STLITE_ERR_INVALID_ARG, "a host layout mirror is NULL");
+  if (!p->cu_seqlens || !p->cu_frames || !p->cu_budget || (p->n_frames > 0 && !p->frame_meta))
+    return fail(STLITE_ERR_INVALID_ARG, "a device layout array is NULL");
+  if (p->h_cu_seqlens[0] != 0) return fail(STLITE_ERR_INVALID_ARG, "cu_seqlens[0] must be 0");
+  if (p->h_cu_frames[0] != 0) return fail(STLITE_ERR_INVALID_ARG, "cu_frames[0] must be 0");
+  if (p->h_cu_budget[0] != 0) return fail(STLITE_ERR_INVALID_ARG, "cu_budget[0] must be 0");
+  for (int s = 0; s < p->n_seqs; ++s) {
+    const int64_t a = p->h_cu_seqlens[s], b = p->h_cu_seqlens[s + 1];
+    if (b - a < p->window)
+      return fail(STLITE_ERR_INVALID_ARG, "sequence %d has %lld tokens, fewer than the window %d", s,
+                  (long long)(b - a), p->window);
+    const int64_t B = int64_t(p->h_cu_budget[s + 1]) - p->h_cu_budget[s];
+    if (B < 0 || B > b - a)
+      return fail(STLITE_ERR_INVALID_ARG, "sequence %d: budget %lld outside [0, %lld]", s, (long long)B,
+                  (long long)(b - a));
+    const int32_t f0 = p->h_cu_frames[s], f1 = p->h_cu_frames[s + 1];
+    if (f1 < f0 || f1 > p->n_frames)
+      return fail(STLITE_ERR_INVALID_ARG, "cu_frames is not a prefix sum ending at n_frames");
+    int64_t prev_end = a;
+    for (int32_t f = f0; f < f1; ++f) {
+      const int64_t off = p->h_frame_meta[3 * f], r = p->h_frame_meta[3 * f + 1], c = p->h_frame_meta[3 * f + 2];
+      if (r < 1 || c < 1) return fail(STLITE_ERR_INVALID_ARG, "frame %d has an empty grid (%lld x %lld)", f,
+                                      (long long)r, (long long)c);
+      if (off < prev_end || off + r * c > b)
+        return fail(STLITE_ERR_INVALID_ARG,
+                    "frame %d [%lld, %lld) overlaps its predecessor or leaves sequence %d [%lld, %lld)", f,
+                    (long long)off, (long long)(off + r * c), s, (long long)a, (long long)b);
+      prev_end = off + r * c;
+    }
+  }
+  if (p->h_cu_frames[p->n_seqs] != p->n_frames)
+    return fail(STLITE_ERR_INVALID_ARG, "cu_frames[n_seqs] = %d but n_frames = %d", p->h_cu_frames[p->n_seqs],
+                p->n_frames);
+  if (p->total_tokens != p->h_cu_seqlens[p->n_seqs])
+    return fail(STLITE_ERR_INVALID_ARG, "total_tokens %lld != cu_seqlens[n_seqs] %d", (long long)p->total_tokens,
+                p->h_cu_seqlens[p->n_seqs]);
+  if (p->total_budget != p->h_cu_budget[p->n_seqs])
+    return fail(STLITE_ERR_INVALID_ARG, "total_budget %lld != cu_budget[n_seqs] %d", (long long)p->total_budget,
+                p->h_cu_budget[p->n_seqs]);
+  if (int64_t(p->n_layers) * p->n_kv_heads > 65535)
+    return fail(STLITE_ERR_UNSUPPORTED, "more than 65535 (layer, kv head) units");
+  return ok();
+}
+
+stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, size_t* bytes) {
+  if (!bytes) return fail(STLITE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = 0;
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  const Facts f = derive(p);
+  const size_t per_token = size_t(f.units) * size_t(p->total_tokens);
+  switch (call) {
+    case STLITE_CALL_SCORE_WINDOW:
+      *bytes = align_up(size_t(f.units) * f.total_chunks * f.rows_pad * sizeof(float2)) +
+               align_up(size_t(f.units) * p->n_seqs * f.rows_pad * sizeof(float));
+      break;
+    case STLITE_CALL_TSG_GATE:
+      *bytes = 3 * align_up(per_token * sizeof(float));  // rho scratch, current-frame norms, keys
+      break;
+    case STLITE_CALL_TSG_THRESHOLD:
+    case STLITE_CALL_SELECT_TOPK:
+      *bytes = align_up(per_token * sizeof(uint32_t));
+      break;
+    case STLITE_CALL_CSS_SALIENCY:
+    case STLITE_CALL_COMPACT_KV:
+      *bytes = 0;
+      break;
+    default:
+      return fail(STLITE_ERR_INVALID_ARG, "unknown call %d", int(call));
+  }
+  return ok();
+}
+
+stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win, const uint16_t* k,
+                                  float* a_base, void* ws, size_t ws_bytes, void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_SCORE_WINDOW, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (!q_win || !k || !a_base) return fail(STLITE_ERR_INVALID_ARG, "q_win, k and a_base must be non-NULL");
+  if (!aligned16(q_win) || !aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "q_win and k must be 16-byte aligned");
+  const Facts f = derive(p);
+  ScoreArgs a;
+  a.lay = make_layout(p);
+  a.q = q_win;
+  a.k = k;
+  a.a_base = a_base;
+  a.partial = static_cast<float2*>(ws);
+  a.lse2 = reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                    align_up(size_t(f.units) * f.total_chunks * f.rows_pad * sizeof(float2)));
+  a.n_q_heads = p->n_q_heads;
+  a.group = p->n_q_heads / p->n_kv_heads;
+  a.window = p->window;
+  a.rows = f.rows;
+  a.rows_pad = f.rows_pad;
+  a.waves = f.waves;
+  a.row_blocks = f.row_blocks;
+  a.chunk = f.chunk;
+  a.total_chunks = int32_t(f.total_chunks);
+  return hip_status(launch_score_window(a, static_cast<hipStream_t>(stream)), "score_window launch");
+}
+
+stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, float* phi, void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (!k || !phi) return fail(STLITE_ERR_INVALID_ARG, "k and phi must be non-NULL");
+  if (!aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "k must be 16-byte aligned");
+  CssArgs a;
+  a.lay = make_layout(p);
+  a.k = k;
+  a.phi = phi;
+  a.splits = 8;
+  return hip_status(launch_css(a, static_cast<hipStream_t>(stream)), "css_saliency launch");
+}
+
+stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float* rho, float* tau,
+                              uint8_t* gate, void* ws, size_t ws_bytes, void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_TSG_GATE, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (!k || !gate) return fail(STLITE_ERR_INVALID_ARG, "k and gate must be non-NULL");
+  if (!aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "k must be 16-byte aligned");
+  const Facts f = derive(p);
+  const size_t slab = align_up(size_t(f.units) * p->total_tokens * sizeof(float));
+  char* w = static_cast<char*>(ws);
+  RhoArgs r;
+  r.lay = make_layout(p);
+  r.k = k;
+  r.rn_cur = reinterpret_cast<float*>(w + slab);
+  r.rho = rho ? rho : reinterpret_cast<float*>(w);
+  r.total_hist_blocks = int32_t(f.total_hist_blocks);
+  r.max_cur = int32_t(f.max_cur);
+  GateArgs g;
+  g.lay = r.lay;
+  g.rho = r.rho;
+  g.rho_zero_fill = rho;
+  g.tau = tau;
+  g.gate = gate;
+  g.keys = reinterpret_cast<uint32_t*>(w + 2 * slab);
+  return hip_status(launch_tsg_gate(r, g, static_cast<hipStream_t>(stream)), "tsg_gate launch");
+}
+
+stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, float* tau, uint8_t* gate,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_TSG_THRESHOLD, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (!rho || !gate) return fail(STLITE_ERR_INVALID_ARG, "rho and gate must be non-NULL");
+  GateArgs g;
+  g.lay = make_layout(p);
+  g.rho = rho;
+  g.rho_zero_fill = nullptr;
+  g.tau = tau;
+  g.gate = gate;
+  g.keys = static_cast<uint32_t*>(ws);
+  return hip_status(launch_tsg_threshold(g, static_cast<hipStream_t>(stream)), "tsg_threshold launch");
+}
+
+stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base, const float* phi,
+                                 const uint8_t* gate, float alpha, int32_t* kept, float* score, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_SELECT_TOPK, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (!a_base || (!kept && p->total_budget > 0))
+    return fail(STLITE_ERR_INVALID_ARG, "a_base and kept must be non-NULL");
+  if (!(alpha >= 0.0f) || !std::isfinite(alpha))
+    return fail(STLITE_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  SelectArgs a;
+  a.lay = make_layout(p);
+  a.a_base = a_base;
+  a.phi = phi;
+  a.gate = gate;
+  a.alpha = alpha;
+  a.kept = kept;
+  a.score = score;
+  a.keys = static_cast<uint32_t*>(ws);
+  return hip_status(launch_select(a, static_cast<hipStream_t>(stream)), "select_topk launch");
+}
+
+stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                const int32_t* kept, uint16_t* k_out, uint16_t* v_out, void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (p->total_budget == 0) return ok();
+  if (!k || !v || !kept || !k_out || !v_out)
+    return fail(STLITE_ERR_INVALID_ARG, "k, v, kept, k_out and v_out must be non-NULL");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out))
+    return fail(STLITE_ERR_INVALID_ARG, "k, v, k_out and v_out must be 16-byte aligned");
+  CompactArgs a;
+  a.lay = make_layout(p);
+  a.k = k;
+  a.v = v;
+  a.kept = kept;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)), "compact_kv launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,120 @@
+// Internal declarations shared by the host layer and the gfx950 kernels of
+// libstlite.  Nothing here is part of the public ABI (include/stlite.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace stlite {
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxWindowRows = 512;  // G * window limit (window queries stay in registers)
+
+// ---------------------------------------------------------------------------
+// Per-call launch descriptions (filled by the host layer, passed by value).
+// ---------------------------------------------------------------------------
+
+struct Layout {
+  const int32_t* cu_seqlens;
+  const int32_t* cu_frames;
+  const int32_t* frame_meta;
+  const int32_t* cu_budget;
+  int32_t n_seqs;
+  int32_t n_frames;
+  int32_t n_units;       // n_layers * n_kv_heads
+  int32_t n_kv_heads;
+  int64_t total_tokens;
+  int64_t total_budget;
+};
+
+struct ScoreArgs {
+  Layout lay;
+  const uint16_t* q;     // [layers][seqs][Hq][window][d]
+  const uint16_t* k;     // [units][L][d]
+  float* a_base;         // [units][L]
+  float2* partial;       // workspace [units][total_chunks][rows_pad] (max, sum) in log2 units
+  float* lse2;           // workspace [units][seqs][rows_pad]
+  int32_t n_q_heads;
+  int32_t group;         // G
+  int32_t window;
+  int32_t rows;          // G * window
+  int32_t rows_pad;      // waves * row_blocks * 16
+  int32_t waves;
+  int32_t row_blocks;    // 16-row MFMA blocks per wave
+  int32_t chunk;         // keys per work-group (multiple of 64)
+  int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
+};
+
+struct RhoArgs {
+  Layout lay;
+  const uint16_t* k;
+  float* rn_cur;         // workspace [units][L]: inverse norms of current-frame keys
+  float* rho;            // [units][L]; written on historical tokens
+  int32_t total_hist_blocks;  // sum over sequences of ceil(N_hist_s / 256)
+  int32_t max_cur;       // largest current frame (tokens)
+};
+
+struct GateArgs {
+  Layout lay;
+  const float* rho;      // [units][L] (historical entries read)
+  float* rho_zero_fill;  // nullable: non-historical entries of this array are set to 0
+  float* tau;            // nullable [units][seqs]
+  uint8_t* gate;         // [units][L]
+  uint32_t* keys;        // workspace [units][L] (compact historical keys)
+};
+
+struct CssArgs {
+  Layout lay;
+  const uint16_t* k;
+  float* phi;
+  int32_t splits;        // work-groups per frame
+};
+
+struct SelectArgs {
+  Layout lay;
+  const float* a_base;
+  const float* phi;      // nullable
+  const uint8_t* gate;   // nullable
+  float alpha;
+  int32_t* kept;         // [units][total_budget]
+  float* score;          // nullable [units][L]
+  uint32_t* keys;        // workspace [units][L]
+};
+
+struct CompactArgs {
+  Layout lay;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* kept;
+  uint16_t* k_out;
+  uint16_t* v_out;
+};
+
+hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream);
+hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
+hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
+hipError_t launch_css(const CssArgs& a, hipStream_t stream);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Total order of fp32 values as unsigned integers (ascending key = ascending
+// value); -0 is folded onto +0 so that the two zeros tie.
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = __float_as_uint(x + 0.0f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float order_key_value(uint32_t key) {
+  uint32_t u = (key & 0x80000000u) ? (key & 0x7fffffffu) : ~key;
+  return __uint_as_float(u);
+}
+
+}  // namespace stlite

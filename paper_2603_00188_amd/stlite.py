@@ -1,0 +1,228 @@
+"""Python binding of libstlite (ctypes; argument marshalling only).
+
+Every function here forwards to the C entry point of the same name declared in
+include/stlite.h; all arithmetic runs in the library's gfx950 kernels.  PyTorch
+provides device memory and the stream.  There is no fallback: if the library
+is not built, ``load()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstlite.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD = range(6)
+
+EXPORTS = (
+    "stlite_abi_version", "stlite_status_string", "stlite_last_error", "stlite_budget",
+    "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
+    "stlite_tsg_gate", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
+)
+
+
+class StliteError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status}: {detail}")
+        self.status = status
+
+
+class _CProblem(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("n_seqs", ctypes.c_int32), ("n_frames", ctypes.c_int32),
+        ("window", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("total_tokens", ctypes.c_int64), ("total_budget", ctypes.c_int64),
+        ("cu_seqlens", ctypes.c_void_p), ("cu_frames", ctypes.c_void_p),
+        ("frame_meta", ctypes.c_void_p), ("cu_budget", ctypes.c_void_p),
+        ("h_cu_seqlens", ctypes.c_void_p), ("h_cu_frames", ctypes.c_void_p),
+        ("h_frame_meta", ctypes.c_void_p), ("h_cu_budget", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libstlite.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2603_00188_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(_CProblem)
+    vp, sz, i64, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int64, ctypes.c_float
+    st = ctypes.c_int
+    sig = {
+        "stlite_abi_version": (ctypes.c_int32, []),
+        "stlite_status_string": (ctypes.c_char_p, [st]),
+        "stlite_last_error": (ctypes.c_char_p, []),
+        "stlite_budget": (i64, [i64, i64, i64]),
+        "stlite_validate": (st, [P]),
+        "stlite_workspace_size": (st, [P, st, ctypes.POINTER(sz)]),
+        "stlite_score_window": (st, [P, vp, vp, vp, vp, sz, vp]),
+        "stlite_css_saliency": (st, [P, vp, vp, vp]),
+        "stlite_tsg_gate": (st, [P, vp, vp, vp, vp, vp, sz, vp]),
+        "stlite_tsg_threshold": (st, [P, vp, vp, vp, vp, sz, vp]),
+        "stlite_select_topk": (st, [P, vp, vp, vp, f32, vp, vp, vp, sz, vp]),
+        "stlite_compact_kv": (st, [P, vp, vp, vp, vp, vp, vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise StliteError(status, where, load().stlite_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+class Problem:
+    """An stlite_problem plus the host and device copies of its layout arrays."""
+
+    def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, window: int,
+                 cu_seqlens, cu_frames, frame_meta, cu_budget, head_dim: int = 128,
+                 device="cuda"):
+        import torch
+        self.h = {
+            "cu_seqlens": np.ascontiguousarray(cu_seqlens, dtype=np.int32),
+            "cu_frames": np.ascontiguousarray(cu_frames, dtype=np.int32),
+            "frame_meta": np.ascontiguousarray(np.asarray(frame_meta, dtype=np.int32).reshape(-1, 3)),
+            "cu_budget": np.ascontiguousarray(cu_budget, dtype=np.int32),
+        }
+        self.d = {k: torch.from_numpy(v.reshape(-1).copy()).to(device) for k, v in self.h.items()}
+        n_seqs = len(self.h["cu_seqlens"]) - 1
+        c = _CProblem()
+        c.n_layers, c.n_q_heads, c.n_kv_heads, c.head_dim = n_layers, n_q_heads, n_kv_heads, head_dim
+        c.n_seqs, c.n_frames, c.window, c.reserved = n_seqs, len(self.h["frame_meta"]), window, 0
+        c.total_tokens = int(self.h["cu_seqlens"][-1])
+        c.total_budget = int(self.h["cu_budget"][-1])
+        for k in self.h:
+            setattr(c, k, self.d[k].data_ptr() if self.d[k].numel() else None)
+            setattr(c, "h_" + k, self.h[k].ctypes.data if self.h[k].size else None)
+        self.c = c
+        self.n_layers, self.n_q_heads, self.n_kv_heads, self.window = n_layers, n_q_heads, n_kv_heads, window
+        self.n_seqs = n_seqs
+        self.total_tokens = c.total_tokens
+        self.total_budget = c.total_budget
+        self.units = n_layers * n_kv_heads
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+    def workspace_size(self, call: int) -> int:
+        n = ctypes.c_size_t(0)
+        _check(load().stlite_workspace_size(self.ref, call, ctypes.byref(n)), "stlite_workspace_size")
+        return n.value
+
+
+def budgets(cu_seqlens, beta_num: int, beta_den: int) -> np.ndarray:
+    """cu_budget prefix sums with B_s = stlite_budget(L_s, beta)."""
+    lib = load()
+    L = np.diff(np.asarray(cu_seqlens, dtype=np.int64))
+    B = [lib.stlite_budget(int(l), int(beta_num), int(beta_den)) for l in L]
+    if any(b < 0 for b in B):
+        raise ValueError("invalid budget ratio")
+    return np.concatenate([[0], np.cumsum(B)]).astype(np.int32)
+
+
+def stlite_budget(L: int, beta_num: int, beta_den: int) -> int:
+    return load().stlite_budget(L, beta_num, beta_den)
+
+
+def stlite_validate(p: Problem) -> None:
+    _check(load().stlite_validate(p.ref), "stlite_validate")
+
+
+def stlite_score_window(p: Problem, q_win, k, a_base, workspace, stream=None) -> None:
+    _check(load().stlite_score_window(p.ref, _ptr(q_win), _ptr(k), _ptr(a_base), _ptr(workspace),
+                                      _nbytes(workspace), _stream(stream)), "stlite_score_window")
+
+
+def stlite_css_saliency(p: Problem, k, phi, stream=None) -> None:
+    _check(load().stlite_css_saliency(p.ref, _ptr(k), _ptr(phi), _stream(stream)), "stlite_css_saliency")
+
+
+def stlite_tsg_gate(p: Problem, k, rho, tau, gate, workspace, stream=None) -> None:
+    _check(load().stlite_tsg_gate(p.ref, _ptr(k), _ptr(rho), _ptr(tau), _ptr(gate), _ptr(workspace),
+                                  _nbytes(workspace), _stream(stream)), "stlite_tsg_gate")
+
+
+def stlite_tsg_threshold(p: Problem, rho, tau, gate, workspace, stream=None) -> None:
+    _check(load().stlite_tsg_threshold(p.ref, _ptr(rho), _ptr(tau), _ptr(gate), _ptr(workspace),
+                                       _nbytes(workspace), _stream(stream)), "stlite_tsg_threshold")
+
+
+def stlite_select_topk(p: Problem, a_base, phi, gate, alpha: float, kept, score, workspace,
+                       stream=None) -> None:
+    _check(load().stlite_select_topk(p.ref, _ptr(a_base), _ptr(phi), _ptr(gate), float(alpha), _ptr(kept),
+                                     _ptr(score), _ptr(workspace), _nbytes(workspace), _stream(stream)),
+           "stlite_select_topk")
+
+
+def stlite_compact_kv(p: Problem, k, v, kept, k_out, v_out, stream=None) -> None:
+    _check(load().stlite_compact_kv(p.ref, _ptr(k), _ptr(v), _ptr(kept), _ptr(k_out), _ptr(v_out),
+                                    _stream(stream)), "stlite_compact_kv")
+
+
+class Buffers:
+    """Device outputs and workspaces for one problem (allocated once, reused)."""
+
+    def __init__(self, p: Problem, device="cuda", keep_stages: bool = True):
+        import torch
+        U, L, Bt = p.units, p.total_tokens, p.total_budget
+        f32 = dict(dtype=torch.float32, device=device)
+        self.a_base = torch.empty((U, L), **f32)
+        self.phi = torch.empty((U, L), **f32)
+        self.rho = torch.empty((U, L), **f32) if keep_stages else None
+        self.tau = torch.empty((U, p.n_seqs), **f32) if keep_stages else None
+        self.score = torch.empty((U, L), **f32) if keep_stages else None
+        self.gate = torch.empty((U, L), dtype=torch.uint8, device=device)
+        self.kept = torch.empty((U, max(Bt, 1)), dtype=torch.int32, device=device)
+        self.k_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
+        self.v_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
+        ws = max(p.workspace_size(c) for c in range(6))
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+
+
+def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: bool = True,
+             tsg: bool = True, stream=None) -> Buffers:
+    """The whole pass: score, gate, saliency, select, compact (five C calls)."""
+    stlite_score_window(p, q_win, k, out.a_base, out.ws, stream)
+    if tsg:
+        stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws, stream)
+    if css:
+        stlite_css_saliency(p, k, out.phi, stream)
+    stlite_select_topk(p, out.a_base, out.phi if css else None, out.gate if tsg else None, alpha,
+                       out.kept, out.score, out.ws, stream)
+    stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, stream)
+    return out

@@ -1,0 +1,149 @@
+"""Host side of the C ABI, without a GPU: the library loads, exports every
+function include/stlite.h declares, computes budgets exactly, and rejects
+malformed problems before anything is launched."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2603_00188_amd import stlite as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "stlite.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(S.LIB_PATH), reason="libstlite.so not built")
+
+FAKE_DEV = 0x100000  # never dereferenced: validation reads only the host mirrors
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(stlite_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_match_header():
+    lib = S.load()
+    names = declared_functions()
+    assert set(names) == set(S.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.stlite_abi_version() == 1
+
+
+def test_budget_exact():
+    lib = S.load()
+    assert lib.stlite_budget(2592, 76, 100) == 1969
+    assert lib.stlite_budget(100, 29, 100) == 29
+    assert lib.stlite_budget(150528, 1, 5) == 30105
+    assert lib.stlite_budget(62720, 2, 5) == 25088
+    assert lib.stlite_budget(7, 1, 1) == 7
+    assert lib.stlite_budget(0, 1, 5) == 0
+    assert lib.stlite_budget(10, 3, 2) == -1
+    assert lib.stlite_budget(10, 0, 2) == -1
+    assert lib.stlite_budget(-1, 1, 2) == -1
+    big = 2 ** 40
+    assert lib.stlite_budget(big, 2 ** 30 - 1, 2 ** 30) == (big * (2 ** 30 - 1)) // 2 ** 30
+
+
+class HostProblem:
+    """A _CProblem whose host mirrors are real and whose device pointers are fake."""
+
+    def __init__(self, cu_seqlens, frames_per_seq, budgets, n_layers=2, n_q_heads=28, n_kv_heads=4,
+                 window=8, head_dim=128):
+        self.cu_seqlens = np.asarray(cu_seqlens, np.int32)
+        self.cu_frames = np.asarray(np.concatenate([[0], np.cumsum([len(f) for f in frames_per_seq])]), np.int32)
+        fm = [x for f in frames_per_seq for x in f]
+        self.frame_meta = np.asarray(fm, np.int32).reshape(-1, 3) if fm else np.zeros((0, 3), np.int32)
+        self.cu_budget = np.asarray(np.concatenate([[0], np.cumsum(budgets)]), np.int32)
+        c = S._CProblem()
+        c.n_layers, c.n_q_heads, c.n_kv_heads, c.head_dim = n_layers, n_q_heads, n_kv_heads, head_dim
+        c.n_seqs, c.n_frames, c.window, c.reserved = len(cu_seqlens) - 1, len(fm), window, 0
+        c.total_tokens = int(self.cu_seqlens[-1])
+        c.total_budget = int(self.cu_budget[-1])
+        c.cu_seqlens = c.cu_frames = c.cu_budget = FAKE_DEV
+        c.frame_meta = FAKE_DEV if fm else None
+        c.h_cu_seqlens = self.cu_seqlens.ctypes.data
+        c.h_cu_frames = self.cu_frames.ctypes.data
+        c.h_frame_meta = self.frame_meta.ctypes.data if fm else None
+        c.h_cu_budget = self.cu_budget.ctypes.data
+        self.c = c
+
+    def validate(self):
+        return S.load().stlite_validate(ctypes.byref(self.c))
+
+
+def good():
+    # two sequences: [frame 4x5 | 10 text | frame 4x5 | 12 text], [30 text]
+    return HostProblem([0, 72, 102], [[(0, 4, 5), (30, 4, 5)], []], [14, 6])
+
+
+def test_valid_problem_and_workspace_sizes():
+    p = good()
+    assert p.validate() == S.OK, S.load().stlite_last_error()
+    lib = S.load()
+    n = ctypes.c_size_t(0)
+    for call in range(6):
+        assert lib.stlite_workspace_size(ctypes.byref(p.c), call, ctypes.byref(n)) == S.OK
+        if call in (S.CALL_CSS_SALIENCY, S.CALL_COMPACT_KV):
+            assert n.value == 0
+        else:
+            assert n.value > 0 and n.value % 256 == 0
+    assert lib.stlite_workspace_size(ctypes.byref(p.c), 17, ctypes.byref(n)) == S.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("mutate, status, text", [
+    (lambda p: setattr(p.c, "head_dim", 64), S.ERR_UNSUPPORTED, "head_dim"),
+    (lambda p: setattr(p.c, "n_q_heads", 30), S.ERR_INVALID_ARG, "multiple"),
+    (lambda p: setattr(p.c, "window", 0), S.ERR_INVALID_ARG, "window"),
+    (lambda p: setattr(p.c, "window", 31), S.ERR_INVALID_ARG, "fewer than the window"),
+    (lambda p: setattr(p.c, "window", 80), S.ERR_UNSUPPORTED, "G * window"),
+    (lambda p: setattr(p.c, "reserved", 1), S.ERR_INVALID_ARG, "reserved"),
+    (lambda p: setattr(p.c, "total_tokens", 103), S.ERR_INVALID_ARG, "total_tokens"),
+    (lambda p: setattr(p.c, "total_budget", 19), S.ERR_INVALID_ARG, "total_budget"),
+    (lambda p: setattr(p.c, "cu_seqlens", None), S.ERR_INVALID_ARG, "device"),
+    (lambda p: setattr(p.c, "h_cu_budget", None), S.ERR_INVALID_ARG, "host"),
+    (lambda p: p.frame_meta.__setitem__((1, 0), 10), S.ERR_INVALID_ARG, "overlaps"),
+    (lambda p: p.frame_meta.__setitem__((1, 1), 9), S.ERR_INVALID_ARG, "leaves sequence"),
+    (lambda p: p.frame_meta.__setitem__((0, 2), 0), S.ERR_INVALID_ARG, "empty grid"),
+    (lambda p: p.cu_budget.__setitem__(1, 80), S.ERR_INVALID_ARG, "budget"),
+    (lambda p: p.cu_frames.__setitem__(2, 1), S.ERR_INVALID_ARG, "cu_frames"),
+])
+def test_validation_rejects(mutate, status, text):
+    p = good()
+    mutate(p)
+    assert p.validate() == status
+    assert text in S.load().stlite_last_error().decode()
+
+
+def test_calls_fail_before_launch():
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    # workspace missing / too small: nothing is enqueued, no GPU is touched
+    assert lib.stlite_score_window(ref, FAKE_DEV, FAKE_DEV, FAKE_DEV, None, 0, None) == S.ERR_WORKSPACE
+    assert lib.stlite_select_topk(ref, FAKE_DEV, None, None, 1.0, FAKE_DEV, None, FAKE_DEV, 16,
+                                  None) == S.ERR_WORKSPACE
+    n = ctypes.c_size_t(0)
+    lib.stlite_workspace_size(ref, S.CALL_SELECT_TOPK, ctypes.byref(n))
+    assert lib.stlite_select_topk(ref, FAKE_DEV, None, None, -1.0, FAKE_DEV, None, FAKE_DEV, n.value,
+                                  None) == S.ERR_INVALID_ARG
+    assert lib.stlite_select_topk(ref, FAKE_DEV, None, None, float("nan"), FAKE_DEV, None, FAKE_DEV,
+                                  n.value, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_css_saliency(ref, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_compact_kv(ref, FAKE_DEV + 8, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                 None) == S.ERR_INVALID_ARG
+    assert lib.stlite_tsg_gate(ref, FAKE_DEV, None, None, None, None, 0, None) == S.ERR_WORKSPACE
+    p.c.head_dim = 96
+    assert lib.stlite_css_saliency(ref, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
+    assert lib.stlite_status_string(S.ERR_HIP) == b"STLITE_ERR_HIP"
+
+
+def test_budgets_helper_matches_oracle():
+    from oracle import stlite_oracle as O
+    cu = np.array([0, 912, 4304, 5000])
+    got = S.budgets(cu, 1, 5)
+    want = np.concatenate([[0], np.cumsum([O.budget(int(l), 1, 5) for l in np.diff(cu)])])
+    assert got.tolist() == want.tolist()
