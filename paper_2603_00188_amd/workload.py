@@ -368,12 +368,27 @@ def make_layer(w: Workload, scene: Scene, layer: int) -> LayerInputs:
     return LayerInputs(to_bf16_bits(k32), v, to_bf16_bits(q32))
 
 
-def make_inputs(w: Workload, layers: Optional[Sequence[int]] = None):
-    """All layers (or the listed ones) stacked: K, V [nl, Hkv, L, d], Q [nl, S, Hq, win, d]."""
+def make_inputs(w: Workload, layers: Optional[Sequence[int]] = None, workers: int = 8):
+    """All layers (or the listed ones) stacked: K, V [nl, Hkv, L, d], Q [nl, S, Hq, win, d].
+
+    Layers are drawn in parallel threads; every layer has its own random stream,
+    so the result does not depend on ``workers``."""
     scene = make_scene(w)
     layers = list(range(w.n_layers)) if layers is None else list(layers)
-    per = [make_layer(w, scene, l) for l in layers]
-    k = np.stack([p.k for p in per])
-    v = np.stack([p.v for p in per])
-    q = np.stack([p.q for p in per])
+    L = scene.layout.total_tokens
+    k = np.empty((len(layers), w.n_kv_heads, L, w.head_dim), np.uint16)
+    v = np.empty_like(k)
+    q = np.empty((len(layers), scene.layout.n_seqs, w.n_q_heads, w.window, w.head_dim), np.uint16)
+
+    def one(i):
+        p = make_layer(w, scene, layers[i])
+        k[i], v[i], q[i] = p.k, p.v, p.q
+
+    if workers > 1 and len(layers) > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(min(workers, len(layers))) as ex:
+            list(ex.map(one, range(len(layers))))
+    else:
+        for i in range(len(layers)):
+            one(i)
     return scene, k, v, q
