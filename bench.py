@@ -1,0 +1,234 @@
+"""Benchmark of the ST-Lite KV-cache compression pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+
+One step is the whole pass -- stlite_score_window, stlite_tsg_gate,
+stlite_css_saliency, stlite_select_topk, stlite_compact_kv -- over every layer
+and kv head of one synthetic batch that is resident in HBM before timing
+starts.  The default workload is the 50-step GUI trajectory: 48 frames of
+36 x 80 patches, each followed by 256 text tokens (150,528 tokens), 28 layers,
+28 query / 4 kv heads, head_dim 128, window 64, beta = 1/5.
+
+Prints ONE JSON line on stdout.  ``value`` is cached tokens compressed per
+second over all layers (tokens / step time).  ``roofline`` describes the call
+that takes the largest share of the step, timed with HIP events recorded on
+the stream the calls are launched on, inside the timed loop.  ``cpu_baseline``
+times the fp64 oracle on a bounded sample of the same workload on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "cached KV tokens compressed/sec (all layers) at β=20%; % MFMA peak, HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg):
+    sys.stderr.write(f"[bench {time.strftime('%H:%M:%S')}] {msg}\n")
+    sys.stderr.flush()
+
+
+def work_model(w, lay, cu_budget):
+    """Algorithmic work per call of one step (all units): FLOPs and HBM bytes."""
+    units = w.n_layers * w.n_kv_heads
+    d = w.head_dim
+    rows = w.group * w.window
+    L_tot = lay.total_tokens
+    n_hist = n_cur = n_vis = 0
+    for s in range(lay.n_seqs):
+        fm = lay.seq_frames(s)
+        sizes = [int(r) * int(c) for _, r, c in fm]
+        n_vis += sum(sizes)
+        if sizes:
+            n_cur_s = sizes[-1]
+            n_hist_s = sum(sizes[:-1])
+            n_hist += n_hist_s
+            n_cur += n_cur_s * (1 if n_hist_s else 0)
+    hist_cur = 0
+    for s in range(lay.n_seqs):
+        sizes = [int(r) * int(c) for _, r, c in lay.seq_frames(s)]
+        if len(sizes) > 1:
+            hist_cur += sum(sizes[:-1]) * sizes[-1]
+    B_tot = int(cu_budget[-1])
+    return {
+        # QK^T of the window rows against every key, once (the pass forms it twice)
+        "score_window": {"bound": "mfma", "flops": units * 2.0 * rows * L_tot * d,
+                         "bytes": units * (2.0 * L_tot * d * 2 + 4.0 * L_tot)},
+        "tsg_gate": {"bound": "mfma", "flops": units * 2.0 * hist_cur * d,
+                     "bytes": units * (2.0 * (n_hist + n_cur) * d + 4.0 * L_tot + 1.0 * L_tot)},
+        "css_saliency": {"bound": "hbm", "flops": units * 2.0 * 5 * n_vis * d,
+                         "bytes": units * (2.0 * n_vis * d + 4.0 * L_tot)},
+        "select_topk": {"bound": "hbm", "flops": 0.0,
+                        "bytes": units * (9.0 * L_tot + 4.0 * B_tot)},
+        "compact_kv": {"bound": "hbm", "flops": 0.0,
+                       "bytes": units * 4.0 * B_tot * d * 2},
+    }
+
+
+def roofline_entry(model, ms):
+    s = ms * 1e-3
+    if model["bound"] == "mfma":
+        ach = model["flops"] / s / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_BF16_TFLOPS, 4), "ms": round(ms, 4)}
+    ach = model["bytes"] / s / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4), "ms": round(ms, 4)}
+
+
+def cpu_baseline(w, case_inputs, budget_s=12.0, max_units=8):
+    """Time the fp64 oracle on whole (layer, kv head) units until ~budget_s."""
+    from oracle import stlite_oracle as O
+    scene, k, v, q = case_inputs
+    lay = scene.layout
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    units_all = [(l, h) for l in range(w.n_layers) for h in range(w.n_kv_heads)]
+    rng = np.random.default_rng(0)
+    order = rng.permutation(len(units_all))
+    done, t_total = 0, 0.0
+    for i in order[:max_units]:
+        l, h = units_all[i]
+        t0 = time.perf_counter()
+        for s in range(lay.n_seqs):
+            O.compress_sequence(q, k, v, lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s, l, h, w.group,
+                                w.beta, w.alpha)
+        t_total += time.perf_counter() - t0
+        done += 1
+        log(f"cpu baseline: unit ({l},{h}) done, {t_total:.1f} s so far")
+        if t_total >= budget_s:
+            break
+    per_unit = t_total / done
+    rate = lay.total_tokens / (per_unit * len(units_all))
+    return {"value": round(rate, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{done} of {len(units_all)} (layer, kv head) units of the full workload, "
+                      f"every sequence, fp64 NumPy oracle; rate scaled to all {len(units_all)} units "
+                      f"({t_total:.1f} s measured)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        sys.stderr.write("bench.py measures one GPU only: the compression pass is per (layer, kv head) and "
+                         "this build runs it on a single MI355X; --gpus must be 1\n")
+        sys.exit(2)
+
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    from paper_2603_00188_amd import workload as W
+
+    S.load()  # fails loudly without the HIP library
+    torch.cuda.set_device(0)
+    w = W.config(args.config)
+    log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
+    inputs = W.make_inputs(w, workers=16)
+    scene, k, v, q = inputs
+    lay = scene.layout
+    cu_budget = S.budgets(lay.cu_seqlens, *w.beta)
+    prob = S.Problem(w.n_layers, w.n_q_heads, w.n_kv_heads, w.window, lay.cu_seqlens, lay.cu_frames,
+                     lay.frame_meta, cu_budget)
+    dk = torch.from_numpy(k.view(np.int16)).cuda()
+    dv = torch.from_numpy(v.view(np.int16)).cuda()
+    dq = torch.from_numpy(q.view(np.int16)).cuda()
+    out = S.Buffers(prob, keep_stages=False)
+    torch.cuda.synchronize()
+    log(f"inputs resident: K+V {2 * dk.numel() * 2 / 1e9:.2f} GB")
+
+    stream = torch.cuda.current_stream()
+    names = ["score_window", "tsg_gate", "css_saliency", "select_topk", "compact_kv"]
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        S.stlite_score_window(prob, dq, dk, out.a_base, out.ws, stream)
+        if ev: ev[1].record(stream)
+        S.stlite_tsg_gate(prob, dk, None, None, out.gate, out.ws, stream)
+        if ev: ev[2].record(stream)
+        S.stlite_css_saliency(prob, dk, out.phi, stream)
+        if ev: ev[3].record(stream)
+        S.stlite_select_topk(prob, out.a_base, out.phi, out.gate, w.alpha, out.kept, None, out.ws, stream)
+        if ev: ev[4].record(stream)
+        S.stlite_compact_kv(prob, dk, dv, out.kept, out.k_out, out.v_out, stream)
+        if ev: ev[5].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    per_call = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
+    log(f"step {ms_step:.3f} ms; calls: " + ", ".join(f"{n} {t:.3f}" for n, t in per_call.items()))
+
+    model = work_model(w, lay, cu_budget)
+    stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
+    dom = max(names, key=lambda n: per_call[n])
+    kernel_of = {"score_window": "score_rowstats + score_colsum (two MFMA passes)",
+                 "tsg_gate": "rho_kernel (+ cur_norms, gate_kernel in the same call)",
+                 "css_saliency": "css_kernel", "select_topk": "select_kernel", "compact_kv": "compact_kernel"}
+    roof = dict(stages[dom])
+    roof.pop("ms")
+    roof["traffic"] = None
+    roof["kernel"] = kernel_of[dom]
+    roof["call"] = "stlite_" + dom
+    roof["ms_per_launch"] = round(per_call[dom], 4)
+
+    result = {
+        "metric": METRIC,
+        "value": round(lay.total_tokens / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: {lay.n_seqs} sequence(s), {len(lay.frame_meta)} frames of "
+                        f"36x80 patches + text, {lay.total_tokens} tokens, {w.n_layers} layers, "
+                        f"{w.n_q_heads}/{w.n_kv_heads} heads, head_dim {w.head_dim}, window {w.window}, "
+                        f"beta {w.beta[0]}/{w.beta[1]}, alpha {w.alpha}",
+            "tokens": lay.total_tokens, "layers": w.n_layers, "kv_heads": w.n_kv_heads,
+            "q_heads": w.n_q_heads, "window": w.window, "beta": f"{w.beta[0]}/{w.beta[1]}",
+            "budget_per_unit": int(cu_budget[-1]),
+        },
+        "roofline": roof,
+        "stages": stages,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host (cpu baseline)")
+        result["cpu_baseline"] = cpu_baseline(w, inputs)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
