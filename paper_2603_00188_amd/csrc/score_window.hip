@@ -8,8 +8,8 @@
 //   combine            per row: log2 of the softmax denominator over all chunks,
 //   pass 2  (colsum)   per key chunk: 2^(x - lse) summed over the G*window rows.
 // Both passes keep the whole GQA group's window queries resident in VGPRs as
-// the MFMA A operand (each wave owns row_blocks 16-row blocks) and stream
-// 64-key tiles of K through LDS as the B operand, shared by all waves.
+// the MFMA A operand (up to 8 waves, each owning up to four 16-row blocks) and
+// stream 64-key tiles of K through LDS as the B operand, shared by all waves.
 // Logits are kept in log2 units: x = (q . k) * log2(e) / sqrt(d).
 #include "stlite_internal.h"
 
@@ -45,29 +45,48 @@ __device__ inline ChunkPos locate_chunk(const Layout& lay, int32_t chunk, int32_
   return r;
 }
 
-// Stage keys [t0, t0+64) of one sequence (local indices, zero past `end`) into LDS.
-__device__ inline void stage_keys(uint16_t* ks, const uint16_t* kseq, int32_t t0, int32_t end) {
-  const int nthreads = blockDim.x;
-  for (int i = threadIdx.x; i < kTileKeys * 16; i += nthreads) {
-    const int key = i >> 4, part = i & 15;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t0 + key < end)
-      v = *reinterpret_cast<const uint4*>(kseq + size_t(t0 + key) * kHeadDim + part * 8);
-    *reinterpret_cast<uint4*>(ks + key * kKStride + part * 8) = v;
-  }
-}
-
 __device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-template <int RB>
+// Register-prefetched staging of 64-key tiles into LDS: fetch() issues the
+// global loads of the next tile before the current one is consumed, stage()
+// writes them to the other LDS buffer afterwards.  Keys past `end` are zero.
+template <int NW>
+struct KeyStager {
+  static constexpr int kThreads = NW * 64;
+  static constexpr int kPer = kTileKeys * 16 / kThreads;
+  uint4 pre[kPer];
+  __device__ inline void fetch(const uint16_t* kseq, int32_t t0, int32_t end) {
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = threadIdx.x + r * kThreads;
+      const int32_t j = t0 + (i >> 4);
+      pre[r] = j < end ? *reinterpret_cast<const uint4*>(kseq + size_t(j) * kHeadDim + (i & 15) * 8)
+                       : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ inline void stage(uint16_t* ks) const {
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = threadIdx.x + r * kThreads;
+      *reinterpret_cast<uint4*>(ks + (i >> 4) * kKStride + (i & 15) * 8) = pre[r];
+    }
+  }
+};
+
+// Row blocks are dealt to waves round-robin (wave w owns blocks w, w + NW, ...),
+// so that each SIMD of the CU gets the same number of real 16-row blocks.
+template <int NW>
+__device__ inline int block_of(int j) { return (threadIdx.x >> 6) + j * NW; }
+
+template <int RB, int NW>
 __device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int unit, bf16x8_t (&qa)[RB][4]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   const int layer = unit / a.lay.n_kv_heads, kv = unit % a.lay.n_kv_heads;
   const uint16_t* qbase =
       a.q + ((size_t(layer) * a.lay.n_seqs + cp.seq) * a.n_q_heads + size_t(kv) * a.group) * a.window * kHeadDim;
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
-    const int row = (wave * RB + b) * 16 + (lane & 15);
+    const int row = block_of<NW>(b) * 16 + (lane & 15);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -78,79 +97,120 @@ __device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int 
   }
 }
 
+__device__ inline void read_b_operand(const uint16_t* ks, bf16x8_t (&kb)[4][4]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      kb[t][kk] = *reinterpret_cast<const bf16x8_t*>(ks + (t * 16 + (lane & 15)) * kKStride + kk * 32 +
+                                                      (lane >> 4) * 8);
+}
+
+// Q K^T of one 64-key tile for row block b: four 16x16 accumulators (one per
+// 16-key sub-tile); the four MFMA chains are interleaved k-step by k-step.
 template <int RB>
-__global__ __launch_bounds__(256) void score_rowstats_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[kTileKeys * kKStride];
+__device__ inline void tile_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[4][4], int b, f32x4_t (&acc)[4]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
+}
+
+// Last key (local index) a lane's output row i of block b may see, -1 for padding rows.
+template <int NW>
+__device__ inline int32_t row_limit(const ScoreArgs& a, const ChunkPos& cp, int b, int i) {
+  const int lane = threadIdx.x & 63;
+  const int r = block_of<NW>(b) * 16 + (lane >> 4) * 4 + i;
+  return r < a.rows ? cp.seq_len - a.window + (r % a.window) : -1;
+}
+
+// Pass 1 on one tile.  Per lane and window row: running max m of the raw
+// logits (q.k units) and sum of 2^((x - m) s), s = log2(e)/sqrt(d), updated
+// once per tile from the four values the lane holds for that row.
+template <int RB, int NW, bool MASK>
+__device__ inline void rowstats_tile(const ScoreArgs& a, const ChunkPos& cp, int32_t t0, const bf16x8_t (&qa)[RB][4],
+                                     const bf16x8_t (&kb)[4][4], float (&m)[RB][4], float (&sum)[RB][4]) {
+  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    if (block_of<NW>(b) >= a.blocks) break;  // wave-uniform: padding blocks do no work
+    f32x4_t acc[4];
+    tile_logits<RB>(qa, kb, b, acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) v[t] = acc[t][i];
+      if (MASK) {
+        const int32_t lim = min(row_limit<NW>(a, cp, b, i), cp.c1 - 1);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (t0 + t * 16 + (lane & 15) > lim) v[t] = -INFINITY;
+      }
+      const float mx = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(m[b][i], v[0]), v[1]),
+                                       __builtin_fmaxf(v[2], v[3]));
+      const float ms = mx * scale2;
+      float sacc = sum[b][i] * __builtin_amdgcn_exp2f(fmaf(m[b][i], scale2, -ms));
+#pragma unroll
+      for (int t = 0; t < 4; ++t) sacc += __builtin_amdgcn_exp2f(fmaf(v[t], scale2, -ms));
+      sum[b][i] = sacc;
+      m[b][i] = mx;
+    }
+  }
+}
+
+template <int RB, int NW>
+__global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kTileKeys * kKStride];
   const int unit = blockIdx.y;
   const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
   if (cp.seq < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+  const int lane = threadIdx.x & 63;
+  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;
 
   bf16x8_t qa[RB][4];
-  load_queries<RB>(a, cp, unit, qa);
-
-  int32_t pos[RB][4];  // last visible key (local index) of each of the lane's output rows
+  load_queries<RB, NW>(a, cp, unit, qa);
   float m[RB][4], sum[RB][4];
 #pragma unroll
   for (int b = 0; b < RB; ++b)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = (wave * RB + b) * 16 + (lane >> 4) * 4 + i;
-      pos[b][i] = r < a.rows ? cp.seq_len - a.window + (r % a.window) : -1;
       m[b][i] = kNegBig;
       sum[b][i] = 0.0f;
     }
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  // Tiles that end before the window starts are visible to every row: no mask.
+  const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
+  KeyStager<NW> st;
+  st.fetch(kseq, cp.c0, cp.c1);
+  st.stage(ks[0]);
+  __syncthreads();
+  int buf = 0;
   for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
-    __syncthreads();
-    stage_keys(ks, kseq, t0, cp.c1);
-    __syncthreads();
+    const bool more = t0 + kTileKeys < cp.c1;
+    if (more) st.fetch(kseq, t0 + kTileKeys, cp.c1);
     bf16x8_t kb[4][4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        kb[t][kk] = *reinterpret_cast<const bf16x8_t*>(ks + (t * 16 + (lane & 15)) * kKStride + kk * 32 +
-                                                        (lane >> 4) * 8);
-    const bool clean = (t0 + kTileKeys <= cp.c1) && (t0 + kTileKeys - 1 <= cp.seq_len - a.window);
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      f32x4_t acc[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          v[t] = acc[t][i] * scale2;
-          if (!clean) {
-            const int32_t j = t0 + t * 16 + (lane & 15);
-            if (j >= cp.c1 || j > pos[b][i]) v[t] = -INFINITY;
-          }
-        }
-        const float mx = fmaxf(fmaxf(fmaxf(m[b][i], v[0]), fmaxf(v[1], v[2])), v[3]);
-        sum[b][i] = sum[b][i] * __builtin_amdgcn_exp2f(m[b][i] - mx) + __builtin_amdgcn_exp2f(v[0] - mx) +
-                    __builtin_amdgcn_exp2f(v[1] - mx) + __builtin_amdgcn_exp2f(v[2] - mx) +
-                    __builtin_amdgcn_exp2f(v[3] - mx);
-        m[b][i] = mx;
-      }
-    }
+    read_b_operand(ks[buf], kb);
+    if (t0 + kTileKeys <= clean_end)
+      rowstats_tile<RB, NW, false>(a, cp, t0, qa, kb, m, sum);
+    else
+      rowstats_tile<RB, NW, true>(a, cp, t0, qa, kb, m, sum);
+    if (more) st.stage(ks[buf ^ 1]);
+    __syncthreads();
+    buf ^= 1;
   }
 
-  // Merge the 16 lanes that hold the same rows (different key columns).
+  // Merge the 16 lanes that hold the same rows (different key columns); log2 units.
 #pragma unroll
   for (int b = 0; b < RB; ++b)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float mm = m[b][i], ss = sum[b][i];
+      float mm = m[b][i] * scale2, ss = sum[b][i];
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) {
         const float mo = __shfl_xor(mm, off);
@@ -160,7 +220,7 @@ __global__ __launch_bounds__(256) void score_rowstats_kernel(ScoreArgs a) {
         mm = mx;
       }
       if ((lane & 15) == 0) {
-        const int r = (wave * RB + b) * 16 + (lane >> 4) * 4 + i;
+        const int r = block_of<NW>(b) * 16 + (lane >> 4) * 4 + i;
         a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(mm, ss);
       }
     }
@@ -192,70 +252,72 @@ __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
   }
 }
 
-template <int RB>
-__global__ __launch_bounds__(256) void score_colsum_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[kTileKeys * kKStride];
-  __shared__ float red[4][kTileKeys];
+// Pass 2 on one tile: col[t] += 2^(x s - lse) over the lane's rows, for the
+// lane's key column of sub-tile t.
+template <int RB, int NW, bool MASK>
+__device__ inline void colsum_tile(const ScoreArgs& a, const ChunkPos& cp, int32_t t0, const bf16x8_t (&qa)[RB][4],
+                                   const bf16x8_t (&kb)[4][4], const float (&lse)[RB][4], float (&col)[4]) {
+  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    if (block_of<NW>(b) >= a.blocks) break;  // wave-uniform: padding blocks do no work
+    f32x4_t acc[4];
+    tile_logits<RB>(qa, kb, b, acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int32_t lim = 0;
+      if (MASK) lim = min(row_limit<NW>(a, cp, b, i), cp.c1 - 1);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float p = __builtin_amdgcn_exp2f(fmaf(acc[t][i], scale2, -lse[b][i]));
+        if (MASK && t0 + t * 16 + (lane & 15) > lim) p = 0.0f;
+        col[t] += p;
+      }
+    }
+  }
+}
+
+// Pass 2.  A_j = (1/G) sum over rows of 2^(x_rj - lse_r): the lane's four
+// rows per block are summed in registers, then across the four lane groups
+// that share a key column, then across waves in LDS.
+template <int RB, int NW>
+__global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kTileKeys * kKStride];
+  __shared__ float red[2][NW][kTileKeys];  // per LDS buffer: no barrier between read and next write
   const int unit = blockIdx.y;
   const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
   if (cp.seq < 0) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
-  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;
   const float inv_g = 1.0f / float(a.group);
 
   bf16x8_t qa[RB][4];
-  load_queries<RB>(a, cp, unit, qa);
-
-  int32_t pos[RB][4];
+  load_queries<RB, NW>(a, cp, unit, qa);
   float lse[RB][4];
   const float* lrow = a.lse2 + (size_t(unit) * a.lay.n_seqs + cp.seq) * a.rows_pad;
 #pragma unroll
   for (int b = 0; b < RB; ++b)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (wave * RB + b) * 16 + (lane >> 4) * 4 + i;
-      pos[b][i] = r < a.rows ? cp.seq_len - a.window + (r % a.window) : -1;
-      lse[b][i] = lrow[r];
-    }
+    for (int i = 0; i < 4; ++i) lse[b][i] = lrow[block_of<NW>(b) * 16 + (lane >> 4) * 4 + i];
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
   float* aout = a.a_base + size_t(unit) * a.lay.total_tokens + cp.seq_start;
+  const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
+  KeyStager<NW> st;
+  st.fetch(kseq, cp.c0, cp.c1);
+  st.stage(ks[0]);
+  __syncthreads();
+  int buf = 0;
   for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
-    __syncthreads();
-    stage_keys(ks, kseq, t0, cp.c1);
-    __syncthreads();
+    const bool more = t0 + kTileKeys < cp.c1;
+    if (more) st.fetch(kseq, t0 + kTileKeys, cp.c1);
     bf16x8_t kb[4][4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        kb[t][kk] = *reinterpret_cast<const bf16x8_t*>(ks + (t * 16 + (lane & 15)) * kKStride + kk * 32 +
-                                                        (lane >> 4) * 8);
-    const bool clean = (t0 + kTileKeys <= cp.c1) && (t0 + kTileKeys - 1 <= cp.seq_len - a.window);
+    read_b_operand(ks[buf], kb);
     float col[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      f32x4_t acc[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          float p = __builtin_amdgcn_exp2f(acc[t][i] * scale2 - lse[b][i]);
-          if (!clean) {
-            const int32_t j = t0 + t * 16 + (lane & 15);
-            if (j >= cp.c1 || j > pos[b][i]) p = 0.0f;
-          }
-          col[t] += p;
-        }
-    }
+    if (t0 + kTileKeys <= clean_end)
+      colsum_tile<RB, NW, false>(a, cp, t0, qa, kb, lse, col);
+    else
+      colsum_tile<RB, NW, true>(a, cp, t0, qa, kb, lse, col);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       col[t] += __shfl_xor(col[t], 16);
@@ -263,45 +325,54 @@ __global__ __launch_bounds__(256) void score_colsum_kernel(ScoreArgs a) {
     }
     if (lane < 16) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) red[wave][t * 16 + lane] = col[t];
+      for (int t = 0; t < 4; ++t) red[buf][wave][t * 16 + lane] = col[t];
     }
+    if (more) st.stage(ks[buf ^ 1]);
     __syncthreads();
     if (threadIdx.x < kTileKeys) {
       float s = 0.0f;
-      for (int w = 0; w < nwaves; ++w) s += red[w][threadIdx.x];
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[buf][w][threadIdx.x];
       const int32_t j = t0 + threadIdx.x;
       if (j < cp.c1) aout[j] = s * inv_g;
     }
+    buf ^= 1;
   }
 }
 
-template <int RB>
+template <int RB, int NW>
 hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   const dim3 grid(a.total_chunks, a.lay.n_units);
-  const dim3 block(64 * a.waves);
-  hipLaunchKernelGGL(score_rowstats_kernel<RB>, grid, block, 0, stream, a);
+  const dim3 block(64 * NW);
+  hipLaunchKernelGGL((score_rowstats_kernel<RB, NW>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(score_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(score_colsum_kernel<RB>, grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_colsum_kernel<RB, NW>), grid, block, 0, stream, a);
   return hipGetLastError();
+}
+
+template <int NW>
+hipError_t launch_nw(const ScoreArgs& a, hipStream_t stream) {
+  switch (a.row_blocks) {
+    case 1: return launch_rb<1, NW>(a, stream);
+    case 2: return launch_rb<2, NW>(a, stream);
+    case 3: return launch_rb<3, NW>(a, stream);
+    case 4: return launch_rb<4, NW>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
 
 hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream) {
-  if (a.waves < 1 || a.waves > 4) return hipErrorInvalidValue;
-  switch (a.row_blocks) {
-    case 1: return launch_rb<1>(a, stream);
-    case 2: return launch_rb<2>(a, stream);
-    case 3: return launch_rb<3>(a, stream);
-    case 4: return launch_rb<4>(a, stream);
-    case 5: return launch_rb<5>(a, stream);
-    case 6: return launch_rb<6>(a, stream);
-    case 7: return launch_rb<7>(a, stream);
-    case 8: return launch_rb<8>(a, stream);
+  switch (a.waves) {
+    case 1: return launch_nw<1>(a, stream);
+    case 2: return launch_nw<2>(a, stream);
+    case 4: return launch_nw<4>(a, stream);
+    case 8: return launch_nw<8>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }

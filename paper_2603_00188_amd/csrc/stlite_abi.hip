@@ -39,7 +39,7 @@ struct Facts {
   int64_t max_seq;
   int64_t total_hist_blocks;
   int64_t max_cur;
-  int32_t rows, rows_pad, waves, row_blocks, chunk;
+  int32_t rows, rows_pad, blocks, waves, row_blocks, chunk;
   int64_t total_chunks;
 };
 
@@ -49,7 +49,10 @@ Facts derive(const stlite_problem* p) {
   const int32_t G = p->n_q_heads / p->n_kv_heads;
   f.rows = G * p->window;
   const int nb = (f.rows + 15) / 16;
-  f.waves = (nb + 7) / 8;  // <= 4 waves of <= 8 resident 16-row blocks
+  // 1, 2, 4 or 8 waves, each holding at most four resident 16-row blocks.
+  f.blocks = nb;
+  f.waves = 1;
+  while (f.waves * 4 < nb) f.waves *= 2;
   f.row_blocks = (nb + f.waves - 1) / f.waves;
   f.rows_pad = f.waves * f.row_blocks * 16;
   // Key chunk per work-group: aim for >= 2048 work-groups so that all 256 CUs
@@ -208,7 +211,9 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
                align_up(size_t(f.units) * p->n_seqs * f.rows_pad * sizeof(float));
       break;
     case STLITE_CALL_TSG_GATE:
-      *bytes = 3 * align_up(per_token * sizeof(float));  // rho scratch, current-frame norms, keys
+      // rho scratch, current-frame norms, gate keys, historical-token table, block table
+      *bytes = 3 * align_up(per_token * sizeof(float)) + align_up(size_t(p->total_tokens) * sizeof(int32_t)) +
+               align_up(size_t(f.total_hist_blocks) * sizeof(HistBlock));
       break;
     case STLITE_CALL_TSG_THRESHOLD:
     case STLITE_CALL_SELECT_TOPK:
@@ -244,6 +249,7 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
   a.window = p->window;
   a.rows = f.rows;
   a.rows_pad = f.rows_pad;
+  a.blocks = f.blocks;
   a.waves = f.waves;
   a.row_blocks = f.row_blocks;
   a.chunk = f.chunk;
@@ -278,6 +284,8 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
   r.k = k;
   r.rn_cur = reinterpret_cast<float*>(w + slab);
   r.rho = rho ? rho : reinterpret_cast<float*>(w);
+  r.hist_tok = reinterpret_cast<int32_t*>(w + 3 * slab);
+  r.blocks = reinterpret_cast<HistBlock*>(w + 3 * slab + align_up(size_t(p->total_tokens) * sizeof(int32_t)));
   r.total_hist_blocks = int32_t(f.total_hist_blocks);
   r.max_cur = int32_t(f.max_cur);
   GateArgs g;

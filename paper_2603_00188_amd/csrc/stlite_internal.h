@@ -39,10 +39,18 @@ struct ScoreArgs {
   int32_t window;
   int32_t rows;          // G * window
   int32_t rows_pad;      // waves * row_blocks * 16
-  int32_t waves;
-  int32_t row_blocks;    // 16-row MFMA blocks per wave
+  int32_t blocks;        // ceil(rows / 16) real 16-row blocks
+  int32_t waves;         // 1, 2, 4 or 8
+  int32_t row_blocks;    // 16-row MFMA blocks per wave (1..4)
   int32_t chunk;         // keys per work-group (multiple of 64)
   int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
+};
+
+// One 256-row block of historical tokens: sequence, block index within the
+// sequence, the sequence's historical token count, and where its historical
+// tokens start in the flattened hist_tok table.
+struct HistBlock {
+  int32_t seq, hb, n_hist, hist_base;
 };
 
 struct RhoArgs {
@@ -50,6 +58,8 @@ struct RhoArgs {
   const uint16_t* k;
   float* rn_cur;         // workspace [units][L]: inverse norms of current-frame keys
   float* rho;            // [units][L]; written on historical tokens
+  int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
+  HistBlock* blocks;     // workspace [total_hist_blocks]
   int32_t total_hist_blocks;  // sum over sequences of ceil(N_hist_s / 256)
   int32_t max_cur;       // largest current frame (tokens)
 };

@@ -12,18 +12,13 @@
 // inverse norm and keeps a running row max; 16-lane butterflies finish the max.
 #include "block_select.h"
 #include "stlite_internal.h"
+#include "tile_lds.h"
 
 namespace stlite {
 namespace {
 
 constexpr int kRhoRows = 256;
-constexpr int kCurTile = 64;
-constexpr int kKStride = kHeadDim + 8;
 constexpr float kSnap = 1.0f - 1.0e-4f;
-
-struct HistBlock {
-  int32_t seq, hb, n_hist;
-};
 
 __device__ inline int32_t frame_size(const Layout& lay, int32_t f) {
   return lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
@@ -36,26 +31,27 @@ __device__ inline int32_t hist_count(const Layout& lay, int32_t s) {
   return n;
 }
 
-__device__ inline HistBlock locate_hist_block(const Layout& lay, int32_t x) {
-  int32_t acc = 0;
-  for (int32_t s = 0; s < lay.n_seqs; ++s) {
-    const int32_t nh = hist_count(lay, s);
-    const int32_t nb = (nh + kRhoRows - 1) / kRhoRows;
-    if (x < acc + nb) return HistBlock{s, x - acc, nh};
-    acc += nb;
+// Per sequence: the flattened table of historical tokens (frames in order,
+// row-major inside a frame) and the 256-row block descriptors of the rho GEMM.
+__global__ __launch_bounds__(256) void tsg_plan_kernel(RhoArgs a) {
+  const Layout& lay = a.lay;
+  const int s = blockIdx.x;
+  int32_t hist_base = 0, blk_base = 0;
+  for (int32_t t = 0; t < s; ++t) {
+    const int32_t n = hist_count(lay, t);
+    hist_base += n;
+    blk_base += (n + kRhoRows - 1) / kRhoRows;
   }
-  return HistBlock{-1, 0, 0};
-}
-
-// Absolute token of the h-th historical visual token of sequence s.
-__device__ inline int32_t hist_token(const Layout& lay, int32_t s, int32_t h) {
+  const int32_t n_hist = hist_count(lay, s);
+  const int32_t nb = (n_hist + kRhoRows - 1) / kRhoRows;
+  for (int32_t b = threadIdx.x; b < nb; b += blockDim.x) a.blocks[blk_base + b] = HistBlock{s, b, n_hist, hist_base};
   const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
+  int32_t h = hist_base;
   for (int32_t f = f0; f + 1 < f1; ++f) {
-    const int32_t n = frame_size(lay, f);
-    if (h < n) return lay.frame_meta[3 * f] + h;
-    h -= n;
+    const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
+    for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.hist_tok[h + j] = off + j;
+    h += n;
   }
-  return -1;
 }
 
 __device__ inline float sumsq8(uint4 v) {
@@ -90,40 +86,69 @@ __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void rho_kernel(RhoArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[kCurTile * kKStride];
-  __shared__ float rn_tile[kCurTile];
+// One work-group = 4 waves x 64 historical rows (the MFMA A operand, resident
+// in VGPRs).  The current frame streams through a three-stage ring of LDS
+// tiles filled by direct global->LDS DMA: tile n+2 is in flight while tile n
+// feeds the matrix cores.  Key slots past the end of the frame repeat the
+// frame's last key, which leaves every row max unchanged and needs no mask.
+// The three stages are distinct LDS arrays and the loop is unrolled by three,
+// so that the compiler can tell which DMA a tile read depends on.
+__global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
+  __shared__ __attribute__((aligned(16))) float rn0[kTileKeys], rn1[kTileKeys], rn2[kTileKeys];
   __shared__ int32_t tok_s[kRhoRows];
   __shared__ float rnrow_s[kRhoRows];
   const Layout& lay = a.lay;
   const int unit = blockIdx.y;
-  const HistBlock hb = locate_hist_block(lay, blockIdx.x);
-  if (hb.seq < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const HistBlock hb = a.blocks[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t last = lay.cu_frames[hb.seq + 1] - 1;
   const int32_t cur_off = lay.frame_meta[3 * last];
   const int32_t n_cur = frame_size(lay, last);
+  const int32_t ntiles = (n_cur + kTileKeys - 1) / kTileKeys;
   const uint16_t* kunit = a.k + size_t(unit) * lay.total_tokens * kHeadDim;
+  const uint16_t* kcur = kunit + size_t(cur_off) * kHeadDim;
+  const float* rn_cur = a.rn_cur + size_t(unit) * lay.total_tokens + cur_off;
+
+  // Tile n: 4 key wave-loads per wave, plus the 64 inverse norms on wave 0.
+  auto issue = [&](int32_t n, uint16_t* tile, float* rn) {
+    tile_dma<4>(kcur, n * kTileKeys, n_cur - 1, tile);
+    if (wave == 0)
+      __builtin_amdgcn_global_load_lds(rn_cur + min(n * kTileKeys + lane, n_cur - 1), (lds_void_t)rn, 4, 0, 0);
+  };
+  issue(0, ks0, rn0);
+  if (ntiles > 1) issue(1, ks1, rn1);
 
   // Historical rows: A operand (row = lane & 15 of each 16-row block).
-  bf16x8_t ha[4][4];
+  int32_t tok[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const int32_t h = hb.hb * kRhoRows + wave * 64 + b * 16 + (lane & 15);
-    const int32_t tok = h < hb.n_hist ? hist_token(lay, hb.seq, h) : -1;
-    float ss = 0.0f;
+    tok[b] = h < hb.n_hist ? a.hist_tok[hb.hist_base + h] : -1;
+  }
+  bf16x8_t ha[4][4];
+  float ss[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    uint4 v[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      v[kk] = tok[b] >= 0 ? *reinterpret_cast<const uint4*>(kunit + size_t(tok[b]) * kHeadDim + kk * 32 + (lane >> 4) * 8)
+                          : make_uint4(0, 0, 0, 0);
+    ss[b] = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (tok >= 0) v = *reinterpret_cast<const uint4*>(kunit + size_t(tok) * kHeadDim + kk * 32 + (lane >> 4) * 8);
-      ss += sumsq8(v);
-      ha[b][kk] = __builtin_bit_cast(bf16x8_t, v);
+      ss[b] += sumsq8(v[kk]);
+      ha[b][kk] = __builtin_bit_cast(bf16x8_t, v[kk]);
     }
-    ss += __shfl_xor(ss, 16);
-    ss += __shfl_xor(ss, 32);
+  }
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    float x = ss[b] + __shfl_xor(ss[b], 16);
+    x += __shfl_xor(x, 32);
     if (lane < 16) {
-      tok_s[wave * 64 + b * 16 + lane] = tok;
-      rnrow_s[wave * 64 + b * 16 + lane] = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+      tok_s[wave * 64 + b * 16 + lane] = tok[b];
+      rnrow_s[wave * 64 + b * 16 + lane] = x > 0.0f ? 1.0f / sqrtf(x) : 0.0f;
     }
   }
 
@@ -133,46 +158,50 @@ __global__ __launch_bounds__(256) void rho_kernel(RhoArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) runmax[b][i] = -INFINITY;
 
-  const float* rn_cur = a.rn_cur + size_t(unit) * lay.total_tokens + cur_off;
-  const uint16_t* kcur = kunit + size_t(cur_off) * kHeadDim;
-  for (int32_t c0 = 0; c0 < n_cur; c0 += kCurTile) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < kCurTile * 16; i += blockDim.x) {
-      const int key = i >> 4, part = i & 15;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c0 + key < n_cur) v = *reinterpret_cast<const uint4*>(kcur + size_t(c0 + key) * kHeadDim + part * 8);
-      *reinterpret_cast<uint4*>(ks + key * kKStride + part * 8) = v;
+  // One tile: wait for its DMA (at most tile n+1's loads stay outstanding),
+  // read the B operand, launch the DMA of tile n+2 into the stage read in the
+  // previous step, then the 64 MFMAs and the scaled running row max.
+  auto step = [&](int32_t n, const uint16_t* tile, const float* rn, uint16_t* nxt, float* nxt_rn) {
+    if (n + 1 < ntiles) {
+      if (wave == 0) wait_vmcnt<5>(); else wait_vmcnt<4>();
+    } else {
+      wait_vmcnt<0>();
     }
-    if (threadIdx.x < kCurTile) rn_tile[threadIdx.x] = (c0 + threadIdx.x < n_cur) ? rn_cur[c0 + threadIdx.x] : 0.0f;
-    __syncthreads();
+    barrier_lds();
     bf16x8_t kb[4][4];
     float rnl[4];
-    bool valid[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      rnl[t] = rn_tile[t * 16 + (lane & 15)];
-      valid[t] = c0 + t * 16 + (lane & 15) < n_cur;
+      rnl[t] = rn[t * 16 + (lane & 15)];
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        kb[t][kk] = *reinterpret_cast<const bf16x8_t*>(ks + (t * 16 + (lane & 15)) * kKStride + kk * 32 +
-                                                        (lane >> 4) * 8);
+      for (int kk = 0; kk < 4; ++kk) kb[t][kk] = tile_b_operand(tile, t, kk);
     }
+    if (n + 2 < ntiles) issue(n + 2, nxt, nxt_rn);
+    f32x4_t acc[4][4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
+    for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < 4; ++t) acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[t][kk], acc, 0, 0, 0);
+    for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float v = valid[t] ? acc[i] * rnl[t] : -INFINITY;
-          runmax[b][i] = fmaxf(runmax[b][i], v);
-        }
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[t][kk], acc[b][t], 0, 0, 0);
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float m = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rnl[0]), acc[b][1][i] * rnl[1]);
+        runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(m, acc[b][2][i] * rnl[2]), acc[b][3][i] * rnl[3]);
       }
-    }
+  };
+  for (int32_t n = 0; n < ntiles; n += 3) {
+    step(n, ks0, rn0, ks2, rn2);
+    if (n + 1 < ntiles) step(n + 1, ks1, rn1, ks0, rn0);
+    if (n + 2 < ntiles) step(n + 2, ks2, rn2, ks1, rn1);
   }
-  __syncthreads();
 
   float* rho = a.rho + size_t(unit) * lay.total_tokens;
 #pragma unroll
@@ -184,11 +213,11 @@ __global__ __launch_bounds__(256) void rho_kernel(RhoArgs a) {
       for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
       if ((lane & 15) == 0) {
         const int r = wave * 64 + b * 16 + (lane >> 4) * 4 + i;
-        const int32_t tok = tok_s[r];
-        if (tok >= 0) {
+        const int32_t t = tok_s[r];
+        if (t >= 0) {
           float x = fminf(fmaxf(mx * rnrow_s[r], -1.0f), 1.0f);
           if (x >= kSnap) x = 1.0f;
-          rho[tok] = x + 0.0f;
+          rho[t] = x + 0.0f;
         }
       }
     }
@@ -262,8 +291,11 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) {
 }
 
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
-  hipLaunchKernelGGL(cur_norms_kernel, dim3(r.lay.n_seqs, r.lay.n_units), dim3(256), 0, stream, r);
+  hipLaunchKernelGGL(tsg_plan_kernel, dim3(r.lay.n_seqs), dim3(256), 0, stream, r);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(cur_norms_kernel, dim3(r.lay.n_seqs, r.lay.n_units), dim3(256), 0, stream, r);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (r.total_hist_blocks > 0) {
     hipLaunchKernelGGL(rho_kernel, dim3(r.total_hist_blocks, r.lay.n_units), dim3(256), 0, stream, r);
