@@ -8,16 +8,17 @@
 //   combine            per row: log2 of the softmax denominator over all chunks,
 //   pass 2  (colsum)   per key chunk: 2^(x - lse) summed over the G*window rows.
 // Both passes keep the whole GQA group's window queries resident in VGPRs as
-// the MFMA A operand (up to 8 waves, each owning up to four 16-row blocks) and
-// stream 64-key tiles of K through LDS as the B operand, shared by all waves.
+// the MFMA A operand (up to eight waves, each owning up to four 16-row blocks)
+// and stream 64-key tiles of K, DMA'd into a three-stage LDS ring, as the B
+// operand shared by all waves.  Inside a wave the MFMAs of one row block run
+// under the softmax arithmetic of the previous one.
 // Logits are kept in log2 units: x = (q . k) * log2(e) / sqrt(d).
 #include "stlite_internal.h"
+#include "tile_lds.h"
 
 namespace stlite {
 namespace {
 
-constexpr int kTileKeys = 64;
-constexpr int kKStride = kHeadDim + 8;  // staged key row: 272 bytes, keeps ds_read_b128 conflict-free
 constexpr float kNegBig = -1.0e30f;
 
 struct ChunkPos {
@@ -47,32 +48,6 @@ __device__ inline ChunkPos locate_chunk(const Layout& lay, int32_t chunk, int32_
 
 __device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// Register-prefetched staging of 64-key tiles into LDS: fetch() issues the
-// global loads of the next tile before the current one is consumed, stage()
-// writes them to the other LDS buffer afterwards.  Keys past `end` are zero.
-template <int NW>
-struct KeyStager {
-  static constexpr int kThreads = NW * 64;
-  static constexpr int kPer = kTileKeys * 16 / kThreads;
-  uint4 pre[kPer];
-  __device__ inline void fetch(const uint16_t* kseq, int32_t t0, int32_t end) {
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int i = threadIdx.x + r * kThreads;
-      const int32_t j = t0 + (i >> 4);
-      pre[r] = j < end ? *reinterpret_cast<const uint4*>(kseq + size_t(j) * kHeadDim + (i & 15) * 8)
-                       : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ inline void stage(uint16_t* ks) const {
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int i = threadIdx.x + r * kThreads;
-      *reinterpret_cast<uint4*>(ks + (i >> 4) * kKStride + (i & 15) * 8) = pre[r];
-    }
-  }
-};
-
 // Row blocks are dealt to waves round-robin (wave w owns blocks w, w + NW, ...),
 // so that each SIMD of the CU gets the same number of real 16-row blocks.
 template <int NW>
@@ -97,120 +72,136 @@ __device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int 
   }
 }
 
-__device__ inline void read_b_operand(const uint16_t* ks, bf16x8_t (&kb)[4][4]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      kb[t][kk] = *reinterpret_cast<const bf16x8_t*>(ks + (t * 16 + (lane & 15)) * kKStride + kk * 32 +
-                                                      (lane >> 4) * 8);
-}
-
-// Q K^T of one 64-key tile for row block b: four 16x16 accumulators (one per
-// 16-key sub-tile); the four MFMA chains are interleaved k-step by k-step.
+// Q K^T of half a tile (32 keys: sub-tiles 2h and 2h+1) for row block b: two
+// 16x16 accumulators, two interleaved MFMA chains over the k-steps.
 template <int RB>
-__device__ inline void tile_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[4][4], int b, f32x4_t (&acc)[4]) {
+__device__ inline void half_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[2][4], int b, f32x4_t (&acc)[2]) {
 #pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < 2; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
+    for (int t = 0; t < 2; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
 }
 
-// Last key (local index) a lane's output row i of block b may see, -1 for padding rows.
-template <int NW>
-__device__ inline int32_t row_limit(const ScoreArgs& a, const ChunkPos& cp, int b, int i) {
-  const int lane = threadIdx.x & 63;
-  const int r = block_of<NW>(b) * 16 + (lane >> 4) * 4 + i;
-  return r < a.rows ? cp.seq_len - a.window + (r % a.window) : -1;
+__device__ inline void load_half_b(const uint16_t* tile, int h, bf16x8_t (&kb)[2][4]) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) kb[t][kk] = tile_b_operand(tile, 2 * h + t, kk);
 }
 
-// Pass 1 on one tile.  Per lane and window row: running max m of the raw
-// logits (q.k units) and sum of 2^((x - m) s), s = log2(e)/sqrt(d), updated
-// once per tile from the four values the lane holds for that row.
+// Ask the scheduler to alternate one MFMA with `valu` vector instructions, so
+// that the softmax arithmetic of one block runs under the next block's MFMAs.
+template <int valu>
+__device__ inline void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, valu, 0);
+  }
+}
+
+// Masked tiles read each window row's last visible key (local index; -1 for
+// padding rows) from a small LDS table instead of keeping it in VGPRs.
+__device__ inline void fill_row_limits(const ScoreArgs& a, const ChunkPos& cp, int32_t* lim_s) {
+  for (int r = threadIdx.x; r < a.rows_pad; r += blockDim.x)
+    lim_s[r] = r < a.rows ? min(cp.seq_len - a.window + (r % a.window), cp.c1 - 1) : -1;
+}
+
+// Sets the two values of row i of block b (sub-tiles 2h, 2h+1) that the row
+// may not see to -inf.
+template <int NW, bool MASK>
+__device__ inline void mask_pair(int32_t t0, int h, int b, int i, const int32_t* lim_s, float (&v)[2]) {
+  if (MASK) {
+    const int lane = threadIdx.x & 63;
+    const int32_t lim = lim_s[block_of<NW>(b) * 16 + (lane >> 4) * 4 + i];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      if (t0 + (2 * h + t) * 16 + (lane & 15) > lim) v[t] = -INFINITY;
+  }
+}
+
+// Pass 1 keeps, per lane and window row, an offset o (log2 units) and
+// sum = sum of 2^(x s - o) over the lane's keys, s = log2(e)/sqrt(d).  The
+// offsets are the lane's row maxima over the chunk's first tile; every tile
+// then only adds 2^(x s - o) and tracks amax, the largest exponent argument
+// of the lane.  amax <= kArgLimit keeps every term and sum finite; a chunk
+// where it is exceeded is recomputed by score_rowstats_exact_kernel.
+constexpr float kArgLimit = 64.0f;
+constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+
 template <int RB, int NW, bool MASK>
-__device__ inline void rowstats_tile(const ScoreArgs& a, const ChunkPos& cp, int32_t t0, const bf16x8_t (&qa)[RB][4],
-                                     const bf16x8_t (&kb)[4][4], float (&m)[RB][4], float (&sum)[RB][4]) {
-  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
-  const int lane = threadIdx.x & 63;
+__device__ inline void rowstats_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
+                                     const float (&o)[RB][4], float (&sum)[RB][4], float& amax) {
 #pragma unroll
-  for (int b = 0; b < RB; ++b) {
-    if (block_of<NW>(b) >= a.blocks) break;  // wave-uniform: padding blocks do no work
-    f32x4_t acc[4];
-    tile_logits<RB>(qa, kb, b, acc);
+  for (int i = 0; i < 4; ++i) {
+    float v[2] = {acc[0][i], acc[1][i]};
+    mask_pair<NW, MASK>(t0, h, b, i, lim_s, v);
+    const float x0 = fmaf(v[0], kScale2, -o[b][i]);
+    const float x1 = fmaf(v[1], kScale2, -o[b][i]);
+    amax = __builtin_fmaxf(__builtin_fmaxf(amax, x0), x1);
+    sum[b][i] += __builtin_amdgcn_exp2f(x0) + __builtin_amdgcn_exp2f(x1);
+  }
+}
+
+template <int RB, int NW, bool MASK>
+__device__ inline void colsum_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
+                                   const float (&lse)[RB][4], float (&col)[2]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float v[4];
+  for (int i = 0; i < 4; ++i) {
+    float v[2] = {acc[0][i], acc[1][i]};
+    mask_pair<NW, MASK>(t0, h, b, i, lim_s, v);
+    col[0] += __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -lse[b][i]));
+    col[1] += __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -lse[b][i]));
+  }
+}
+
+// One tile of pass 1 (PASS == 1) or pass 2 (PASS == 2), as two 32-key halves;
+// within a half the MFMAs of block b+1 are issued among the vector
+// instructions of block b.
+template <int RB, int NW, int PASS, bool MASK>
+__device__ inline void score_tile(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4], const uint16_t* tile,
+                                  const int32_t* lim_s, const float (&o)[RB][4], float (&sum)[RB][4], float& amax,
+                                  float (&col)[4]) {
+  const bool last_real = block_of<NW>(RB - 1) < a.blocks;  // wave-uniform
 #pragma unroll
-      for (int t = 0; t < 4; ++t) v[t] = acc[t][i];
-      if (MASK) {
-        const int32_t lim = min(row_limit<NW>(a, cp, b, i), cp.c1 - 1);
+  for (int h = 0; h < 2; ++h) {
+    bf16x8_t kb[2][4];
+    load_half_b(tile, h, kb);
+    f32x4_t acc[2][2];
+    half_logits<RB>(qa, kb, 0, acc[0]);
+    float c2[2] = {0.f, 0.f};
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          if (t0 + t * 16 + (lane & 15) > lim) v[t] = -INFINITY;
+    for (int b = 0; b < RB; ++b) {
+      if (b + 1 < RB - 1 || (b + 1 == RB - 1 && last_real)) half_logits<RB>(qa, kb, b + 1, acc[(b + 1) & 1]);
+      if (b < RB - 1 || last_real) {
+        if (PASS == 1)
+          rowstats_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, sum, amax);
+        else
+          colsum_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, c2);
       }
-      const float mx = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(m[b][i], v[0]), v[1]),
-                                       __builtin_fmaxf(v[2], v[3]));
-      const float ms = mx * scale2;
-      float sacc = sum[b][i] * __builtin_amdgcn_exp2f(fmaf(m[b][i], scale2, -ms));
-#pragma unroll
-      for (int t = 0; t < 4; ++t) sacc += __builtin_amdgcn_exp2f(fmaf(v[t], scale2, -ms));
-      sum[b][i] = sacc;
-      m[b][i] = mx;
+      interleave_mfma_valu<PASS == 1 ? 4 : 3>();
+      __builtin_amdgcn_sched_barrier(0);  // at most two blocks' accumulators live
+    }
+    if (PASS == 2) {
+      col[2 * h] += c2[0];
+      col[2 * h + 1] += c2[1];
     }
   }
 }
 
+// Merge the 16 lanes that hold the same rows (different key columns) and
+// write the chunk's (offset, sum) per window row; log2 units.
 template <int RB, int NW>
-__global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kTileKeys * kKStride];
-  const int unit = blockIdx.y;
-  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
-  if (cp.seq < 0) return;
+__device__ inline void write_partials(const ScoreArgs& a, const ChunkPos& cp, int unit, const float (&o)[RB][4],
+                                      const float (&sum)[RB][4]) {
   const int lane = threadIdx.x & 63;
-  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;
-
-  bf16x8_t qa[RB][4];
-  load_queries<RB, NW>(a, cp, unit, qa);
-  float m[RB][4], sum[RB][4];
 #pragma unroll
   for (int b = 0; b < RB; ++b)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      m[b][i] = kNegBig;
-      sum[b][i] = 0.0f;
-    }
-
-  const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
-  // Tiles that end before the window starts are visible to every row: no mask.
-  const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
-  KeyStager<NW> st;
-  st.fetch(kseq, cp.c0, cp.c1);
-  st.stage(ks[0]);
-  __syncthreads();
-  int buf = 0;
-  for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
-    const bool more = t0 + kTileKeys < cp.c1;
-    if (more) st.fetch(kseq, t0 + kTileKeys, cp.c1);
-    bf16x8_t kb[4][4];
-    read_b_operand(ks[buf], kb);
-    if (t0 + kTileKeys <= clean_end)
-      rowstats_tile<RB, NW, false>(a, cp, t0, qa, kb, m, sum);
-    else
-      rowstats_tile<RB, NW, true>(a, cp, t0, qa, kb, m, sum);
-    if (more) st.stage(ks[buf ^ 1]);
-    __syncthreads();
-    buf ^= 1;
-  }
-
-  // Merge the 16 lanes that hold the same rows (different key columns); log2 units.
-#pragma unroll
-  for (int b = 0; b < RB; ++b)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float mm = m[b][i] * scale2, ss = sum[b][i];
+      float mm = o[b][i], ss = sum[b][i];
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) {
         const float mo = __shfl_xor(mm, off);
@@ -224,6 +215,150 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
         a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(mm, ss);
       }
     }
+}
+
+// Pass 1 offsets: the lane's maximum of each row over the first tile (raw
+// logits of masked-out keys excluded; a row that sees none of them sees none
+// of the chunk's later keys either and gets kNegBig).
+template <int RB, int NW>
+__device__ inline void first_tile_offsets(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4],
+                                          const uint16_t* tile, const int32_t* lim_s, float (&o)[RB][4]) {
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    if (block_of<NW>(b) < a.blocks) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        bf16x8_t kb[2][4];
+        load_half_b(tile, h, kb);
+        f32x4_t acc[2];
+        half_logits<RB>(qa, kb, b, acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v[2] = {acc[0][i], acc[1][i]};
+          mask_pair<NW, true>(t0, h, b, i, lim_s, v);
+          mx[i] = __builtin_fmaxf(__builtin_fmaxf(mx[i], v[0]), v[1]);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[b][i] = mx[i] == -INFINITY ? kNegBig : mx[i] * kScale2;
+  }
+}
+
+template <int RB, int NW>
+__global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
+  __shared__ int32_t lim_s[NW * RB * 16];
+  __shared__ int32_t risky;
+  const int unit = blockIdx.y;
+  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
+  if (cp.seq < 0) return;
+  if (threadIdx.x == 0) risky = 0;
+  fill_row_limits(a, cp, lim_s);
+  bf16x8_t qa[RB][4];
+  load_queries<RB, NW>(a, cp, unit, qa);
+
+  const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  // Tiles that end before the window starts are visible to every row: no mask.
+  const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
+  const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
+  constexpr int kLoads = 16 / NW;  // tile DMA wave-loads per wave
+  tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
+  if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
+
+  float o[RB][4], sum[RB][4], amax = -INFINITY, col_unused[4];
+  {
+    if (ntiles > 1) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
+    barrier_lds();
+    first_tile_offsets<RB, NW>(a, cp.c0, qa, ks0, lim_s, o);
+  }
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sum[b][i] = 0.0f;
+
+  auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt) {
+    if (n > 0) {
+      if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
+      barrier_lds();
+    }
+    if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
+    const int32_t t0 = cp.c0 + n * kTileKeys;
+    if (t0 + kTileKeys <= clean_end)
+      score_tile<RB, NW, 1, false>(a, t0, qa, tile, lim_s, o, sum, amax, col_unused);
+    else
+      score_tile<RB, NW, 1, true>(a, t0, qa, tile, lim_s, o, sum, amax, col_unused);
+  };
+  for (int32_t n = 0; n < ntiles; n += 3) {
+    step(n, ks0, ks2);
+    if (n + 1 < ntiles) step(n + 1, ks1, ks0);
+    if (n + 2 < ntiles) step(n + 2, ks2, ks1);
+  }
+
+  write_partials<RB, NW>(a, cp, unit, o, sum);
+  if (__ballot(amax > kArgLimit) != 0 && (threadIdx.x & 63) == 0) atomicOr(&risky, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = risky;
+}
+
+// Exact pass 1 for the chunks flagged by score_rowstats_kernel: a running row
+// max per lane with the sums rescaled on every tile (plain staging; it only
+// runs when a chunk's logits rise more than kArgLimit above the first tile's).
+template <int RB, int NW>
+__global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems];
+  __shared__ int32_t lim_s[NW * RB * 16];
+  const int unit = blockIdx.y;
+  if (a.redo[size_t(unit) * a.total_chunks + blockIdx.x] == 0) return;
+  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
+  if (cp.seq < 0) return;
+  fill_row_limits(a, cp, lim_s);
+  bf16x8_t qa[RB][4];
+  load_queries<RB, NW>(a, cp, unit, qa);
+  float m[RB][4], sum[RB][4];
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      m[b][i] = kNegBig;
+      sum[b][i] = 0.0f;
+    }
+  const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
+    __syncthreads();
+    tile_dma<NW>(kseq, t0, cp.c1 - 1, ks0);
+    wait_vmcnt<0>();
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      if (block_of<NW>(b) >= a.blocks) break;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        bf16x8_t kb[2][4];
+        load_half_b(ks0, h, kb);
+        f32x4_t acc[2];
+        half_logits<RB>(qa, kb, b, acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v[2] = {acc[0][i], acc[1][i]};
+          mask_pair<NW, true>(t0, h, b, i, lim_s, v);
+          const float mx = __builtin_fmaxf(__builtin_fmaxf(m[b][i], v[0]), v[1]);
+          const float ms = mx * kScale2;
+          sum[b][i] = sum[b][i] * __builtin_amdgcn_exp2f(fmaf(m[b][i], kScale2, -ms)) +
+                      __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -ms)) +
+                      __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -ms));
+          m[b][i] = mx;
+        }
+      }
+    }
+  }
+  float o[RB][4];
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[b][i] = m[b][i] * kScale2;
+  write_partials<RB, NW>(a, cp, unit, o, sum);
 }
 
 __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
@@ -254,43 +389,21 @@ __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
 
 // Pass 2 on one tile: col[t] += 2^(x s - lse) over the lane's rows, for the
 // lane's key column of sub-tile t.
-template <int RB, int NW, bool MASK>
-__device__ inline void colsum_tile(const ScoreArgs& a, const ChunkPos& cp, int32_t t0, const bf16x8_t (&qa)[RB][4],
-                                   const bf16x8_t (&kb)[4][4], const float (&lse)[RB][4], float (&col)[4]) {
-  const float scale2 = 1.4426950408889634f * 0.08838834764831845f;
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int b = 0; b < RB; ++b) {
-    if (block_of<NW>(b) >= a.blocks) break;  // wave-uniform: padding blocks do no work
-    f32x4_t acc[4];
-    tile_logits<RB>(qa, kb, b, acc);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int32_t lim = 0;
-      if (MASK) lim = min(row_limit<NW>(a, cp, b, i), cp.c1 - 1);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        float p = __builtin_amdgcn_exp2f(fmaf(acc[t][i], scale2, -lse[b][i]));
-        if (MASK && t0 + t * 16 + (lane & 15) > lim) p = 0.0f;
-        col[t] += p;
-      }
-    }
-  }
-}
-
 // Pass 2.  A_j = (1/G) sum over rows of 2^(x_rj - lse_r): the lane's four
 // rows per block are summed in registers, then across the four lane groups
 // that share a key column, then across waves in LDS.
 template <int RB, int NW>
 __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kTileKeys * kKStride];
-  __shared__ float red[2][NW][kTileKeys];  // per LDS buffer: no barrier between read and next write
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
+  __shared__ float red0[NW][kTileKeys], red1[NW][kTileKeys], red2[NW][kTileKeys];
+  __shared__ int32_t lim_s[NW * RB * 16];
   const int unit = blockIdx.y;
   const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
   if (cp.seq < 0) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float inv_g = 1.0f / float(a.group);
 
+  fill_row_limits(a, cp, lim_s);
   bf16x8_t qa[RB][4];
   load_queries<RB, NW>(a, cp, unit, qa);
   float lse[RB][4];
@@ -303,21 +416,33 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
   float* aout = a.a_base + size_t(unit) * a.lay.total_tokens + cp.seq_start;
   const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
-  KeyStager<NW> st;
-  st.fetch(kseq, cp.c0, cp.c1);
-  st.stage(ks[0]);
-  __syncthreads();
-  int buf = 0;
-  for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
-    const bool more = t0 + kTileKeys < cp.c1;
-    if (more) st.fetch(kseq, t0 + kTileKeys, cp.c1);
-    bf16x8_t kb[4][4];
-    read_b_operand(ks[buf], kb);
+  const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
+  constexpr int kLoads = 16 / NW;
+  // Column sums of tile n are reduced across waves after the barrier of step n+1.
+  auto reduce = [&](int32_t n, const float (&r)[NW][kTileKeys]) {
+    if (threadIdx.x < kTileKeys) {
+      float s = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += r[w][threadIdx.x];
+      const int32_t j = cp.c0 + n * kTileKeys + threadIdx.x;
+      if (j < cp.c1) aout[j] = s * inv_g;
+    }
+  };
+  tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
+  if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
+  float sum_unused[RB][4], amax_unused = 0.0f;
+  auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt, float (&r)[NW][kTileKeys],
+                  const float (&rprev)[NW][kTileKeys]) {
+    if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
+    barrier_lds();
+    if (n > 0) reduce(n - 1, rprev);
+    if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
+    const int32_t t0 = cp.c0 + n * kTileKeys;
     float col[4] = {0.f, 0.f, 0.f, 0.f};
     if (t0 + kTileKeys <= clean_end)
-      colsum_tile<RB, NW, false>(a, cp, t0, qa, kb, lse, col);
+      score_tile<RB, NW, 2, false>(a, t0, qa, tile, lim_s, lse, sum_unused, amax_unused, col);
     else
-      colsum_tile<RB, NW, true>(a, cp, t0, qa, kb, lse, col);
+      score_tile<RB, NW, 2, true>(a, t0, qa, tile, lim_s, lse, sum_unused, amax_unused, col);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       col[t] += __shfl_xor(col[t], 16);
@@ -325,19 +450,17 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
     }
     if (lane < 16) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) red[buf][wave][t * 16 + lane] = col[t];
+      for (int t = 0; t < 4; ++t) r[wave][t * 16 + lane] = col[t];
     }
-    if (more) st.stage(ks[buf ^ 1]);
-    __syncthreads();
-    if (threadIdx.x < kTileKeys) {
-      float s = 0.0f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) s += red[buf][w][threadIdx.x];
-      const int32_t j = t0 + threadIdx.x;
-      if (j < cp.c1) aout[j] = s * inv_g;
-    }
-    buf ^= 1;
+  };
+  for (int32_t n = 0; n < ntiles; n += 3) {
+    step(n, ks0, ks2, red0, red2);
+    if (n + 1 < ntiles) step(n + 1, ks1, ks0, red1, red0);
+    if (n + 2 < ntiles) step(n + 2, ks2, ks1, red2, red1);
   }
+  barrier_lds();
+  const int last = (ntiles - 1) % 3;
+  reduce(ntiles - 1, last == 0 ? red0 : (last == 1 ? red1 : red2));
 }
 
 template <int RB, int NW>
@@ -346,6 +469,9 @@ hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   const dim3 block(64 * NW);
   hipLaunchKernelGGL((score_rowstats_kernel<RB, NW>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((score_rowstats_exact_kernel<RB, NW>), grid, block, 0, stream, a);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(score_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   e = hipGetLastError();

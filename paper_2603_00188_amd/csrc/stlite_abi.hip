@@ -208,7 +208,8 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
   switch (call) {
     case STLITE_CALL_SCORE_WINDOW:
       *bytes = align_up(size_t(f.units) * f.total_chunks * f.rows_pad * sizeof(float2)) +
-               align_up(size_t(f.units) * p->n_seqs * f.rows_pad * sizeof(float));
+               align_up(size_t(f.units) * p->n_seqs * f.rows_pad * sizeof(float)) +
+               align_up(size_t(f.units) * f.total_chunks * sizeof(int32_t));
       break;
     case STLITE_CALL_TSG_GATE:
       // rho scratch, current-frame norms, gate keys, historical-token table, block table
@@ -242,8 +243,10 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
   a.k = k;
   a.a_base = a_base;
   a.partial = static_cast<float2*>(ws);
-  a.lse2 = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                    align_up(size_t(f.units) * f.total_chunks * f.rows_pad * sizeof(float2)));
+  const size_t part_bytes = align_up(size_t(f.units) * f.total_chunks * f.rows_pad * sizeof(float2));
+  a.lse2 = reinterpret_cast<float*>(static_cast<char*>(ws) + part_bytes);
+  a.redo = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + part_bytes +
+                                      align_up(size_t(f.units) * p->n_seqs * f.rows_pad * sizeof(float)));
   a.n_q_heads = p->n_q_heads;
   a.group = p->n_q_heads / p->n_kv_heads;
   a.window = p->window;

@@ -34,6 +34,7 @@ struct ScoreArgs {
   float* a_base;         // [units][L]
   float2* partial;       // workspace [units][total_chunks][rows_pad] (max, sum) in log2 units
   float* lse2;           // workspace [units][seqs][rows_pad]
+  int32_t* redo;         // workspace [units][total_chunks]: chunk needs the exact pass 1
   int32_t n_q_heads;
   int32_t group;         // G
   int32_t window;

@@ -216,3 +216,27 @@ def test_config3_sampled(torch_cuda):
 @pytest.mark.timeout(900)
 def test_config4_sampled(torch_cuda):
     _full(4, samples=((0, 0, 0), (13, 2, 4), (27, 3, 7)))
+
+
+def test_logit_spike_takes_exact_pass(torch_cuda):
+    """Keys aligned with a window query, far into a chunk, push that query's
+    logits more than 64 (log2 units) above the chunk's first tile: the lean
+    first pass flags those chunks and the exact pass recomputes them."""
+    import torch
+    H = _H()
+    from oracle import stlite_oracle as O
+    from paper_2603_00188_amd import workload as W2
+    w = _small([[(F, 12, 21), (T, 37), (F, 12, 21), (T, 37), (F, 12, 21), (T, 150)]],
+               G=4, Hkv=3, window=16, beta=(3, 10), layers=1)
+    case = H.Case(w)
+    q = O.bf16_to_f64(case.q[0, 0, 0, 0])           # head 0, window position 0
+    unit_dir = q / np.linalg.norm(q)
+    spike = W2.to_bf16_bits((250.0 * unit_dir).astype(np.float32))
+    for j in (200, 460, 700):                       # not in the first tile of their chunk
+        case.k[0, 0, j] = spike
+    case.dk.copy_(torch.from_numpy(case.k.view(np.int16)))
+    res = case.run()
+    for kv in range(w.n_kv_heads):
+        H.compare_unit(case, res, 0, kv, 0)
+    A = res["a_base"][0]
+    assert A[200] > 0.2 and A[460] > 0.2, "spike keys should carry most of head 0's window mass"
