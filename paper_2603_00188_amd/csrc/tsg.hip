@@ -158,9 +158,56 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) runmax[b][i] = -INFINITY;
 
+  // Ping-pong inside the wave.  A tile is two halves (16-key sub-tiles 0-1 and
+  // 2-3); the 32 MFMAs of one half are issued among the scale-and-max
+  // instructions of the other half (carried across the tile boundary), and
+  // the B operand is read from LDS one k-step ahead of its MFMAs.
+  auto mfma_half = [&](const uint16_t* tile, int h, f32x4_t (&acc)[4][2]) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    bf16x8_t kb[2][2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) kb[0][t] = tile_b_operand(tile, 2 * h + t, 0);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (kk + 1 < 4) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) kb[(kk + 1) & 1][t] = tile_b_operand(tile, 2 * h + t, kk + 1);
+      }
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[kk & 1][t], acc[b][t], 0, 0, 0);
+    }
+  };
+  auto max_half = [&](const f32x4_t (&acc)[4][2], float rn0, float rn1) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rn0), acc[b][1][i] * rn1);
+  };
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // 3 VALU
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  f32x4_t accA[4][2], accB[4][2];
+  // Before the first tile the "previous second half" contributes -inf to every max.
+  float rnB0 = 1.0f, rnB1 = 1.0f;  // norms of the previous tile's second half
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) accB[b][t] = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
   // One tile: wait for its DMA (at most tile n+1's loads stay outstanding),
-  // read the B operand, launch the DMA of tile n+2 into the stage read in the
-  // previous step, then the 64 MFMAs and the scaled running row max.
+  // launch the DMA of tile n+2 into the stage read in the previous step.
   auto step = [&](int32_t n, const uint16_t* tile, const float* rn, uint16_t* nxt, float* nxt_rn) {
     if (n + 1 < ntiles) {
       if (wave == 0) wait_vmcnt<5>(); else wait_vmcnt<4>();
@@ -168,40 +215,24 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
       wait_vmcnt<0>();
     }
     barrier_lds();
-    bf16x8_t kb[4][4];
-    float rnl[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      rnl[t] = rn[t * 16 + (lane & 15)];
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) kb[t][kk] = tile_b_operand(tile, t, kk);
-    }
+    const float rnA0 = rn[0 * 16 + (lane & 15)], rnA1 = rn[1 * 16 + (lane & 15)];
+    const float rnN0 = rn[2 * 16 + (lane & 15)], rnN1 = rn[3 * 16 + (lane & 15)];
     if (n + 2 < ntiles) issue(n + 2, nxt, nxt_rn);
-    f32x4_t acc[4][4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[t][kk], acc[b][t], 0, 0, 0);
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float m = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rnl[0]), acc[b][1][i] * rnl[1]);
-        runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(m, acc[b][2][i] * rnl[2]), acc[b][3][i] * rnl[3]);
-      }
+    mfma_half(tile, 0, accA);
+    max_half(accB, rnB0, rnB1);
+    interleave();
+    mfma_half(tile, 1, accB);
+    max_half(accA, rnA0, rnA1);
+    interleave();
+    rnB0 = rnN0;
+    rnB1 = rnN1;
   };
   for (int32_t n = 0; n < ntiles; n += 3) {
     step(n, ks0, rn0, ks2, rn2);
     if (n + 1 < ntiles) step(n + 1, ks1, rn1, ks0, rn0);
     if (n + 2 < ntiles) step(n + 2, ks2, rn2, ks1, rn1);
   }
+  max_half(accB, rnB0, rnB1);
 
   float* rho = a.rho + size_t(unit) * lay.total_tokens;
 #pragma unroll
