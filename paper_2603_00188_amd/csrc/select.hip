@@ -1,84 +1,142 @@
 // Integrated score and flat top-B (Eq. modal_scoring and Sec. integrated
-// scoring of the paper), one work-group per (unit, sequence):
+// scoring of the paper), for every (unit, sequence) segment at once:
 //   S = A on text tokens, S = M * (A + alpha * Phi) on visual tokens,
 //   I_keep = the B tokens first in (S descending, index ascending) order,
 //   written in ascending token order.
-// S is turned into a descending order key once, the B-th key is found by a
-// four-pass radix select, and one ordered pass with two work-group scans
-// resolves ties at the threshold by lowest index and compacts the survivors.
-#include "block_select.h"
+// The selection is the segmented radix select of segsel.h on the keys
+// ~order_key(S) (ascending key = descending S).
+#include "segsel.h"
 #include "stlite_internal.h"
 
 namespace stlite {
 namespace {
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
-  __shared__ SelectShared sh;
+constexpr int kMaxChunkFrames = 64;
+
+// Sequence table of the selection: n = L_s, k = B_s.
+__global__ __launch_bounds__(64) void select_plan_kernel(SelectArgs a) {
+  if (threadIdx.x != 0) return;
+  SeqInfo* info = a.info;
   const Layout& lay = a.lay;
-  const int s = blockIdx.x, unit = blockIdx.y, tid = threadIdx.x;
-  const int32_t seq_start = lay.cu_seqlens[s], seq_end = lay.cu_seqlens[s + 1];
-  const int32_t L = seq_end - seq_start;
-  const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
-  const int32_t kept_base = lay.cu_budget[s];
-  const int32_t B = lay.cu_budget[s + 1] - kept_base;
-  const size_t ubase = size_t(unit) * lay.total_tokens;
-  const float* A = a.a_base + ubase;
-  const float* phi = a.phi ? a.phi + ubase : nullptr;
-  const uint8_t* gate = a.gate ? a.gate + ubase : nullptr;
-  float* score = a.score ? a.score + ubase : nullptr;
-  uint32_t* keys = a.keys + ubase + seq_start;  // keys[j] for token seq_start + j
-  int32_t* kept = a.kept + size_t(unit) * lay.total_budget + kept_base;
-  const float alpha = a.alpha;
-
-  // Scores, segment by segment (text gap, frame, ..., trailing text).
-  int32_t prev = seq_start;
-  for (int32_t f = f0; f <= f1; ++f) {
-    const bool is_frame = f < f1;
-    const int32_t off = is_frame ? lay.frame_meta[3 * f] : seq_end;
-    for (int32_t j = prev + tid; j < off; j += kSelThreads) {
-      const float S = A[j];
-      if (score) score[j] = S;
-      keys[j - seq_start] = ~order_key(S);
-    }
-    if (is_frame) {
-      const int32_t n = lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
-      for (int32_t j = off + tid; j < off + n; j += kSelThreads) {
-        const float x = phi ? fmaf(alpha, phi[j], A[j]) : A[j];
-        const float S = (gate && gate[j] == 0) ? 0.0f : x;
-        if (score) score[j] = S;
-        keys[j - seq_start] = ~order_key(S);
-      }
-      prev = off + n;
-    }
+  int32_t cb = 0;
+  for (int32_t q = 0; q < lay.n_seqs; ++q) {
+    const int32_t n = lay.cu_seqlens[q + 1] - lay.cu_seqlens[q];
+    info[q] = SeqInfo{n, lay.cu_budget[q + 1] - lay.cu_budget[q], cb, 0};
+    cb += (n + kSegChunk - 1) / kSegChunk;
   }
-  if (B == 0) return;
+  info[lay.n_seqs] = SeqInfo{0, 0, cb, 0};
+}
+
+// Does token `tok` (absolute) lie in one of the sequence's frames f0 .. f1-1?
+__device__ inline bool is_visual_search(const Layout& lay, int32_t f0, int32_t f1, int32_t tok) {
+  int32_t lo = f0, hi = f1 - 1, hit = -1;
+  while (lo <= hi) {  // last frame with offset <= tok
+    const int32_t mid = (lo + hi) >> 1;
+    if (lay.frame_meta[3 * mid] <= tok) { hit = mid; lo = mid + 1; } else { hi = mid - 1; }
+  }
+  return hit >= 0 && tok < lay.frame_meta[3 * hit] + lay.frame_meta[3 * hit + 1] * lay.frame_meta[3 * hit + 2];
+}
+
+// Scores, order keys and the level-0 histogram of one 4096-token chunk.
+__global__ __launch_bounds__(kSegThreads) void select_keys_kernel(SelectArgs a) {
+  const SegSel& s = a.sel;
+  __shared__ uint32_t lh[kSegBins];
+  __shared__ int32_t fr_lo[kMaxChunkFrames], fr_hi[kMaxChunkFrames];
+  __shared__ int32_t nfr;
+  const Layout& lay = a.lay;
+  const int unit = blockIdx.y;
+  const ChunkRef cr = seg_chunk(s, blockIdx.x);
+  const int32_t seq_start = lay.cu_seqlens[cr.seq];
+  const int32_t t_begin = seq_start + cr.begin, t_end = seq_start + cr.end;
+  const int32_t f0 = lay.cu_frames[cr.seq], f1 = lay.cu_frames[cr.seq + 1];
+  seg_hist_zero(lh);
+  if (threadIdx.x == 0) {
+    // frames overlapping [t_begin, t_end), in order; -1 if there are too many
+    int32_t lo = f0, hi = f1 - 1, first = f1;
+    while (lo <= hi) {  // first frame that ends after t_begin
+      const int32_t mid = (lo + hi) >> 1;
+      const int32_t end = lay.frame_meta[3 * mid] + lay.frame_meta[3 * mid + 1] * lay.frame_meta[3 * mid + 2];
+      if (end > t_begin) { first = mid; hi = mid - 1; } else { lo = mid + 1; }
+    }
+    int32_t n = 0;
+    for (int32_t f = first; f < f1 && lay.frame_meta[3 * f] < t_end; ++f) {
+      if (n == kMaxChunkFrames) { n = -1; break; }
+      fr_lo[n] = lay.frame_meta[3 * f];
+      fr_hi[n] = lay.frame_meta[3 * f] + lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
+      ++n;
+    }
+    nfr = n;
+  }
   __syncthreads();
-
-  int32_t need = 0;
-  uint32_t T = 0xffffffffu;
-  if (B < L) T = block_radix_select(keys, L, B, sh, &need);
-  else need = L;  // keep everything: every key is <= T
-
-  int32_t running_eq = 0, running_kept = 0;
-  for (int32_t base = 0; base < L; base += kSelThreads) {
-    const int32_t j = base + tid;
-    const bool in = j < L;
-    const uint32_t key = in ? keys[j] : 0xffffffffu;
-    const bool eq = in && key == T;
-    int32_t eq_tot, kept_tot;
-    const int32_t eq_incl = block_inclusive_scan(eq ? 1 : 0, sh.wave_tot, &eq_tot);
-    const bool take = (in && key < T) || (eq && running_eq + eq_incl - 1 < need);
-    const int32_t k_incl = block_inclusive_scan(take ? 1 : 0, sh.wave_tot2, &kept_tot);
-    if (take && running_kept + k_incl - 1 < B) kept[running_kept + k_incl - 1] = seq_start + j;
-    running_eq += eq_tot;
-    running_kept += kept_tot;
+  const int32_t n_fr = nfr;
+  const size_t ubase = size_t(unit) * lay.total_tokens;
+  uint32_t* keys = seg_keys(s, unit, cr.seq);
+#pragma unroll 4
+  for (int j = 0; j < kSegPer; ++j) {
+    const int32_t i = cr.begin + j * kSegThreads + threadIdx.x;
+    const bool in = i < cr.end;
+    uint32_t key = 0;
+    if (in) {
+      const int32_t tok = seq_start + i;
+      bool visual = false;
+      if (n_fr >= 0) {
+        for (int32_t f = 0; f < n_fr; ++f) visual |= (tok >= fr_lo[f]) & (tok < fr_hi[f]);
+      } else {
+        visual = is_visual_search(lay, f0, f1, tok);
+      }
+      const float A = a.a_base[ubase + tok];
+      float S = A;
+      if (visual) {
+        const float x = a.phi ? fmaf(a.alpha, a.phi[ubase + tok], A) : A;
+        S = (a.gate && a.gate[ubase + tok] == 0) ? 0.0f : x;
+      }
+      if (a.score) a.score[ubase + tok] = S;
+      key = ~order_key(S);
+      keys[i] = key;
+    }
+    seg_hist_add(lh, in, key >> 21);
   }
+  __syncthreads();
+  seg_hist_flush(lh, seg_hist(s, unit, cr.seq, 0));
+}
+
+// Kept token indices, ascending, at cu_budget[seq] + rank.
+__global__ __launch_bounds__(kSegThreads) void select_emit_kernel(SelectArgs a) {
+  const SegSel& s = a.sel;
+  __shared__ int32_t scratch[kSegThreads / 64];
+  const Layout& lay = a.lay;
+  const int unit = blockIdx.y;
+  const ChunkRef cr = seg_chunk(s, blockIdx.x);
+  TakeChunk tc;
+  take_chunk(s, unit, cr, scratch, tc);
+  const int32_t seq_start = lay.cu_seqlens[cr.seq];
+  const int32_t kb = lay.cu_budget[cr.seq], B = lay.cu_budget[cr.seq + 1] - kb;
+  int32_t* kept = a.kept + size_t(unit) * lay.total_budget + kb;
+  const int32_t i0 = cr.begin + threadIdx.x * kSegPer;
+#pragma unroll
+  for (int i = 0; i < kSegPer; ++i)
+    if (tc.take[i] && tc.pos[i] < B) kept[tc.pos[i]] = seq_start + i0 + i;
 }
 
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(kSelThreads), 0, stream, a);
+  const SegSel& s = a.sel;
+  const int32_t U = a.lay.n_units;
+  hipLaunchKernelGGL(select_plan_kernel, dim3(1), dim3(64), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_segsel_zero(s, U, stream);
+  if (e != hipSuccess) return e;
+  const dim3 chunk_grid(s.chunks_per_unit, U);
+  if (s.chunks_per_unit > 0) {
+    hipLaunchKernelGGL(select_keys_kernel, chunk_grid, dim3(kSegThreads), 0, stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  e = launch_segsel_middle(s, U, stream);
+  if (e != hipSuccess || s.chunks_per_unit == 0) return e;
+  hipLaunchKernelGGL(select_emit_kernel, chunk_grid, dim3(kSegThreads), 0, stream, a);
   return hipGetLastError();
 }
 

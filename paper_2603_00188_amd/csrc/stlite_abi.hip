@@ -41,6 +41,8 @@ struct Facts {
   int64_t max_cur;
   int32_t rows, rows_pad, blocks, waves, row_blocks, chunk;
   int64_t total_chunks;
+  int64_t sel_chunks;   // selection chunks per unit over all tokens (top-B)
+  int64_t gate_chunks;  // selection chunks per unit over historical tokens (gate)
 };
 
 Facts derive(const stlite_problem* p) {
@@ -75,8 +77,60 @@ Facts derive(const stlite_problem* p) {
         f.max_cur = std::max(f.max_cur, n);
     }
     f.total_hist_blocks += ceil_div(hist, 256);
+    f.sel_chunks += ceil_div(L, kSegChunk);
+    f.gate_chunks += ceil_div(hist, kSegChunk);
   }
   return f;
+}
+
+// Workspace of one segmented selection: keys, histograms, per-segment state,
+// per-chunk counts and offsets.
+size_t seg_bytes(const stlite_problem* p, const Facts& f, int64_t chunks) {
+  return align_up(size_t(f.units) * p->total_tokens * sizeof(uint32_t)) +
+         align_up(size_t(f.units) * p->n_seqs * 3 * 2048 * sizeof(uint32_t)) +
+         align_up(size_t(f.units) * p->n_seqs * sizeof(SegState)) +
+         align_up(size_t(f.units) * chunks * sizeof(SegCount)) +
+         align_up(size_t(f.units) * chunks * sizeof(SegOffset));
+}
+
+SegSel seg_carve(const stlite_problem* p, const Facts& f, int64_t chunks, const SeqInfo* info, char* w) {
+  SegSel s;
+  s.info = info;
+  s.cu_seqlens = p->cu_seqlens;
+  s.n_seqs = p->n_seqs;
+  s.chunks_per_unit = int32_t(chunks);
+  s.total_tokens = p->total_tokens;
+  s.keys = reinterpret_cast<uint32_t*>(w);
+  w += align_up(size_t(f.units) * p->total_tokens * sizeof(uint32_t));
+  s.hist = reinterpret_cast<uint32_t*>(w);
+  w += align_up(size_t(f.units) * p->n_seqs * 3 * 2048 * sizeof(uint32_t));
+  s.state = reinterpret_cast<SegState*>(w);
+  w += align_up(size_t(f.units) * p->n_seqs * sizeof(SegState));
+  s.counts = reinterpret_cast<SegCount*>(w);
+  w += align_up(size_t(f.units) * chunks * sizeof(SegCount));
+  s.offsets = reinterpret_cast<SegOffset*>(w);
+  s.pivot_value = nullptr;
+  return s;
+}
+
+size_t info_bytes(const stlite_problem* p) { return align_up(size_t(p->n_seqs + 1) * sizeof(SeqInfo)); }
+
+// Gate workspace after the rho slabs: historical-token table, rho block table,
+// segment table, then the selection.
+size_t gate_tail_bytes(const stlite_problem* p, const Facts& f) {
+  return align_up(size_t(p->total_tokens) * sizeof(int32_t)) +
+         align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock)) + info_bytes(p) +
+         seg_bytes(p, f, f.gate_chunks);
+}
+
+void gate_carve(const stlite_problem* p, const Facts& f, char* w, GateArgs& g) {
+  g.hist_tok = reinterpret_cast<int32_t*>(w);
+  w += align_up(size_t(p->total_tokens) * sizeof(int32_t));
+  g.blocks = reinterpret_cast<HistBlock*>(w);
+  w += align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock));
+  g.info = reinterpret_cast<SeqInfo*>(w);
+  w += info_bytes(p);
+  g.sel = seg_carve(p, f, f.gate_chunks, g.info, w);
 }
 
 Layout make_layout(const stlite_problem* p) {
@@ -212,13 +266,14 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
                align_up(size_t(f.units) * f.total_chunks * sizeof(int32_t));
       break;
     case STLITE_CALL_TSG_GATE:
-      // rho scratch, current-frame norms, gate keys, historical-token table, block table
-      *bytes = 3 * align_up(per_token * sizeof(float)) + align_up(size_t(p->total_tokens) * sizeof(int32_t)) +
-               align_up(size_t(f.total_hist_blocks) * sizeof(HistBlock));
+      // rho scratch, current-frame norms, then the threshold's workspace
+      *bytes = 2 * align_up(per_token * sizeof(float)) + gate_tail_bytes(p, f);
       break;
     case STLITE_CALL_TSG_THRESHOLD:
+      *bytes = gate_tail_bytes(p, f);
+      break;
     case STLITE_CALL_SELECT_TOPK:
-      *bytes = align_up(per_token * sizeof(uint32_t));
+      *bytes = info_bytes(p) + seg_bytes(p, f, f.sel_chunks);
       break;
     case STLITE_CALL_CSS_SALIENCY:
     case STLITE_CALL_COMPACT_KV:
@@ -282,22 +337,22 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
   const Facts f = derive(p);
   const size_t slab = align_up(size_t(f.units) * p->total_tokens * sizeof(float));
   char* w = static_cast<char*>(ws);
+  GateArgs g;
+  g.lay = make_layout(p);
+  g.rho = rho ? rho : reinterpret_cast<float*>(w);
+  g.rho_zero_fill = rho;
+  g.gate = gate;
+  gate_carve(p, f, w + 2 * slab, g);
+  g.sel.pivot_value = tau;
   RhoArgs r;
-  r.lay = make_layout(p);
+  r.lay = g.lay;
   r.k = k;
   r.rn_cur = reinterpret_cast<float*>(w + slab);
-  r.rho = rho ? rho : reinterpret_cast<float*>(w);
-  r.hist_tok = reinterpret_cast<int32_t*>(w + 3 * slab);
-  r.blocks = reinterpret_cast<HistBlock*>(w + 3 * slab + align_up(size_t(p->total_tokens) * sizeof(int32_t)));
+  r.rho = const_cast<float*>(g.rho);
+  r.hist_tok = g.hist_tok;
+  r.blocks = g.blocks;
   r.total_hist_blocks = int32_t(f.total_hist_blocks);
   r.max_cur = int32_t(f.max_cur);
-  GateArgs g;
-  g.lay = r.lay;
-  g.rho = r.rho;
-  g.rho_zero_fill = rho;
-  g.tau = tau;
-  g.gate = gate;
-  g.keys = reinterpret_cast<uint32_t*>(w + 2 * slab);
   return hip_status(launch_tsg_gate(r, g, static_cast<hipStream_t>(stream)), "tsg_gate launch");
 }
 
@@ -306,13 +361,14 @@ stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, fl
   stlite_status st = check_ws(p, STLITE_CALL_TSG_THRESHOLD, ws, ws_bytes);
   if (st != STLITE_OK) return st;
   if (!rho || !gate) return fail(STLITE_ERR_INVALID_ARG, "rho and gate must be non-NULL");
+  const Facts f = derive(p);
   GateArgs g;
   g.lay = make_layout(p);
   g.rho = rho;
   g.rho_zero_fill = nullptr;
-  g.tau = tau;
   g.gate = gate;
-  g.keys = static_cast<uint32_t*>(ws);
+  gate_carve(p, f, static_cast<char*>(ws), g);
+  g.sel.pivot_value = tau;
   return hip_status(launch_tsg_threshold(g, static_cast<hipStream_t>(stream)), "tsg_threshold launch");
 }
 
@@ -333,7 +389,9 @@ stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base, c
   a.alpha = alpha;
   a.kept = kept;
   a.score = score;
-  a.keys = static_cast<uint32_t*>(ws);
+  const Facts f = derive(p);
+  a.info = static_cast<SeqInfo*>(ws);
+  a.sel = seg_carve(p, f, f.sel_chunks, a.info, static_cast<char*>(ws) + info_bytes(p));
   return hip_status(launch_select(a, static_cast<hipStream_t>(stream)), "select_topk launch");
 }
 

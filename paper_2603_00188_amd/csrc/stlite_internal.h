@@ -47,6 +47,46 @@ struct ScoreArgs {
   int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
 };
 
+// Segmented k-smallest selection (segsel.h).  A segment is one (unit,
+// sequence) pair; its keys are cut into chunks of kSegChunk.
+constexpr int kSegChunk = 4096;
+
+struct SeqInfo {
+  int32_t n;            // keys in the segment (same for every unit)
+  int32_t k;            // keys to select
+  int32_t chunk_begin;  // first chunk of this sequence (chunks of all sequences of a unit are numbered together)
+  int32_t aux;          // producer-specific (first historical row of the sequence for the gate)
+};
+
+struct SegState {
+  uint32_t prefix, mask;
+  int32_t k_rem;        // rank still to find inside the current prefix; after level 2: keys == T to take
+  int32_t k;            // total selected
+};
+
+struct SegCount {
+  int32_t less, eq;
+};
+
+struct SegOffset {
+  int32_t out;          // selected keys in earlier chunks of the segment
+  int32_t eq_before;    // keys == T in earlier chunks of the segment
+};
+
+struct SegSel {
+  const SeqInfo* info;     // [n_seqs + 1]: entry n_seqs holds chunk_begin = chunks per unit
+  const int32_t* cu_seqlens;
+  int32_t n_seqs;
+  int32_t chunks_per_unit;
+  int64_t total_tokens;
+  uint32_t* keys;          // [units][total_tokens]
+  uint32_t* hist;          // [units][n_seqs][3][kSegBins]
+  SegState* state;         // [units][n_seqs]
+  SegCount* counts;        // [units][chunks_per_unit]
+  SegOffset* offsets;      // [units][chunks_per_unit]
+  float* pivot_value;      // nullable [units][n_seqs]: value of the k-th key, NaN when k = 0
+};
+
 // One 256-row block of historical tokens: sequence, block index within the
 // sequence, the sequence's historical token count, and where its historical
 // tokens start in the flattened hist_tok table.
@@ -68,10 +108,12 @@ struct RhoArgs {
 struct GateArgs {
   Layout lay;
   const float* rho;      // [units][L] (historical entries read)
-  float* rho_zero_fill;  // nullable: non-historical entries of this array are set to 0
-  float* tau;            // nullable [units][seqs]
+  float* rho_zero_fill;  // nullable: every entry of this array is zeroed before rho is written
   uint8_t* gate;         // [units][L]
-  uint32_t* keys;        // workspace [units][L] (compact historical keys)
+  int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
+  HistBlock* blocks;     // workspace [total_hist_blocks]
+  SeqInfo* info;         // workspace [n_seqs + 1]: segment table (n = N_hist, k = min(B, N_hist))
+  SegSel sel;            // keys in compact historical order; pivot_value = tau
 };
 
 struct CssArgs {
@@ -89,7 +131,8 @@ struct SelectArgs {
   float alpha;
   int32_t* kept;         // [units][total_budget]
   float* score;          // nullable [units][L]
-  uint32_t* keys;        // workspace [units][L]
+  SeqInfo* info;         // workspace [n_seqs + 1]: segment table (n = L_s, k = B_s)
+  SegSel sel;
 };
 
 struct CompactArgs {

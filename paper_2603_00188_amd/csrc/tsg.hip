@@ -10,7 +10,9 @@
 // the current frame streamed through LDS in 64-key tiles (B operand).  The
 // epilogue never stores the logits: each lane scales its column by the key's
 // inverse norm and keeps a running row max; 16-lane butterflies finish the max.
-#include "block_select.h"
+#include <algorithm>
+
+#include "segsel.h"
 #include "stlite_internal.h"
 #include "tile_lds.h"
 
@@ -32,25 +34,57 @@ __device__ inline int32_t hist_count(const Layout& lay, int32_t s) {
 }
 
 // Per sequence: the flattened table of historical tokens (frames in order,
-// row-major inside a frame) and the 256-row block descriptors of the rho GEMM.
-__global__ __launch_bounds__(256) void tsg_plan_kernel(RhoArgs a) {
+// row-major inside a frame), the 256-row block descriptors of the rho GEMM and
+// the gate's selection segment (n = N_hist, k = min(B, N_hist)).
+__global__ __launch_bounds__(256) void tsg_plan_kernel(GateArgs a) {
   const Layout& lay = a.lay;
   const int s = blockIdx.x;
-  int32_t hist_base = 0, blk_base = 0;
+  int32_t hist_base = 0, blk_base = 0, chunk_base = 0;
   for (int32_t t = 0; t < s; ++t) {
     const int32_t n = hist_count(lay, t);
     hist_base += n;
     blk_base += (n + kRhoRows - 1) / kRhoRows;
+    chunk_base += (n + kSegChunk - 1) / kSegChunk;
   }
   const int32_t n_hist = hist_count(lay, s);
   const int32_t nb = (n_hist + kRhoRows - 1) / kRhoRows;
   for (int32_t b = threadIdx.x; b < nb; b += blockDim.x) a.blocks[blk_base + b] = HistBlock{s, b, n_hist, hist_base};
+  if (threadIdx.x == 0) {
+    const int32_t B = lay.cu_budget[s + 1] - lay.cu_budget[s];
+    a.info[s] = SeqInfo{n_hist, min(B, n_hist), chunk_base, hist_base};
+    if (s == lay.n_seqs - 1) a.info[s + 1] = SeqInfo{0, 0, chunk_base + (n_hist + kSegChunk - 1) / kSegChunk, 0};
+  }
   const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
   int32_t h = hist_base;
   for (int32_t f = f0; f + 1 < f1; ++f) {
     const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
     for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.hist_tok[h + j] = off + j;
     h += n;
+  }
+}
+
+// gate = 1 on every token (the emit pass then decides the historical ones) and,
+// when asked, rho = 0 everywhere (the rho pass then writes the historical ones).
+__global__ __launch_bounds__(256) void gate_fill_kernel(GateArgs a, size_t n) {
+  const size_t stride = size_t(gridDim.x) * blockDim.x;
+  const size_t i0 = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const bool vec = (reinterpret_cast<uintptr_t>(a.gate) & 3) == 0 &&
+                   (!a.rho_zero_fill || (reinterpret_cast<uintptr_t>(a.rho_zero_fill) & 15) == 0);
+  if (vec) {
+    const size_t n4 = n / 4;
+    for (size_t i = i0; i < n4; i += stride) {
+      reinterpret_cast<uint32_t*>(a.gate)[i] = 0x01010101u;
+      if (a.rho_zero_fill) reinterpret_cast<float4*>(a.rho_zero_fill)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    for (size_t i = 4 * n4 + i0; i < n; i += stride) {
+      a.gate[i] = 1;
+      if (a.rho_zero_fill) a.rho_zero_fill[i] = 0.0f;
+    }
+  } else {
+    for (size_t i = i0; i < n; i += stride) {
+      a.gate[i] = 1;
+      if (a.rho_zero_fill) a.rho_zero_fill[i] = 0.0f;
+    }
   }
 }
 
@@ -254,76 +288,86 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
     }
 }
 
-// Rank-form gate for one (unit, sequence): admit the m = min(B, N_hist)
-// smallest rho in (rho, index) order.
-__global__ __launch_bounds__(kSelThreads) void gate_kernel(GateArgs a) {
-  __shared__ SelectShared sh;
-  const Layout& lay = a.lay;
-  const int s = blockIdx.x, unit = blockIdx.y, tid = threadIdx.x;
-  const int32_t seq_start = lay.cu_seqlens[s], seq_end = lay.cu_seqlens[s + 1];
-  const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
-  const int32_t B = lay.cu_budget[s + 1] - lay.cu_budget[s];
-  const size_t ubase = size_t(unit) * lay.total_tokens;
-  uint32_t* keys = a.keys + ubase + seq_start;  // compact historical keys, in token order
-  const float* rho = a.rho + ubase;
-  uint8_t* gate = a.gate + ubase;
-  float* zf = a.rho_zero_fill ? a.rho_zero_fill + ubase : nullptr;
-
-  int32_t nh = 0;
-  for (int32_t f = f0; f + 1 < f1; ++f) {
-    const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
-    for (int32_t j = tid; j < n; j += kSelThreads) keys[nh + j] = order_key(rho[off + j]);
-    nh += n;
+// Gate keys (rho ascending) of one 4096-row chunk of a sequence's historical
+// tokens, in compact order, and the level-0 histogram.
+__global__ __launch_bounds__(kSegThreads) void gate_keys_kernel(GateArgs a) {
+  __shared__ uint32_t lh[kSegBins];
+  const SegSel& s = a.sel;
+  const int unit = blockIdx.y;
+  const ChunkRef cr = seg_chunk(s, blockIdx.x);
+  const int32_t* htok = a.hist_tok + s.info[cr.seq].aux;
+  const float* rho = a.rho + size_t(unit) * a.lay.total_tokens;
+  uint32_t* keys = seg_keys(s, unit, cr.seq);
+  seg_hist_zero(lh);
+  __syncthreads();
+#pragma unroll 4
+  for (int j = 0; j < kSegPer; ++j) {
+    const int32_t i = cr.begin + j * kSegThreads + threadIdx.x;
+    const bool in = i < cr.end;
+    uint32_t key = 0;
+    if (in) {
+      key = order_key(rho[htok[i]]);
+      keys[i] = key;
+    }
+    seg_hist_add(lh, in, key >> 21);
   }
   __syncthreads();
-  const int32_t m = min(B, nh);
-  uint32_t T = 0;
-  int32_t need = 0;
-  if (m > 0) T = block_radix_select(keys, nh, m, sh, &need);
-  if (tid == 0 && a.tau) a.tau[size_t(unit) * lay.n_seqs + s] = m > 0 ? order_key_value(T) : __builtin_nanf("");
+  seg_hist_flush(lh, seg_hist(s, unit, cr.seq, 0));
+}
 
-  int32_t running_eq = 0, h = 0, prev = seq_start;
-  for (int32_t f = f0; f <= f1; ++f) {
-    const bool is_frame = f < f1;
-    const int32_t off = is_frame ? lay.frame_meta[3 * f] : seq_end;
-    const int32_t n = is_frame ? frame_size(lay, f) : 0;
-    for (int32_t j = prev + tid; j < off; j += kSelThreads) {  // text before this frame
-      gate[j] = 1;
-      if (zf) zf[j] = 0.0f;
-    }
-    if (is_frame && f == f1 - 1) {  // current frame: exempt from the gate
-      for (int32_t j = tid; j < n; j += kSelThreads) {
-        gate[off + j] = 1;
-        if (zf) zf[off + j] = 0.0f;
-      }
-    } else if (is_frame) {
-      for (int32_t base = 0; base < n; base += kSelThreads) {
-        const int32_t j = base + tid;
-        const bool in = j < n;
-        const uint32_t key = in ? keys[h + j] : 0u;
-        const bool eq = in && m > 0 && key == T;
-        int32_t eq_tot;
-        const int32_t eq_incl = block_inclusive_scan(eq ? 1 : 0, sh.wave_tot, &eq_tot);
-        const bool take = (in && m > 0 && key < T) || (eq && running_eq + eq_incl - 1 < need);
-        if (in) gate[off + j] = take ? 1 : 0;
-        running_eq += eq_tot;
-      }
-      h += n;
-    }
-    prev = off + n;
+// gate = 1 for the selected historical tokens, 0 for the others.
+__global__ __launch_bounds__(kSegThreads) void gate_emit_kernel(GateArgs a) {
+  __shared__ int32_t scratch[kSegThreads / 64];
+  const SegSel& s = a.sel;
+  const int unit = blockIdx.y;
+  const ChunkRef cr = seg_chunk(s, blockIdx.x);
+  TakeChunk tc;
+  take_chunk(s, unit, cr, scratch, tc);
+  const int32_t* htok = a.hist_tok + s.info[cr.seq].aux;
+  uint8_t* gate = a.gate + size_t(unit) * a.lay.total_tokens;
+  const int32_t i0 = cr.begin + threadIdx.x * kSegPer;
+#pragma unroll
+  for (int i = 0; i < kSegPer; ++i)
+    if (i0 + i < cr.end) gate[htok[i0 + i]] = tc.take[i] ? 1 : 0;
+}
+
+hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
+  hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs), dim3(256), 0, stream, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t n = size_t(g.lay.n_units) * g.lay.total_tokens;
+  const unsigned blocks = unsigned(std::min<size_t>((n / 4 + 255) / 256 + 1, 8192));
+  hipLaunchKernelGGL(gate_fill_kernel, dim3(blocks), dim3(256), 0, stream, g, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
+  const SegSel& s = g.sel;
+  const int32_t U = g.lay.n_units;
+  hipError_t e = launch_segsel_zero(s, U, stream);
+  if (e != hipSuccess) return e;
+  const dim3 chunk_grid(s.chunks_per_unit, U);
+  if (s.chunks_per_unit > 0) {
+    hipLaunchKernelGGL(gate_keys_kernel, chunk_grid, dim3(kSegThreads), 0, stream, g);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
+  e = launch_segsel_middle(s, U, stream);
+  if (e != hipSuccess || s.chunks_per_unit == 0) return e;
+  hipLaunchKernelGGL(gate_emit_kernel, chunk_grid, dim3(kSegThreads), 0, stream, g);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) {
-  hipLaunchKernelGGL(gate_kernel, dim3(g.lay.n_seqs, g.lay.n_units), dim3(kSelThreads), 0, stream, g);
-  return hipGetLastError();
+  hipError_t e = launch_gate_prologue(g, stream);
+  if (e != hipSuccess) return e;
+  return launch_gate_select(g, stream);
 }
 
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
-  hipLaunchKernelGGL(tsg_plan_kernel, dim3(r.lay.n_seqs), dim3(256), 0, stream, r);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_gate_prologue(g, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(cur_norms_kernel, dim3(r.lay.n_seqs, r.lay.n_units), dim3(256), 0, stream, r);
   e = hipGetLastError();
@@ -333,7 +377,7 @@ hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stre
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return launch_tsg_threshold(g, stream);
+  return launch_gate_select(g, stream);
 }
 
 }  // namespace stlite
