@@ -2,89 +2,183 @@
 //   H_{u,v} = mean over the in-grid Moore neighbours n of cos(h_{u,v}, h_n),
 //   Phi = 1 - H  (0 when a frame is 1x1; 0 on text tokens).
 //
-// A work-group stages an 8 x 16 tile of a frame's patch grid plus its one-cell
-// halo (10 x 18 keys, 49 KB) in LDS, computes the 180 inverse norms once, and
-// then gives each interior cell to 16 lanes: every lane keeps 8 dimensions of
-// the centre key and, for each neighbour, adds rn_n * (its 8-dimension partial
-// dot), so one 16-lane reduction per cell yields sum_n cos * ||centre||.
-// Each key is read from HBM once per tile; halo re-reads hit L2.
+// One wave sweeps a vertical strip of a frame row by row.  A strip is 16
+// loaded columns: 14 output columns plus one halo column on each side.  Four
+// lanes share a cell, each holding 32 of the 128 dimensions, so a dot product
+// is 16 v_dot2 per lane and a two-step quad reduction.
+//
+// Each unordered neighbour pair is evaluated once: a cell computes only its
+// forward cosines E (r, c+1), S (r+1, c), SE (r+1, c+1) and SW (r+1, c-1).
+// Row r's mean combines its own forward cosines, its west neighbour's E, and
+// the previous row's S / SE / SW carried in registers.
+//
+// Rows stream into a four-slot LDS ring by direct global->LDS DMA, two rows
+// ahead of the row being combined, so every key is read from HBM once per
+// strip.  The strips of one frame are given to work-groups that land on the
+// same XCD, where the halo columns hit the shared L2.
 #include "stlite_internal.h"
+#include "tile_lds.h"
 
 namespace stlite {
 namespace {
 
-constexpr int kTU = 8, kTV = 16;
-constexpr int kHU = kTU + 2, kHV = kTV + 2;
-constexpr int kCells = kHU * kHV;
-constexpr int kCStride = kHeadDim + 8;
+constexpr int kStripCells = 16;  // loaded columns per strip (one per lane quad)
+constexpr int kStripOut = 14;    // output columns per strip
+constexpr int kRowElems = kStripCells * kHeadDim;
+constexpr int kRowLoads = kStripCells * kHeadDim * 2 / (64 * 16);  // wave-loads of 16 B per lane: 4
 
-__device__ inline float dot8(uint4 a, uint4 b) {
-  float s = 0.0f;
-  s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.x), __builtin_bit_cast(bf16x2_t, b.x), s, false);
-  s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.y), __builtin_bit_cast(bf16x2_t, b.y), s, false);
-  s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.z), __builtin_bit_cast(bf16x2_t, b.z), s, false);
-  s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.w), __builtin_bit_cast(bf16x2_t, b.w), s, false);
-  return s;
-}
+// The 16-byte chunk ch (dims 8ch .. 8ch+7) of loaded cell g sits at slot
+// ch ^ 4 (g & 1): lanes 0..7 of a b128 read then cover all 32 banks.
+__device__ inline int chunk_slot(int g, int ch) { return ch ^ ((g & 1) << 2); }
 
-__global__ __launch_bounds__(256) void css_kernel(CssArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t cells[kCells * kCStride];
-  __shared__ float rn[kCells];
-  const Layout& lay = a.lay;
-  const int f = blockIdx.x, split = blockIdx.y, unit = blockIdx.z;
-  const int32_t off = lay.frame_meta[3 * f], R = lay.frame_meta[3 * f + 1], C = lay.frame_meta[3 * f + 2];
-  const int32_t ntx = (C + kTV - 1) / kTV, nty = (R + kTU - 1) / kTU;
-  const uint16_t* kframe = a.k + (size_t(unit) * lay.total_tokens + off) * kHeadDim;
-  float* out = a.phi + size_t(unit) * lay.total_tokens + off;
-  const int tid = threadIdx.x, group = tid >> 4, gl = tid & 15;
-
-  for (int32_t t = split; t < nty * ntx; t += a.splits) {
-    const int32_t u0 = (t / ntx) * kTU, v0 = (t % ntx) * kTV;
-    __syncthreads();
-    for (int i = tid; i < kCells * 16; i += blockDim.x) {
-      const int cell = i >> 4, part = i & 15;
-      const int32_t u = u0 - 1 + cell / kHV, v = v0 - 1 + cell % kHV;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (u >= 0 && u < R && v >= 0 && v < C)
-        val = *reinterpret_cast<const uint4*>(kframe + size_t(u * C + v) * kHeadDim + part * 8);
-      *reinterpret_cast<uint4*>(cells + cell * kCStride + part * 8) = val;
-    }
-    __syncthreads();
-    for (int cell = group; cell < kCells; cell += 16) {
-      const uint4 x = *reinterpret_cast<const uint4*>(cells + cell * kCStride + gl * 8);
-      float ss = dot8(x, x);
+// DMA of one strip row (16 cells, column-clamped) into `dst`.
+__device__ inline void row_dma(const uint16_t* kframe, int32_t row, int32_t c0, int32_t C, uint16_t* dst) {
+  const int lane = threadIdx.x & 63;
+  // The slot being refilled was last read two steps ago; make sure those LDS
+  // reads have completed before the DMA can land.
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
-      if (gl == 0) rn[cell] = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
-    }
-    __syncthreads();
-    for (int ic = group; ic < kTU * kTV; ic += 16) {
-      const int iu = ic / kTV, iv = ic % kTV;
-      const int32_t u = u0 + iu, v = v0 + iv;
-      const int centre = (iu + 1) * kHV + (iv + 1);
-      const uint4 cx = *reinterpret_cast<const uint4*>(cells + centre * kCStride + gl * 8);
-      float acc = 0.0f;
-      int cnt = 0;
-#pragma unroll
-      for (int du = -1; du <= 1; ++du)
-#pragma unroll
-        for (int dv = -1; dv <= 1; ++dv) {
-          if (du == 0 && dv == 0) continue;
-          const int32_t uu = u + du, vv = v + dv;
-          if (uu < 0 || uu >= R || vv < 0 || vv >= C) continue;
-          const int nb = centre + du * kHV + dv;
-          const uint4 nx = *reinterpret_cast<const uint4*>(cells + nb * kCStride + gl * 8);
-          acc = fmaf(dot8(cx, nx), rn[nb], acc);
-          ++cnt;
-        }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) acc += __shfl_xor(acc, o);
-      if (gl == 0 && u < R && v < C) out[u * C + v] = cnt > 0 ? 1.0f - acc * rn[centre] / float(cnt) : 0.0f;
-    }
+  for (int m = 0; m < kRowLoads; ++m) {
+    const int g = 4 * m + (lane >> 4);
+    const int slot = lane & 15;
+    const int ch = chunk_slot(g, slot);  // the mapping is its own inverse
+    const int32_t col = min(max(c0 - 1 + g, 0), C - 1);
+    // The LDS address goes through an opaque copy, so the compiler does not
+    // tie the DMA to the ring array and add its own (full) vmcnt waits before
+    // the ring is read; the kernel waits for exactly the rows it needs.
+    uint32_t lds = uint32_t(reinterpret_cast<uintptr_t>(dst + 4 * m * kHeadDim));
+    asm volatile("" : "+s"(lds));
+    __builtin_amdgcn_global_load_lds(kframe + (size_t(row) * C + col) * kHeadDim + ch * 8,
+                                     (lds_void_t)(uintptr_t)lds, 16, 0, 0);
   }
 }
 
-// phi = 0 on every text token (the gaps between and after the frames).
+// Lane (g, s) holds chunks s, s+4, s+8, s+12 of cell g.
+struct Slice {
+  uint4 c[4];
+};
+
+__device__ inline Slice read_slice(const uint16_t* row, int g, int s) {
+  Slice x;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    x.c[j] = *reinterpret_cast<const uint4*>(row + g * kHeadDim + chunk_slot(g, 4 * j + s) * 8);
+  return x;
+}
+
+__device__ inline float dot_slice(const Slice& a, const Slice& b) {
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t wa[4] = {a.c[j].x, a.c[j].y, a.c[j].z, a.c[j].w};
+    const uint32_t wb[4] = {b.c[j].x, b.c[j].y, b.c[j].z, b.c[j].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, wa[i]), __builtin_bit_cast(bf16x2_t, wb[i]), s,
+                                          false);
+  }
+  return s;
+}
+
+// Sum over the four lanes of a quad (lanes 4g .. 4g+3).
+__device__ inline float quad_sum(float x) {
+  x += __shfl_xor(x, 1);
+  x += __shfl_xor(x, 2);
+  return x;
+}
+
+__device__ inline float inv_norm(float ss) { return ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f; }
+
+__global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t ring0[kRowElems], ring1[kRowElems], ring2[kRowElems],
+      ring3[kRowElems];
+  const Layout& lay = a.lay;
+  const int unit = blockIdx.y;
+  // XCD-aware order: work-groups i, i + 8, i + 16, ... share an XCD, so they
+  // take consecutive strips (the grid width is a multiple of 8).
+  const int32_t per_xcd = int32_t(gridDim.x) >> 3;
+  const int32_t logical = int32_t(blockIdx.x & 7) * per_xcd + int32_t(blockIdx.x >> 3);
+  const int32_t f = logical / a.strips, strip = logical - f * a.strips;
+  if (f >= lay.n_frames) return;
+  const int32_t off = lay.frame_meta[3 * f], R = lay.frame_meta[3 * f + 1], C = lay.frame_meta[3 * f + 2];
+  const int32_t c0 = strip * kStripOut;
+  if (c0 >= C) return;
+
+  const int lane = threadIdx.x & 63, g = lane >> 2, s = lane & 3;
+  const int32_t col = c0 - 1 + g;
+  const bool out_lane = g >= 1 && g <= kStripOut && col < C;
+  const bool has_w = col >= 1, has_e = col + 1 < C;
+  const int32_t ncols = 1 + (col > 0 ? 1 : 0) + (col < C - 1 ? 1 : 0);
+  const uint16_t* kframe = a.k + (size_t(unit) * lay.total_tokens + off) * kHeadDim;
+  // Phi of the frame through a buffer resource: lanes without an output store
+  // to an offset past the end, which the hardware drops, so the store needs no
+  // branch (and the number of memory operations per step stays fixed).
+  const uint32_t frame_bytes = uint32_t(R) * uint32_t(C) * 4u;
+  const __amdgpu_buffer_rsrc_t phi_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(a.phi + size_t(unit) * lay.total_tokens + off, 0, frame_bytes, 0x00020000);
+  const int ge = min(g + 1, kStripCells - 1), gw = max(g - 1, 0);
+
+  // Every step issues one row (rows past the end repeat row R-1 and hit L2),
+  // so the number of loads in flight is the same on every path: 2 rows.
+  row_dma(kframe, 0, c0, C, ring0);
+  row_dma(kframe, min(1, R - 1), c0, C, ring1);
+  row_dma(kframe, min(2, R - 1), c0, C, ring2);
+
+  // Row 0: own slice and inverse norm.
+  wait_vmcnt<2 * kRowLoads>();
+  Slice own = read_slice(ring0, g, s);
+  float rn_own = inv_norm(quad_sum(dot_slice(own, own)));
+  float carry = 0.0f;  // sum of row r-1's cosines with (r, col)
+
+  auto step = [&](int32_t r, uint16_t* cur, uint16_t* nxt, uint16_t* issue_dst) {
+    const bool has_s = r + 1 < R;
+    row_dma(kframe, min(r + 3, R - 1), c0, C, issue_dst);
+    wait_vmcnt<2 * kRowLoads>();  // row r+1 has landed
+    // East neighbour in this row; norms of the east cell come by shuffle.
+    const Slice e = read_slice(cur, ge, s);
+    const float dE = quad_sum(dot_slice(own, e));
+    const float rnE = __shfl(rn_own, (ge << 2) | s);
+    const float cE = has_e ? dE * rn_own * rnE : 0.0f;
+    // Row r+1 (on the last row the slot holds a repeat of row R-1; masked).
+    const Slice down = read_slice(nxt, g, s);
+    const Slice se = read_slice(nxt, ge, s);
+    const Slice sw = read_slice(nxt, gw, s);
+    const float rn_down = inv_norm(quad_sum(dot_slice(down, down)));
+    const float dS = quad_sum(dot_slice(own, down));
+    const float dSE = quad_sum(dot_slice(own, se));
+    const float dSW = quad_sum(dot_slice(own, sw));
+    const float rnSE = __shfl(rn_down, (ge << 2) | s);
+    const float rnSW = __shfl(rn_down, (gw << 2) | s);
+    const float cS = has_s ? dS * rn_own * rn_down : 0.0f;
+    const float cSE = has_s && has_e ? dSE * rn_own * rnSE : 0.0f;
+    const float cSW = has_s && has_w ? dSW * rn_own * rnSW : 0.0f;
+    // Cosines owned by the west / east neighbours of this cell.
+    const float cE_w = __shfl(cE, (gw << 2) | s);
+    const float cSE_w = __shfl(cSE, (gw << 2) | s);
+    const float cSW_e = __shfl(cSW, (ge << 2) | s);
+    const float H = carry + cE + cS + cSE + cSW + (has_w ? cE_w : 0.0f);
+    const int32_t nrows = 1 + (r > 0 ? 1 : 0) + (has_s ? 1 : 0);
+    const int32_t nn = nrows * ncols - 1;
+    const bool store = r < R && out_lane && s == 0;
+    const uint32_t byte_off = store ? uint32_t(r * C + col) * 4u : frame_bytes;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(nn > 0 ? 1.0f - H / float(nn) : 0.0f), phi_rsrc, byte_off,
+                                          0, 0);
+    carry = cS + (has_w ? cSE_w : 0.0f) + (has_e ? cSW_e : 0.0f);
+    own = down;
+    rn_own = rn_down;
+  };
+
+  // Row r lives in slot r % 4; unrolled by four so each slot is a distinct
+  // array.  Steps past the last row only keep the load count uniform.
+  for (int32_t r = 0; r < R; r += 4) {
+    step(r, ring0, ring1, ring3);
+    step(r + 1, ring1, ring2, ring0);
+    step(r + 2, ring2, ring3, ring1);
+    step(r + 3, ring3, ring0, ring2);
+  }
+  wait_vmcnt<0>();  // no DMA into LDS may outlive the work-group
+}
+
 __global__ __launch_bounds__(256) void css_text_kernel(CssArgs a) {
   const Layout& lay = a.lay;
   const int s = blockIdx.x, unit = blockIdx.y;
@@ -104,7 +198,9 @@ hipError_t launch_css(const CssArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.lay.n_frames == 0) return e;
-  hipLaunchKernelGGL(css_kernel, dim3(a.lay.n_frames, a.splits, a.lay.n_units), dim3(256), 0, stream, a);
+  const int64_t logical = int64_t(a.lay.n_frames) * a.strips;  // a.strips: max over frames of ceil(C / 14)
+  const int64_t grid_x = (logical + 7) / 8 * 8;
+  hipLaunchKernelGGL(css_kernel, dim3(unsigned(grid_x), a.lay.n_units), dim3(64), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -324,7 +324,10 @@ stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, fl
   a.lay = make_layout(p);
   a.k = k;
   a.phi = phi;
-  a.splits = 8;
+  int32_t strips = 1;
+  for (int32_t fi = 0; fi < p->n_frames; ++fi)
+    strips = std::max<int32_t>(strips, (p->h_frame_meta[3 * fi + 2] + 13) / 14);
+  a.strips = strips;
   return hip_status(launch_css(a, static_cast<hipStream_t>(stream)), "css_saliency launch");
 }
 

@@ -120,7 +120,7 @@ struct CssArgs {
   Layout lay;
   const uint16_t* k;
   float* phi;
-  int32_t splits;        // work-groups per frame
+  int32_t strips;        // largest number of 14-column strips in a frame
 };
 
 struct SelectArgs {
