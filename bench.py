@@ -64,8 +64,11 @@ def work_model(w, lay, cu_budget):
         # QK^T of the window rows against every key, once (the pass forms it twice)
         "score_window": {"bound": "mfma", "flops": units * 2.0 * rows * L_tot * d,
                          "bytes": units * (2.0 * L_tot * d * 2 + 4.0 * L_tot)},
-        "tsg_gate": {"bound": "mfma", "flops": units * 2.0 * hist_cur * d,
-                     "bytes": units * (2.0 * (n_hist + n_cur) * d + 4.0 * L_tot + 1.0 * L_tot)},
+        # N_hist x N_cur x d cosine contraction; K_hist and K_cur read once, rho written
+        "tsg_rho": {"bound": "mfma", "flops": units * 2.0 * hist_cur * d,
+                    "bytes": units * (2.0 * (n_hist + n_cur) * d + 4.0 * L_tot)},
+        # rho of the historical tokens read, the gate written
+        "tsg_threshold": {"bound": "hbm", "flops": 0.0, "bytes": units * (4.0 * n_hist + 1.0 * L_tot)},
         "css_saliency": {"bound": "hbm", "flops": units * 2.0 * 5 * n_vis * d,
                          "bytes": units * (2.0 * n_vis * d + 4.0 * L_tot)},
         "select_topk": {"bound": "hbm", "flops": 0.0,
@@ -84,6 +87,55 @@ def roofline_entry(model, ms):
     ach = model["bytes"] / s / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(ach / PEAK_HBM_GBS, 4), "ms": round(ms, 4)}
+
+
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = {  # the sources a kernel's counters depend on
+    "rho_kernel": ["paper_2603_00188_amd/csrc/tsg.hip", "paper_2603_00188_amd/csrc/tile_lds.h",
+                   "paper_2603_00188_amd/csrc/stlite_internal.h"],
+}
+
+
+def source_digest(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES.get(kernel, []):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    profiles/<kernel>_<workload>_traffic.md (FETCH_SIZE + WRITE_SIZE, each scaled
+    by the copy-kernel calibration), or None when there is none or the kernel's
+    sources changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_digest") != source_digest(kernel):
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_probe(nbytes):
+    """A plain device-to-device copy of known size, for scaling the counters."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), flush=True)
 
 
 def cpu_baseline(w, case_inputs, budget_s=12.0, max_units=8):
@@ -127,6 +179,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a device copy of BYTES bytes three times (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         sys.stderr.write("bench.py measures one GPU only: the compression pass is per (layer, kv head) and "
@@ -139,6 +193,9 @@ def main():
 
     S.load()  # fails loudly without the HIP library
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     w = W.config(args.config)
     log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
     inputs = W.make_inputs(w, workers=16)
@@ -151,29 +208,34 @@ def main():
     dv = torch.from_numpy(v.view(np.int16)).cuda()
     dq = torch.from_numpy(q.view(np.int16)).cuda()
     out = S.Buffers(prob, keep_stages=False)
+    rho = torch.empty_like(out.a_base)
     torch.cuda.synchronize()
     log(f"inputs resident: K+V {2 * dk.numel() * 2 / 1e9:.2f} GB")
 
     stream = torch.cuda.current_stream()
-    names = ["score_window", "tsg_gate", "css_saliency", "select_topk", "compact_kv"]
+    names = ["score_window", "tsg_rho", "tsg_threshold", "css_saliency", "select_topk", "compact_kv"]
 
     def step(ev=None):
+        # the TSG step as its two calls (rho, then threshold and gate), so that
+        # the rho GEMM is timed on its own
         if ev: ev[0].record(stream)
         S.stlite_score_window(prob, dq, dk, out.a_base, out.ws, stream)
         if ev: ev[1].record(stream)
-        S.stlite_tsg_gate(prob, dk, None, None, out.gate, out.ws, stream)
+        S.stlite_tsg_rho(prob, dk, rho, out.ws, stream)
         if ev: ev[2].record(stream)
-        S.stlite_css_saliency(prob, dk, out.phi, stream)
+        S.stlite_tsg_threshold(prob, rho, None, out.gate, out.ws, stream)
         if ev: ev[3].record(stream)
-        S.stlite_select_topk(prob, out.a_base, out.phi, out.gate, w.alpha, out.kept, None, out.ws, stream)
+        S.stlite_css_saliency(prob, dk, out.phi, stream)
         if ev: ev[4].record(stream)
-        S.stlite_compact_kv(prob, dk, dv, out.kept, out.k_out, out.v_out, stream)
+        S.stlite_select_topk(prob, out.a_base, out.phi, out.gate, w.alpha, out.kept, None, out.ws, stream)
         if ev: ev[5].record(stream)
+        S.stlite_compact_kv(prob, dk, dv, out.kept, out.k_out, out.v_out, stream)
+        if ev: ev[6].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -189,12 +251,13 @@ def main():
     model = work_model(w, lay, cu_budget)
     stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
     dom = max(names, key=lambda n: per_call[n])
-    kernel_of = {"score_window": "score_rowstats + score_colsum (two MFMA passes)",
-                 "tsg_gate": "rho_kernel (+ cur_norms, gate_kernel in the same call)",
-                 "css_saliency": "css_kernel", "select_topk": "select_kernel", "compact_kv": "compact_kernel"}
+    kernel_of = {"score_window": "score_rowstats_kernel + score_colsum_kernel",
+                 "tsg_rho": "rho_kernel", "tsg_threshold": "gate_keys/segsel/gate_emit kernels",
+                 "css_saliency": "css_kernel", "select_topk": "select_keys/segsel/select_emit kernels",
+                 "compact_kv": "compact_kernel"}
     roof = dict(stages[dom])
     roof.pop("ms")
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(kernel_of[dom], w.name)
     roof["kernel"] = kernel_of[dom]
     roof["call"] = "stlite_" + dom
     roof["ms_per_launch"] = round(per_call[dom], 4)

@@ -81,7 +81,8 @@ typedef enum stlite_call {
   STLITE_CALL_CSS_SALIENCY = 2,
   STLITE_CALL_SELECT_TOPK = 3,
   STLITE_CALL_COMPACT_KV = 4,
-  STLITE_CALL_TSG_THRESHOLD = 5
+  STLITE_CALL_TSG_THRESHOLD = 5,
+  STLITE_CALL_TSG_RHO = 6
 } stlite_call;
 
 /*
@@ -172,6 +173,15 @@ stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, fl
 stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float* rho,
                               float* tau, uint8_t* gate, void* workspace,
                               size_t workspace_bytes, void* stream);
+
+/*
+ * The similarity half of stlite_tsg_gate (Sec. TSG, the frame-similarity
+ * maximum): rho [units][total_tokens] receives rho on historical tokens, with
+ * the same clamp and snap, and 0 elsewhere.  rho is required.  Together with
+ * stlite_tsg_threshold it computes exactly what stlite_tsg_gate computes.
+ */
+stlite_status stlite_tsg_rho(const stlite_problem* p, const uint16_t* k, float* rho,
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * The threshold-and-gate half of stlite_tsg_gate on a caller-supplied rho

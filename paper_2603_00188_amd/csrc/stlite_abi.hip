@@ -115,15 +115,14 @@ SegSel seg_carve(const stlite_problem* p, const Facts& f, int64_t chunks, const 
 
 size_t info_bytes(const stlite_problem* p) { return align_up(size_t(p->n_seqs + 1) * sizeof(SeqInfo)); }
 
-// Gate workspace after the rho slabs: historical-token table, rho block table,
-// segment table, then the selection.
-size_t gate_tail_bytes(const stlite_problem* p, const Facts& f) {
+// TSG plan: historical-token table, rho block table, gate segment table.
+size_t plan_bytes(const stlite_problem* p, const Facts& f) {
   return align_up(size_t(p->total_tokens) * sizeof(int32_t)) +
-         align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock)) + info_bytes(p) +
-         seg_bytes(p, f, f.gate_chunks);
+         align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock)) + info_bytes(p);
 }
 
-void gate_carve(const stlite_problem* p, const Facts& f, char* w, GateArgs& g) {
+// Carves the plan at w and, when `select` is set, the gate's selection after it.
+void gate_carve(const stlite_problem* p, const Facts& f, char* w, bool select, GateArgs& g) {
   g.hist_tok = reinterpret_cast<int32_t*>(w);
   w += align_up(size_t(p->total_tokens) * sizeof(int32_t));
   g.blocks = reinterpret_cast<HistBlock*>(w);
@@ -131,6 +130,21 @@ void gate_carve(const stlite_problem* p, const Facts& f, char* w, GateArgs& g) {
   g.info = reinterpret_cast<SeqInfo*>(w);
   w += info_bytes(p);
   g.sel = seg_carve(p, f, f.gate_chunks, g.info, w);
+  if (!select) g.sel.keys = nullptr;
+}
+
+RhoArgs rho_args(const stlite_problem* p, const Facts& f, const uint16_t* k, float* rho, float* rn_cur,
+                 const GateArgs& g) {
+  RhoArgs r;
+  r.lay = g.lay;
+  r.k = k;
+  r.rn_cur = rn_cur;
+  r.rho = rho;
+  r.hist_tok = g.hist_tok;
+  r.blocks = g.blocks;
+  r.total_hist_blocks = int32_t(f.total_hist_blocks);
+  r.max_cur = int32_t(f.max_cur);
+  return r;
 }
 
 Layout make_layout(const stlite_problem* p) {
@@ -266,11 +280,15 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
                align_up(size_t(f.units) * f.total_chunks * sizeof(int32_t));
       break;
     case STLITE_CALL_TSG_GATE:
-      // rho scratch, current-frame norms, then the threshold's workspace
-      *bytes = 2 * align_up(per_token * sizeof(float)) + gate_tail_bytes(p, f);
+      // rho scratch, current-frame norms, plan, selection
+      *bytes = 2 * align_up(per_token * sizeof(float)) + plan_bytes(p, f) + seg_bytes(p, f, f.gate_chunks);
+      break;
+    case STLITE_CALL_TSG_RHO:
+      // current-frame norms, plan
+      *bytes = align_up(per_token * sizeof(float)) + plan_bytes(p, f);
       break;
     case STLITE_CALL_TSG_THRESHOLD:
-      *bytes = gate_tail_bytes(p, f);
+      *bytes = plan_bytes(p, f) + seg_bytes(p, f, f.gate_chunks);
       break;
     case STLITE_CALL_SELECT_TOPK:
       *bytes = info_bytes(p) + seg_bytes(p, f, f.sel_chunks);
@@ -345,18 +363,29 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
   g.rho = rho ? rho : reinterpret_cast<float*>(w);
   g.rho_zero_fill = rho;
   g.gate = gate;
-  gate_carve(p, f, w + 2 * slab, g);
+  gate_carve(p, f, w + 2 * slab, true, g);
   g.sel.pivot_value = tau;
-  RhoArgs r;
-  r.lay = g.lay;
-  r.k = k;
-  r.rn_cur = reinterpret_cast<float*>(w + slab);
-  r.rho = const_cast<float*>(g.rho);
-  r.hist_tok = g.hist_tok;
-  r.blocks = g.blocks;
-  r.total_hist_blocks = int32_t(f.total_hist_blocks);
-  r.max_cur = int32_t(f.max_cur);
+  const RhoArgs r = rho_args(p, f, k, const_cast<float*>(g.rho), reinterpret_cast<float*>(w + slab), g);
   return hip_status(launch_tsg_gate(r, g, static_cast<hipStream_t>(stream)), "tsg_gate launch");
+}
+
+stlite_status stlite_tsg_rho(const stlite_problem* p, const uint16_t* k, float* rho, void* ws, size_t ws_bytes,
+                             void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_TSG_RHO, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (!k || !rho) return fail(STLITE_ERR_INVALID_ARG, "k and rho must be non-NULL");
+  if (!aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "k must be 16-byte aligned");
+  const Facts f = derive(p);
+  const size_t slab = align_up(size_t(f.units) * p->total_tokens * sizeof(float));
+  char* w = static_cast<char*>(ws);
+  GateArgs g;
+  g.lay = make_layout(p);
+  g.rho = rho;
+  g.rho_zero_fill = rho;
+  g.gate = nullptr;
+  gate_carve(p, f, w + slab, false, g);
+  const RhoArgs r = rho_args(p, f, k, rho, reinterpret_cast<float*>(w), g);
+  return hip_status(launch_tsg_rho(r, g, static_cast<hipStream_t>(stream)), "tsg_rho launch");
 }
 
 stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, float* tau, uint8_t* gate,
@@ -370,7 +399,7 @@ stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, fl
   g.rho = rho;
   g.rho_zero_fill = nullptr;
   g.gate = gate;
-  gate_carve(p, f, static_cast<char*>(ws), g);
+  gate_carve(p, f, static_cast<char*>(ws), true, g);
   g.sel.pivot_value = tau;
   return hip_status(launch_tsg_threshold(g, static_cast<hipStream_t>(stream)), "tsg_threshold launch");
 }

@@ -109,7 +109,7 @@ struct GateArgs {
   Layout lay;
   const float* rho;      // [units][L] (historical entries read)
   float* rho_zero_fill;  // nullable: every entry of this array is zeroed before rho is written
-  uint8_t* gate;         // [units][L]
+  uint8_t* gate;         // nullable for the rho-only call; [units][L]
   int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
   HistBlock* blocks;     // workspace [total_hist_blocks]
   SeqInfo* info;         // workspace [n_seqs + 1]: segment table (n = N_hist, k = min(B, N_hist))
@@ -147,6 +147,7 @@ struct CompactArgs {
 hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream);
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
+hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 hipError_t launch_css(const CssArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);

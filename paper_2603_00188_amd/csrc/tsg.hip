@@ -33,58 +33,64 @@ __device__ inline int32_t hist_count(const Layout& lay, int32_t s) {
   return n;
 }
 
-// Per sequence: the flattened table of historical tokens (frames in order,
-// row-major inside a frame), the 256-row block descriptors of the rho GEMM and
-// the gate's selection segment (n = N_hist, k = min(B, N_hist)).
+// Plan of the TSG pass.  Work-groups 0 .. n_seqs-1: per sequence, the 256-row
+// block descriptors of the rho GEMM and the gate's selection segment
+// (n = N_hist, k = min(B, N_hist)).  Work-groups n_seqs + f: the historical
+// token table entries of frame f (frames in order, row-major inside a frame),
+// unless f is its sequence's current frame.
 __global__ __launch_bounds__(256) void tsg_plan_kernel(GateArgs a) {
   const Layout& lay = a.lay;
-  const int s = blockIdx.x;
-  int32_t hist_base = 0, blk_base = 0, chunk_base = 0;
-  for (int32_t t = 0; t < s; ++t) {
-    const int32_t n = hist_count(lay, t);
-    hist_base += n;
-    blk_base += (n + kRhoRows - 1) / kRhoRows;
-    chunk_base += (n + kSegChunk - 1) / kSegChunk;
+  if (int32_t(blockIdx.x) < lay.n_seqs) {
+    const int s = blockIdx.x;
+    int32_t hist_base = 0, blk_base = 0, chunk_base = 0;
+    for (int32_t t = 0; t < s; ++t) {
+      const int32_t n = hist_count(lay, t);
+      hist_base += n;
+      blk_base += (n + kRhoRows - 1) / kRhoRows;
+      chunk_base += (n + kSegChunk - 1) / kSegChunk;
+    }
+    const int32_t n_hist = hist_count(lay, s);
+    const int32_t nb = (n_hist + kRhoRows - 1) / kRhoRows;
+    for (int32_t b = threadIdx.x; b < nb; b += blockDim.x) a.blocks[blk_base + b] = HistBlock{s, b, n_hist, hist_base};
+    if (threadIdx.x == 0) {
+      const int32_t B = lay.cu_budget[s + 1] - lay.cu_budget[s];
+      a.info[s] = SeqInfo{n_hist, min(B, n_hist), chunk_base, hist_base};
+      if (s == lay.n_seqs - 1) a.info[s + 1] = SeqInfo{0, 0, chunk_base + (n_hist + kSegChunk - 1) / kSegChunk, 0};
+    }
+    return;
   }
-  const int32_t n_hist = hist_count(lay, s);
-  const int32_t nb = (n_hist + kRhoRows - 1) / kRhoRows;
-  for (int32_t b = threadIdx.x; b < nb; b += blockDim.x) a.blocks[blk_base + b] = HistBlock{s, b, n_hist, hist_base};
-  if (threadIdx.x == 0) {
-    const int32_t B = lay.cu_budget[s + 1] - lay.cu_budget[s];
-    a.info[s] = SeqInfo{n_hist, min(B, n_hist), chunk_base, hist_base};
-    if (s == lay.n_seqs - 1) a.info[s + 1] = SeqInfo{0, 0, chunk_base + (n_hist + kSegChunk - 1) / kSegChunk, 0};
-  }
-  const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
-  int32_t h = hist_base;
-  for (int32_t f = f0; f + 1 < f1; ++f) {
-    const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
-    for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.hist_tok[h + j] = off + j;
-    h += n;
-  }
+  const int32_t f = int32_t(blockIdx.x) - lay.n_seqs;
+  int32_t s = 0;  // sequence of frame f
+  while (lay.cu_frames[s + 1] <= f) ++s;
+  if (f == lay.cu_frames[s + 1] - 1) return;  // current frame: not historical
+  int32_t h = 0;  // historical rows before frame f, over all sequences
+  for (int32_t t = 0; t < s; ++t) h += hist_count(lay, t);
+  for (int32_t g = lay.cu_frames[s]; g < f; ++g) h += frame_size(lay, g);
+  const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
+  for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.hist_tok[h + j] = off + j;
 }
 
-// gate = 1 on every token (the emit pass then decides the historical ones) and,
-// when asked, rho = 0 everywhere (the rho pass then writes the historical ones).
+// gate = 1 on every token (the emit pass then decides the historical ones) and
+// rho = 0 everywhere (the rho pass then writes the historical ones); either
+// pointer may be null.
 __global__ __launch_bounds__(256) void gate_fill_kernel(GateArgs a, size_t n) {
   const size_t stride = size_t(gridDim.x) * blockDim.x;
   const size_t i0 = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const bool vec = (reinterpret_cast<uintptr_t>(a.gate) & 3) == 0 &&
-                   (!a.rho_zero_fill || (reinterpret_cast<uintptr_t>(a.rho_zero_fill) & 15) == 0);
+  uint8_t* gate = a.gate;
+  float* rho = a.rho_zero_fill;
+  const bool vec = (reinterpret_cast<uintptr_t>(gate) & 3) == 0 && (reinterpret_cast<uintptr_t>(rho) & 15) == 0;
+  size_t done = 0;
   if (vec) {
     const size_t n4 = n / 4;
     for (size_t i = i0; i < n4; i += stride) {
-      reinterpret_cast<uint32_t*>(a.gate)[i] = 0x01010101u;
-      if (a.rho_zero_fill) reinterpret_cast<float4*>(a.rho_zero_fill)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (gate) reinterpret_cast<uint32_t*>(gate)[i] = 0x01010101u;
+      if (rho) reinterpret_cast<float4*>(rho)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    for (size_t i = 4 * n4 + i0; i < n; i += stride) {
-      a.gate[i] = 1;
-      if (a.rho_zero_fill) a.rho_zero_fill[i] = 0.0f;
-    }
-  } else {
-    for (size_t i = i0; i < n; i += stride) {
-      a.gate[i] = 1;
-      if (a.rho_zero_fill) a.rho_zero_fill[i] = 0.0f;
-    }
+    done = 4 * n4;
+  }
+  for (size_t i = done + i0; i < n; i += stride) {
+    if (gate) gate[i] = 1;
+    if (rho) rho[i] = 0.0f;
   }
 }
 
@@ -100,18 +106,20 @@ __device__ inline float sumsq8(uint4 v) {
   return s;
 }
 
-// Inverse norms of the current-frame keys: rn[unit][token] = 1/||k|| (0 for a zero key).
+// Inverse norms of the current-frame keys: rn[unit][token] = 1/||k|| (0 for a
+// zero key).  Work-group (x, seq, unit) covers keys 64 x .. 64 x + 63 of the
+// sequence's current frame, 16 lanes per key.
 __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
-  const int s = blockIdx.x, unit = blockIdx.y;
+  const int s = blockIdx.y, unit = blockIdx.z;
   const Layout& lay = a.lay;
   const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
   if (f1 - f0 < 2) return;  // no history: nothing reads the current-frame norms
   const int32_t off = lay.frame_meta[3 * (f1 - 1)];
-  const int32_t n = frame_size(lay, f1 - 1);
+  const int32_t n = min(frame_size(lay, f1 - 1), int32_t(blockIdx.x + 1) * 64);
   const uint16_t* kunit = a.k + size_t(unit) * lay.total_tokens * kHeadDim;
   float* rn = a.rn_cur + size_t(unit) * lay.total_tokens;
   const int group = threadIdx.x >> 4, gl = threadIdx.x & 15;
-  for (int32_t j = group; j < n; j += blockDim.x >> 4) {
+  for (int32_t j = int32_t(blockIdx.x) * 64 + group; j < n; j += blockDim.x >> 4) {
     const uint4 v = *reinterpret_cast<const uint4*>(kunit + size_t(off + j) * kHeadDim + gl * 8);
     float ss = sumsq8(v);
 #pragma unroll
@@ -332,7 +340,7 @@ __global__ __launch_bounds__(kSegThreads) void gate_emit_kernel(GateArgs a) {
 }
 
 hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
-  hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs), dim3(256), 0, stream, g);
+  hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs + g.lay.n_frames), dim3(256), 0, stream, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t n = size_t(g.lay.n_units) * g.lay.total_tokens;
@@ -366,17 +374,20 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) {
   return launch_gate_select(g, stream);
 }
 
-hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
+hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
   hipError_t e = launch_gate_prologue(g, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(cur_norms_kernel, dim3(r.lay.n_seqs, r.lay.n_units), dim3(256), 0, stream, r);
+  hipLaunchKernelGGL(cur_norms_kernel, dim3((std::max(r.max_cur, 1) + 63) / 64, r.lay.n_seqs, r.lay.n_units), dim3(256),
+                     0, stream, r);
   e = hipGetLastError();
+  if (e != hipSuccess || r.total_hist_blocks == 0) return e;
+  hipLaunchKernelGGL(rho_kernel, dim3(r.total_hist_blocks, r.lay.n_units), dim3(256), 0, stream, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
+  hipError_t e = launch_tsg_rho(r, g, stream);
   if (e != hipSuccess) return e;
-  if (r.total_hist_blocks > 0) {
-    hipLaunchKernelGGL(rho_kernel, dim3(r.total_hist_blocks, r.lay.n_units), dim3(256), 0, stream, r);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   return launch_gate_select(g, stream);
 }
 

@@ -16,12 +16,13 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstlite.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
-CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD = range(6)
+(CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD,
+ CALL_TSG_RHO) = range(7)
 
 EXPORTS = (
     "stlite_abi_version", "stlite_status_string", "stlite_last_error", "stlite_budget",
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
-    "stlite_tsg_gate", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
+    "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
 )
 
 
@@ -69,6 +70,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_score_window": (st, [P, vp, vp, vp, vp, sz, vp]),
         "stlite_css_saliency": (st, [P, vp, vp, vp]),
         "stlite_tsg_gate": (st, [P, vp, vp, vp, vp, vp, sz, vp]),
+        "stlite_tsg_rho": (st, [P, vp, vp, vp, sz, vp]),
         "stlite_tsg_threshold": (st, [P, vp, vp, vp, vp, sz, vp]),
         "stlite_select_topk": (st, [P, vp, vp, vp, f32, vp, vp, vp, sz, vp]),
         "stlite_compact_kv": (st, [P, vp, vp, vp, vp, vp, vp]),
@@ -177,6 +179,11 @@ def stlite_tsg_gate(p: Problem, k, rho, tau, gate, workspace, stream=None) -> No
                                   _nbytes(workspace), _stream(stream)), "stlite_tsg_gate")
 
 
+def stlite_tsg_rho(p: Problem, k, rho, workspace, stream=None) -> None:
+    _check(load().stlite_tsg_rho(p.ref, _ptr(k), _ptr(rho), _ptr(workspace), _nbytes(workspace), _stream(stream)),
+           "stlite_tsg_rho")
+
+
 def stlite_tsg_threshold(p: Problem, rho, tau, gate, workspace, stream=None) -> None:
     _check(load().stlite_tsg_threshold(p.ref, _ptr(rho), _ptr(tau), _ptr(gate), _ptr(workspace),
                                        _nbytes(workspace), _stream(stream)), "stlite_tsg_threshold")
@@ -210,7 +217,7 @@ class Buffers:
         self.kept = torch.empty((U, max(Bt, 1)), dtype=torch.int32, device=device)
         self.k_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
         self.v_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
-        ws = max(p.workspace_size(c) for c in range(6))
+        ws = max(p.workspace_size(c) for c in range(7))
         self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
 
 

@@ -136,6 +136,10 @@ def test_calls_fail_before_launch():
     assert lib.stlite_compact_kv(ref, FAKE_DEV + 8, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
                                  None) == S.ERR_INVALID_ARG
     assert lib.stlite_tsg_gate(ref, FAKE_DEV, None, None, None, None, 0, None) == S.ERR_WORKSPACE
+    assert lib.stlite_tsg_rho(ref, FAKE_DEV, FAKE_DEV, None, 0, None) == S.ERR_WORKSPACE
+    lib.stlite_workspace_size(ref, S.CALL_TSG_RHO, ctypes.byref(n))
+    assert n.value > 0
+    assert lib.stlite_tsg_rho(ref, FAKE_DEV, None, FAKE_DEV, n.value, None) == S.ERR_INVALID_ARG
     p.c.head_dim = 96
     assert lib.stlite_css_saliency(ref, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
     assert lib.stlite_status_string(S.ERR_HIP) == b"STLITE_ERR_HIP"

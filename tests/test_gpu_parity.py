@@ -166,6 +166,29 @@ def test_stage_threshold_and_select_exact(torch_cuda):
         assert (kept[u, cb[s]:cb[s + 1]] == want).all(), (u, s)
 
 
+def test_split_tsg_matches_fused(torch_cuda):
+    """stlite_tsg_rho followed by stlite_tsg_threshold reproduces stlite_tsg_gate
+    bit for bit (rho, gate and tau)."""
+    import torch
+    H = _H()
+    from paper_2603_00188_amd import stlite as S
+    for name in ("ragged", "dups", "beta_tiny"):
+        case = H.Case(SMALL[name])
+        out = case.out
+        S.stlite_tsg_gate(case.prob, case.dk, out.rho, out.tau, out.gate, out.ws)
+        torch.cuda.synchronize()
+        fused = (out.rho.cpu().numpy(), out.gate.cpu().numpy(), out.tau.cpu().numpy())
+        out.rho.fill_(7.0)
+        out.gate.fill_(9)
+        out.tau.fill_(7.0)
+        S.stlite_tsg_rho(case.prob, case.dk, out.rho, out.ws)
+        S.stlite_tsg_threshold(case.prob, out.rho, out.tau, out.gate, out.ws)
+        torch.cuda.synchronize()
+        split = (out.rho.cpu().numpy(), out.gate.cpu().numpy(), out.tau.cpu().numpy())
+        for a, b in zip(fused, split):
+            assert np.array_equal(a, b, equal_nan=True), name
+
+
 def test_determinism(torch_cuda):
     H = _H()
     case = H.Case(SMALL["tiles"])
