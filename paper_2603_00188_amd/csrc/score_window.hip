@@ -125,23 +125,20 @@ __device__ inline void mask_pair(int32_t t0, int h, int b, int i, const int32_t*
 // Pass 1 keeps, per lane and window row, an offset o (log2 units) and
 // sum = sum of 2^(x s - o) over the lane's keys, s = log2(e)/sqrt(d).  The
 // offsets are the lane's row maxima over the chunk's first tile; every tile
-// then only adds 2^(x s - o) and tracks amax, the largest exponent argument
-// of the lane.  amax <= kArgLimit keeps every term and sum finite; a chunk
-// where it is exceeded is recomputed by score_rowstats_exact_kernel.
-constexpr float kArgLimit = 64.0f;
+// then only adds 2^(x s - o).  A logit more than ~128 above its offset
+// overflows the sum to +inf, and score_rowstats_exact_kernel recomputes that
+// chunk.
 constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
 template <int RB, int NW, bool MASK>
 __device__ inline void rowstats_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
-                                     const float (&o)[RB][4], float (&sum)[RB][4], float& amax) {
+                                     const float (&o)[RB][4], float (&sum)[RB][4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float v[2] = {acc[0][i], acc[1][i]};
     mask_pair<NW, MASK>(t0, h, b, i, lim_s, v);
-    const float x0 = fmaf(v[0], kScale2, -o[b][i]);
-    const float x1 = fmaf(v[1], kScale2, -o[b][i]);
-    amax = __builtin_fmaxf(__builtin_fmaxf(amax, x0), x1);
-    sum[b][i] += __builtin_amdgcn_exp2f(x0) + __builtin_amdgcn_exp2f(x1);
+    sum[b][i] += __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -o[b][i])) +
+                 __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -o[b][i]));
   }
 }
 
@@ -162,7 +159,7 @@ __device__ inline void colsum_half(int32_t t0, int h, int b, const f32x4_t (&acc
 // instructions of block b.
 template <int RB, int NW, int PASS, bool MASK>
 __device__ inline void score_tile(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4], const uint16_t* tile,
-                                  const int32_t* lim_s, const float (&o)[RB][4], float (&sum)[RB][4], float& amax,
+                                  const int32_t* lim_s, const float (&o)[RB][4], float (&sum)[RB][4],
                                   float (&col)[4]) {
   const bool last_real = block_of<NW>(RB - 1) < a.blocks;  // wave-uniform
 #pragma unroll
@@ -177,11 +174,11 @@ __device__ inline void score_tile(const ScoreArgs& a, int32_t t0, const bf16x8_t
       if (b + 1 < RB - 1 || (b + 1 == RB - 1 && last_real)) half_logits<RB>(qa, kb, b + 1, acc[(b + 1) & 1]);
       if (b < RB - 1 || last_real) {
         if (PASS == 1)
-          rowstats_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, sum, amax);
+          rowstats_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, sum);
         else
           colsum_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, c2);
       }
-      interleave_mfma_valu<PASS == 1 ? 4 : 3>();
+      interleave_mfma_valu<3>();
       __builtin_amdgcn_sched_barrier(0);  // at most two blocks' accumulators live
     }
     if (PASS == 2) {
@@ -267,7 +264,7 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
   tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
   if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
 
-  float o[RB][4], sum[RB][4], amax = -INFINITY, col_unused[4];
+  float o[RB][4], sum[RB][4], col_unused[4];
   {
     if (ntiles > 1) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
     barrier_lds();
@@ -286,9 +283,9 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
     if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
     const int32_t t0 = cp.c0 + n * kTileKeys;
     if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 1, false>(a, t0, qa, tile, lim_s, o, sum, amax, col_unused);
+      score_tile<RB, NW, 1, false>(a, t0, qa, tile, lim_s, o, sum, col_unused);
     else
-      score_tile<RB, NW, 1, true>(a, t0, qa, tile, lim_s, o, sum, amax, col_unused);
+      score_tile<RB, NW, 1, true>(a, t0, qa, tile, lim_s, o, sum, col_unused);
   };
   for (int32_t n = 0; n < ntiles; n += 3) {
     step(n, ks0, ks2);
@@ -297,14 +294,20 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
   }
 
   write_partials<RB, NW>(a, cp, unit, o, sum);
-  if (__ballot(amax > kArgLimit) != 0 && (threadIdx.x & 63) == 0) atomicOr(&risky, 1);
+  bool bad = false;
+#pragma unroll
+  for (int b = 0; b < RB; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bad |= !(sum[b][i] < INFINITY);
+  if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(&risky, 1);
   __syncthreads();
   if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = risky;
 }
 
 // Exact pass 1 for the chunks flagged by score_rowstats_kernel: a running row
 // max per lane with the sums rescaled on every tile (plain staging; it only
-// runs when a chunk's logits rise more than kArgLimit above the first tile's).
+// runs when a chunk's logits rise far enough above the first tile's to overflow the
+// lean pass's sums).
 template <int RB, int NW>
 __global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems];
@@ -361,6 +364,9 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs
   write_partials<RB, NW>(a, cp, unit, o, sum);
 }
 
+// Per (sequence, row): lse = log2 of the softmax denominator over the
+// sequence's chunks.  Each chunk's (offset, sum) is first turned into its
+// log2 total, so that the merge cannot overflow however large a chunk's sum.
 __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
   const int s = blockIdx.x, unit = blockIdx.y;
   int32_t first = 0;
@@ -374,8 +380,11 @@ __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
     float out = INFINITY;  // padding rows contribute exp2(-inf) = 0 in pass 2
     if (r < a.rows) {
       const float2* pr = a.partial + (size_t(unit) * a.total_chunks + first) * a.rows_pad + r;
-      float M = kNegBig;
-      for (int32_t c = 0; c < nch; ++c) M = fmaxf(M, pr[size_t(c) * a.rows_pad].x);
+      float M = -INFINITY;
+      for (int32_t c = 0; c < nch; ++c) {
+        const float2 v = pr[size_t(c) * a.rows_pad];
+        M = fmaxf(M, v.x + __log2f(v.y));
+      }
       float Z = 0.0f;
       for (int32_t c = 0; c < nch; ++c) {
         const float2 v = pr[size_t(c) * a.rows_pad];
@@ -430,7 +439,7 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
   };
   tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
   if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
-  float sum_unused[RB][4], amax_unused = 0.0f;
+  float sum_unused[RB][4];
   auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt, float (&r)[NW][kTileKeys],
                   const float (&rprev)[NW][kTileKeys]) {
     if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
@@ -440,9 +449,9 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
     const int32_t t0 = cp.c0 + n * kTileKeys;
     float col[4] = {0.f, 0.f, 0.f, 0.f};
     if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 2, false>(a, t0, qa, tile, lim_s, lse, sum_unused, amax_unused, col);
+      score_tile<RB, NW, 2, false>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
     else
-      score_tile<RB, NW, 2, true>(a, t0, qa, tile, lim_s, lse, sum_unused, amax_unused, col);
+      score_tile<RB, NW, 2, true>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       col[t] += __shfl_xor(col[t], 16);

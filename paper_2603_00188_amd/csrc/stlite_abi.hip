@@ -76,7 +76,7 @@ Facts derive(const stlite_problem* p) {
       else
         f.max_cur = std::max(f.max_cur, n);
     }
-    f.total_hist_blocks += ceil_div(hist, 256);
+    f.total_hist_blocks += ceil_div(hist, kRhoRows);
     f.sel_chunks += ceil_div(L, kSegChunk);
     f.gate_chunks += ceil_div(hist, kSegChunk);
   }

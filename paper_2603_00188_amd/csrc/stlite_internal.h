@@ -87,7 +87,10 @@ struct SegSel {
   float* pivot_value;      // nullable [units][n_seqs]: value of the k-th key, NaN when k = 0
 };
 
-// One 256-row block of historical tokens: sequence, block index within the
+// Historical rows per work-group of the rho contraction.
+constexpr int kRhoRows = 256;
+
+// One kRhoRows-row block of historical tokens: sequence, block index within the
 // sequence, the sequence's historical token count, and where its historical
 // tokens start in the flattened hist_tok table.
 struct HistBlock {
@@ -101,7 +104,7 @@ struct RhoArgs {
   float* rho;            // [units][L]; written on historical tokens
   int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
   HistBlock* blocks;     // workspace [total_hist_blocks]
-  int32_t total_hist_blocks;  // sum over sequences of ceil(N_hist_s / 256)
+  int32_t total_hist_blocks;  // sum over sequences of ceil(N_hist_s / kRhoRows)
   int32_t max_cur;       // largest current frame (tokens)
 };
 

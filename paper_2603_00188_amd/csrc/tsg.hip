@@ -19,7 +19,7 @@
 namespace stlite {
 namespace {
 
-constexpr int kRhoRows = 256;
+
 constexpr float kSnap = 1.0f - 1.0e-4f;
 
 __device__ inline int32_t frame_size(const Layout& lay, int32_t f) {
