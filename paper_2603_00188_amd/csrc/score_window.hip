@@ -92,11 +92,12 @@ __device__ inline void load_half_b(const uint16_t* tile, int h, bf16x8_t (&kb)[2
 }
 
 // Ask the scheduler to alternate one MFMA with `valu` vector instructions, so
-// that the softmax arithmetic of one block runs under the next block's MFMAs.
-template <int valu>
+// that the softmax arithmetic of one group of blocks runs under the next
+// group's MFMAs (8 MFMAs per block).
+template <int valu, int GP>
 __device__ inline void interleave_mfma_valu() {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < 8 * GP; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x002, valu, 0);
   }
@@ -129,6 +130,9 @@ __device__ inline void mask_pair(int32_t t0, int h, int b, int i, const int32_t*
 // overflows the sum to +inf, and score_rowstats_exact_kernel recomputes that
 // chunk.
 constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+// Row blocks whose MFMAs are issued together (2 accumulators each).
+constexpr int kRowGroup = 2;
+constexpr int kColGroup = 2;
 
 template <int RB, int NW, bool MASK>
 __device__ inline void rowstats_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
@@ -154,32 +158,58 @@ __device__ inline void colsum_half(int32_t t0, int h, int b, const f32x4_t (&acc
   }
 }
 
+// Q K^T of half a tile for the blocks of group g (GP blocks from block g*GP):
+// 2*GP independent 16x16 accumulators, interleaved over the k-steps.
+template <int RB, int GP>
+__device__ inline void group_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[2][4], int g, bool last_real,
+                                    f32x4_t (&acc)[GP][2]) {
+#pragma unroll
+  for (int j = 0; j < GP; ++j)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) acc[j][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int j = 0; j < GP; ++j) {
+      const int b = g * GP + j;
+      if (b < RB - 1 || (b == RB - 1 && last_real))
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[j][t], 0, 0, 0);
+    }
+}
+
 // One tile of pass 1 (PASS == 1) or pass 2 (PASS == 2), as two 32-key halves;
-// within a half the MFMAs of block b+1 are issued among the vector
-// instructions of block b.
-template <int RB, int NW, int PASS, bool MASK>
+// within a half the blocks go in groups of GP, and the MFMAs of group g+1 are
+// issued among the vector instructions of group g.
+template <int RB, int NW, int PASS, bool MASK, int GP>
 __device__ inline void score_tile(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4], const uint16_t* tile,
                                   const int32_t* lim_s, const float (&o)[RB][4], float (&sum)[RB][4],
                                   float (&col)[4]) {
+  constexpr int NG = (RB + GP - 1) / GP;
   const bool last_real = block_of<NW>(RB - 1) < a.blocks;  // wave-uniform
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     bf16x8_t kb[2][4];
     load_half_b(tile, h, kb);
-    f32x4_t acc[2][2];
-    half_logits<RB>(qa, kb, 0, acc[0]);
+    f32x4_t acc[2][GP][2];
+    group_logits<RB, GP>(qa, kb, 0, last_real, acc[0]);
     float c2[2] = {0.f, 0.f};
 #pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      if (b + 1 < RB - 1 || (b + 1 == RB - 1 && last_real)) half_logits<RB>(qa, kb, b + 1, acc[(b + 1) & 1]);
-      if (b < RB - 1 || last_real) {
-        if (PASS == 1)
-          rowstats_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, sum);
-        else
-          colsum_half<RB, NW, MASK>(t0, h, b, acc[b & 1], lim_s, o, c2);
+    for (int g = 0; g < NG; ++g) {
+      if (g + 1 < NG) group_logits<RB, GP>(qa, kb, g + 1, last_real, acc[(g + 1) & 1]);
+#pragma unroll
+      for (int j = 0; j < GP; ++j) {
+        const int b = g * GP + j;
+        if (b < RB - 1 || (b == RB - 1 && last_real)) {
+          if (PASS == 1)
+            rowstats_half<RB, NW, MASK>(t0, h, b, acc[g & 1][j], lim_s, o, sum);
+          else
+            colsum_half<RB, NW, MASK>(t0, h, b, acc[g & 1][j], lim_s, o, c2);
+        }
       }
-      interleave_mfma_valu<3>();
-      __builtin_amdgcn_sched_barrier(0);  // at most two blocks' accumulators live
+      interleave_mfma_valu<3, GP>();
+      __builtin_amdgcn_sched_barrier(0);  // at most two groups' accumulators live
     }
     if (PASS == 2) {
       col[2 * h] += c2[0];
@@ -283,9 +313,9 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
     if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
     const int32_t t0 = cp.c0 + n * kTileKeys;
     if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 1, false>(a, t0, qa, tile, lim_s, o, sum, col_unused);
+      score_tile<RB, NW, 1, false, kRowGroup>(a, t0, qa, tile, lim_s, o, sum, col_unused);
     else
-      score_tile<RB, NW, 1, true>(a, t0, qa, tile, lim_s, o, sum, col_unused);
+      score_tile<RB, NW, 1, true, kRowGroup>(a, t0, qa, tile, lim_s, o, sum, col_unused);
   };
   for (int32_t n = 0; n < ntiles; n += 3) {
     step(n, ks0, ks2);
@@ -449,9 +479,9 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
     const int32_t t0 = cp.c0 + n * kTileKeys;
     float col[4] = {0.f, 0.f, 0.f, 0.f};
     if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 2, false>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
+      score_tile<RB, NW, 2, false, kColGroup>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
     else
-      score_tile<RB, NW, 2, true>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
+      score_tile<RB, NW, 2, true, kColGroup>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       col[t] += __shfl_xor(col[t], 16);

@@ -209,20 +209,23 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int t = 0; t < 2; ++t) acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    bf16x8_t kb[2][2];
+    bf16x8_t kb[3][2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) kb[0][t] = tile_b_operand(tile, 2 * h + t, 0);
+    for (int t = 0; t < 2; ++t) {
+      kb[0][t] = tile_b_operand(tile, 2 * h + t, 0);
+      kb[1][t] = tile_b_operand(tile, 2 * h + t, 1);
+    }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      if (kk + 1 < 4) {
+      if (kk + 2 < 4) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t) kb[(kk + 1) & 1][t] = tile_b_operand(tile, 2 * h + t, kk + 1);
+        for (int t = 0; t < 2; ++t) kb[(kk + 2) % 3][t] = tile_b_operand(tile, 2 * h + t, kk + 2);
       }
 #pragma unroll
       for (int b = 0; b < 4; ++b)
 #pragma unroll
         for (int t = 0; t < 2; ++t)
-          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[kk & 1][t], acc[b][t], 0, 0, 0);
+          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[kk % 3][t], acc[b][t], 0, 0, 0);
     }
   };
   auto max_half = [&](const f32x4_t (&acc)[4][2], float rn0, float rn1) {
@@ -232,11 +235,18 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
       for (int i = 0; i < 4; ++i)
         runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rn0), acc[b][1][i] * rn1);
   };
+  // Per half: the B fragments of k-step kk+2 are read while the MFMAs of
+  // k-step kk run (LDS latency stays off the MFMA stream).
   auto interleave = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // B fragments of k-steps 0 and 1
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // 3 VALU
+    for (int kk = 0; kk < 4; ++kk) {
+      if (kk + 2 < 4) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // prefetch k-step kk+2
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // 3 VALU
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
   };
