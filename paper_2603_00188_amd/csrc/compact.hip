@@ -12,26 +12,44 @@ constexpr int kRowsPerGroup = 64;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
+  constexpr int kPer = kRowsPerGroup / 16;  // rows per 16-lane group
   const Layout& lay = a.lay;
   const int unit = blockIdx.y;
   const int64_t j0 = int64_t(blockIdx.x) * kRowsPerGroup;
   const int sub = threadIdx.x >> 4, part = threadIdx.x & 15;
   const size_t ubase = size_t(unit) * lay.total_tokens;
   const size_t obase = size_t(unit) * lay.total_budget;
+  // All of a thread's loads are issued before its stores, so that each lane
+  // keeps 2 * kPer 16-byte reads in flight.
+  int32_t tok[kPer];
+  bool row_ok[kPer];
 #pragma unroll
-  for (int r = 0; r < kRowsPerGroup; r += 16) {
-    const int64_t j = j0 + r + sub;
-    if (j >= lay.total_budget) break;
-    const int32_t tok = a.kept[obase + j];
-    u32x4_t kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-    if (tok >= 0 && tok < lay.total_tokens) {
-      const size_t src = (ubase + size_t(tok)) * kHeadDim + part * 8;
-      kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.k + src));
-      vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.v + src));
+  for (int r = 0; r < kPer; ++r) {
+    const int64_t j = j0 + r * 16 + sub;
+    row_ok[r] = j < lay.total_budget;
+    tok[r] = row_ok[r] ? a.kept[obase + j] : -1;
+  }
+  // Loads are unconditional (an out-of-range index reads row 0 and is stored
+  // as zeros), so that no branch forces a wait between them.
+  u32x4_t kv[kPer], vv[kPer];
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const bool ok = tok[r] >= 0 && tok[r] < lay.total_tokens;
+    const size_t src = (ubase + size_t(ok ? tok[r] : 0)) * kHeadDim + part * 8;
+    kv[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.k + src));
+    vv[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.v + src));
+  }
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const bool ok = tok[r] >= 0 && tok[r] < lay.total_tokens;
+    if (!ok) {
+      kv[r] = u32x4_t{0u, 0u, 0u, 0u};
+      vv[r] = u32x4_t{0u, 0u, 0u, 0u};
     }
-    const size_t dst = (obase + size_t(j)) * kHeadDim + part * 8;
-    __builtin_nontemporal_store(kv, reinterpret_cast<u32x4_t*>(a.k_out + dst));
-    __builtin_nontemporal_store(vv, reinterpret_cast<u32x4_t*>(a.v_out + dst));
+    if (!row_ok[r]) continue;
+    const size_t dst = (obase + size_t(j0 + r * 16 + sub)) * kHeadDim + part * 8;
+    __builtin_nontemporal_store(kv[r], reinterpret_cast<u32x4_t*>(a.k_out + dst));
+    __builtin_nontemporal_store(vv[r], reinterpret_cast<u32x4_t*>(a.v_out + dst));
   }
 }
 

@@ -87,7 +87,13 @@ __device__ inline float quad_sum(float x) {
   return x;
 }
 
-__device__ inline float inv_norm(float ss) { return ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f; }
+// 1/||k|| from ||k||^2 (0 for a zero key).  v_rsq_f32 (1 ulp) covers every
+// normal square norm; the exactly rounded form is kept for tiny ones.
+__device__ inline float inv_norm(float ss) {
+  float r = __builtin_amdgcn_rsqf(ss);
+  if (!(ss >= 0x1p-100f)) r = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+  return r;
+}
 
 __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ring0[kRowElems], ring1[kRowElems], ring2[kRowElems],
@@ -161,7 +167,7 @@ __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
     const int32_t nn = nrows * ncols - 1;
     const bool store = r < R && out_lane && s == 0;
     const uint32_t byte_off = store ? uint32_t(r * C + col) * 4u : frame_bytes;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(nn > 0 ? 1.0f - H / float(nn) : 0.0f), phi_rsrc, byte_off,
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(nn > 0 ? 1.0f - H * __builtin_amdgcn_rcpf(float(nn)) : 0.0f), phi_rsrc, byte_off,
                                           0, 0);
     carry = cS + (has_w ? cSE_w : 0.0f) + (has_e ? cSW_e : 0.0f);
     own = down;
