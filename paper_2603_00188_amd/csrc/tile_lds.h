@@ -23,7 +23,8 @@ constexpr int kTileElems = kTileKeys * kHeadDim;  // 16 KB of bf16
 template <int NW>
 __device__ inline void tile_dma(const uint16_t* rows, int32_t first, int32_t last_valid, uint16_t* tile) {
   constexpr int kLoads = 16 / NW;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // The wave index selects the LDS rows through M0: keep it scalar.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
 #pragma unroll
   for (int m = 0; m < kLoads; ++m) {
     const int grp = wave * kLoads + m;
