@@ -179,6 +179,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run score, TSG and CSS on three concurrent streams")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a device copy of BYTES bytes three times (counter calibration)")
     args = ap.parse_args()
@@ -213,29 +215,52 @@ def main():
     log(f"inputs resident: K+V {2 * dk.numel() * 2 / 1e9:.2f} GB")
 
     stream = torch.cuda.current_stream()
+    s_tsg, s_css = out.side
     names = ["score_window", "tsg_rho", "tsg_threshold", "css_saliency", "select_topk", "compact_kv"]
+    # Concurrent streams gain about 1% here (the two MFMA passes share the
+    # matrix cores) and blur the per-kernel times, so the timed step is serial.
+    overlap = args.overlap
 
     def step(ev=None):
-        # the TSG step as its two calls (rho, then threshold and gate), so that
-        # the rho GEMM is timed on its own
-        if ev: ev[0].record(stream)
-        S.stlite_score_window(prob, dq, dk, out.a_base, out.ws, stream)
-        if ev: ev[1].record(stream)
-        S.stlite_tsg_rho(prob, dk, rho, out.ws, stream)
-        if ev: ev[2].record(stream)
-        S.stlite_tsg_threshold(prob, rho, None, out.gate, out.ws, stream)
-        if ev: ev[3].record(stream)
-        S.stlite_css_saliency(prob, dk, out.phi, stream)
-        if ev: ev[4].record(stream)
+        # With --overlap the three independent steps run concurrently (score on
+        # the main stream, TSG and CSS on side streams).  The TSG step runs as
+        # its two calls (rho, then threshold and gate), so that the rho GEMM
+        # is timed on its own.  Per-call events sit on the stream of their call.
+        st = (stream, s_tsg, s_css) if overlap else (stream, stream, stream)
+        if overlap:
+            start = torch.cuda.Event()
+            start.record(stream)
+            s_tsg.wait_event(start)
+            s_css.wait_event(start)
+        if ev: ev["score_window"][0].record(st[0])
+        S.stlite_score_window(prob, dq, dk, out.a_base, out.ws, st[0])
+        if ev: ev["score_window"][1].record(st[0])
+        if ev: ev["tsg_rho"][0].record(st[1])
+        S.stlite_tsg_rho(prob, dk, rho, out.ws_tsg, st[1])
+        if ev: ev["tsg_rho"][1].record(st[1])
+        if ev: ev["tsg_threshold"][0].record(st[1])
+        S.stlite_tsg_threshold(prob, rho, None, out.gate, out.ws_tsg, st[1])
+        if ev: ev["tsg_threshold"][1].record(st[1])
+        if ev: ev["css_saliency"][0].record(st[2])
+        S.stlite_css_saliency(prob, dk, out.phi, st[2])
+        if ev: ev["css_saliency"][1].record(st[2])
+        if overlap:
+            for s in (s_tsg, s_css):
+                done = torch.cuda.Event()
+                done.record(s)
+                stream.wait_event(done)
+        if ev: ev["select_topk"][0].record(stream)
         S.stlite_select_topk(prob, out.a_base, out.phi, out.gate, w.alpha, out.kept, None, out.ws, stream)
-        if ev: ev[5].record(stream)
+        if ev: ev["select_topk"][1].record(stream)
+        if ev: ev["compact_kv"][0].record(stream)
         S.stlite_compact_kv(prob, dk, dv, out.kept, out.k_out, out.v_out, stream)
-        if ev: ev[6].record(stream)
+        if ev: ev["compact_kv"][1].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
+    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
+           for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -245,7 +270,7 @@ def main():
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
-    per_call = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
+    per_call = {n: float(np.mean([e[n][0].elapsed_time(e[n][1]) for e in evs])) for n in names}
     log(f"step {ms_step:.3f} ms; calls: " + ", ".join(f"{n} {t:.3f}" for n, t in per_call.items()))
 
     model = work_model(w, lay, cu_budget)
@@ -283,6 +308,7 @@ def main():
             "tokens": lay.total_tokens, "layers": w.n_layers, "kv_heads": w.n_kv_heads,
             "q_heads": w.n_q_heads, "window": w.window, "beta": f"{w.beta[0]}/{w.beta[1]}",
             "budget_per_unit": int(cu_budget[-1]),
+            "streams": "score | tsg_rho+tsg_threshold | css, then select, compact" if overlap else "one stream",
         },
         "roofline": roof,
         "stages": stages,

@@ -202,7 +202,12 @@ def stlite_compact_kv(p: Problem, k, v, kept, k_out, v_out, stream=None) -> None
 
 
 class Buffers:
-    """Device outputs and workspaces for one problem (allocated once, reused)."""
+    """Device outputs and workspaces for one problem (allocated once, reused).
+
+    ``ws`` serves the calls on the main stream; ``ws_tsg`` is a second
+    workspace for the TSG calls, so that they can run on a side stream while
+    the window scoring uses ``ws``.
+    """
 
     def __init__(self, p: Problem, device="cuda", keep_stages: bool = True):
         import torch
@@ -217,19 +222,49 @@ class Buffers:
         self.kept = torch.empty((U, max(Bt, 1)), dtype=torch.int32, device=device)
         self.k_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
         self.v_out = torch.empty((U, max(Bt, 1), 128), dtype=torch.int16, device=device)
-        ws = max(p.workspace_size(c) for c in range(7))
+        ws = max(p.workspace_size(c) for c in (CALL_SCORE_WINDOW, CALL_CSS_SALIENCY, CALL_SELECT_TOPK,
+                                               CALL_COMPACT_KV))
+        ws_tsg = max(p.workspace_size(c) for c in (CALL_TSG_GATE, CALL_TSG_RHO, CALL_TSG_THRESHOLD))
         self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        self.ws_tsg = torch.empty(max(ws_tsg, 256), dtype=torch.uint8, device=device)
+        # side streams at the default priority
+        self.side = (torch.cuda.Stream(device=device), torch.cuda.Stream(device=device))
 
 
 def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: bool = True,
-             tsg: bool = True, stream=None) -> Buffers:
-    """The whole pass: score, gate, saliency, select, compact (five C calls)."""
-    stlite_score_window(p, q_win, k, out.a_base, out.ws, stream)
-    if tsg:
-        stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws, stream)
-    if css:
-        stlite_css_saliency(p, k, out.phi, stream)
+             tsg: bool = True, stream=None, overlap: bool = False) -> Buffers:
+    """The whole pass: score, gate, saliency, select, compact (five C calls).
+
+    With ``overlap`` the three independent steps run concurrently: the window
+    scoring on ``stream``, TSG and CSS on the two side streams of ``out``;
+    the top-B selection waits for all three.  Otherwise everything runs in
+    order on ``stream``.
+    """
+    import torch
+    main = stream if stream is not None else torch.cuda.current_stream()
+    if not overlap:
+        stlite_score_window(p, q_win, k, out.a_base, out.ws, main)
+        if tsg:
+            stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws_tsg, main)
+        if css:
+            stlite_css_saliency(p, k, out.phi, main)
+    else:
+        s_tsg, s_css = out.side
+        start = torch.cuda.Event()
+        start.record(main)
+        for s in (s_tsg, s_css):
+            s.wait_event(start)
+            k.record_stream(s)
+        stlite_score_window(p, q_win, k, out.a_base, out.ws, main)
+        if tsg:
+            stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws_tsg, s_tsg)
+        if css:
+            stlite_css_saliency(p, k, out.phi, s_css)
+        for s in (s_tsg, s_css):
+            done = torch.cuda.Event()
+            done.record(s)
+            main.wait_event(done)
     stlite_select_topk(p, out.a_base, out.phi if css else None, out.gate if tsg else None, alpha,
-                       out.kept, out.score, out.ws, stream)
-    stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, stream)
+                       out.kept, out.score, out.ws, main)
+    stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, main)
     return out

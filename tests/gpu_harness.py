@@ -49,10 +49,10 @@ class Case:
         self.dk, self.dv, self.dq = as_dev(self.k), as_dev(self.v), as_dev(self.q)
         self.out = S.Buffers(self.prob, device=device)
 
-    def run(self, alpha=None, css=True, tsg=True):
+    def run(self, alpha=None, css=True, tsg=True, overlap=False):
         import torch
         S.compress(self.prob, self.dq, self.dk, self.dv, self.out,
-                   alpha=self.w.alpha if alpha is None else alpha, css=css, tsg=tsg)
+                   alpha=self.w.alpha if alpha is None else alpha, css=css, tsg=tsg, overlap=overlap)
         torch.cuda.synchronize()
         o = self.out
         U = self.prob.units

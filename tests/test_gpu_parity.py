@@ -145,7 +145,7 @@ def test_stage_threshold_and_select_exact(torch_cuda):
     dev = lambda x: torch.from_numpy(x).cuda()
     drho, dA, dphi = dev(rho), dev(A), dev(phi)
     out = case.out
-    S.stlite_tsg_threshold(case.prob, drho, out.tau, out.gate, out.ws)
+    S.stlite_tsg_threshold(case.prob, drho, out.tau, out.gate, out.ws_tsg)
     torch.cuda.synchronize()
     gate = out.gate.cpu().numpy()
     for (u, s), r in refs.items():
@@ -175,18 +175,29 @@ def test_split_tsg_matches_fused(torch_cuda):
     for name in ("ragged", "dups", "beta_tiny"):
         case = H.Case(SMALL[name])
         out = case.out
-        S.stlite_tsg_gate(case.prob, case.dk, out.rho, out.tau, out.gate, out.ws)
+        S.stlite_tsg_gate(case.prob, case.dk, out.rho, out.tau, out.gate, out.ws_tsg)
         torch.cuda.synchronize()
         fused = (out.rho.cpu().numpy(), out.gate.cpu().numpy(), out.tau.cpu().numpy())
         out.rho.fill_(7.0)
         out.gate.fill_(9)
         out.tau.fill_(7.0)
-        S.stlite_tsg_rho(case.prob, case.dk, out.rho, out.ws)
-        S.stlite_tsg_threshold(case.prob, out.rho, out.tau, out.gate, out.ws)
+        S.stlite_tsg_rho(case.prob, case.dk, out.rho, out.ws_tsg)
+        S.stlite_tsg_threshold(case.prob, out.rho, out.tau, out.gate, out.ws_tsg)
         torch.cuda.synchronize()
         split = (out.rho.cpu().numpy(), out.gate.cpu().numpy(), out.tau.cpu().numpy())
         for a, b in zip(fused, split):
             assert np.array_equal(a, b, equal_nan=True), name
+
+
+def test_overlapped_streams_match_serial(torch_cuda):
+    """compress() with score, TSG and CSS on three concurrent streams gives
+    the same bits as the serial pass."""
+    H = _H()
+    case = H.Case(SMALL["ragged"])
+    r1 = case.run()
+    r2 = case.run(overlap=True)
+    for k in r1:
+        assert np.array_equal(r1[k], r2[k], equal_nan=True), k
 
 
 def test_determinism(torch_cuda):
