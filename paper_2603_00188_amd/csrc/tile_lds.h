@@ -19,7 +19,11 @@ constexpr int kTileElems = kTileKeys * kHeadDim;  // 16 KB of bf16
 
 // Issue the DMA of keys first .. first+63 of `rows` ([.][128] bf16) into `tile`;
 // key indices past `last_valid` repeat key `last_valid`.  Every wave issues
-// 16 / NW wave-loads (4 keys each); wait for them with wait_vmcnt.
+// 16 / NW wave-loads (4 keys each); wait for them with wait_vmcnt (and a
+// barrier for the other waves' rows) before reading the tile.  The LDS
+// address reaches the instruction through an opaque copy: the compiler then
+// inserts none of its own (full) waits before tile reads, which it would
+// otherwise add wherever it cannot count the loads still in flight.
 template <int NW>
 __device__ inline void tile_dma(const uint16_t* rows, int32_t first, int32_t last_valid, uint16_t* tile) {
   constexpr int kLoads = 16 / NW;
@@ -31,8 +35,9 @@ __device__ inline void tile_dma(const uint16_t* rows, int32_t first, int32_t las
     const int kl = grp * 4 + (lane >> 4);
     const int chunk = (lane & 15) ^ (kl & 15);
     const int32_t key = min(first + kl, last_valid);
-    __builtin_amdgcn_global_load_lds(rows + size_t(key) * kHeadDim + chunk * 8,
-                                     (lds_void_t)(tile + grp * 4 * kHeadDim), 16, 0, 0);
+    uint32_t dst = uint32_t(reinterpret_cast<uintptr_t>(tile + grp * 4 * kHeadDim));
+    asm volatile("" : "+s"(dst));
+    __builtin_amdgcn_global_load_lds(rows + size_t(key) * kHeadDim + chunk * 8, (lds_void_t)(uintptr_t)dst, 16, 0, 0);
   }
 }
 
