@@ -12,7 +12,7 @@
 // Row r's mean combines its own forward cosines, its west neighbour's E, and
 // the previous row's S / SE / SW carried in registers.
 //
-// Rows stream into a four-slot LDS ring by direct global->LDS DMA, two rows
+// Rows stream into a four-slot LDS ring by direct memory->LDS DMA, two rows
 // ahead of the row being combined, so every key is read from HBM once per
 // strip.  The strips of one frame are given to work-groups that land on the
 // same XCD, where the halo columns hit the shared L2.
@@ -37,6 +37,10 @@ __device__ inline void row_dma(const uint16_t* kframe, int32_t row, int32_t c0, 
   // The slot being refilled was last read two steps ago; make sure those LDS
   // reads have completed before the DMA can land.
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  // A buffer load into LDS over the frame row: tracked by the vector-memory
+  // counter only, so the ring reads keep exact lgkmcnt waits.
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kframe + size_t(row) * C * kHeadDim), 0, C * (kHeadDim * 2), kBufferFlags);
 #pragma unroll
   for (int m = 0; m < kRowLoads; ++m) {
     const int g = 4 * m + (lane >> 4);
@@ -48,8 +52,8 @@ __device__ inline void row_dma(const uint16_t* kframe, int32_t row, int32_t c0, 
     // the ring is read; the kernel waits for exactly the rows it needs.
     uint32_t lds = uint32_t(reinterpret_cast<uintptr_t>(dst + 4 * m * kHeadDim));
     asm volatile("" : "+s"(lds));
-    __builtin_amdgcn_global_load_lds(kframe + (size_t(row) * C + col) * kHeadDim + ch * 8,
-                                     (lds_void_t)(uintptr_t)lds, 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t)(uintptr_t)lds, 16,
+                                             uint32_t(col) * (kHeadDim * 2) + uint32_t(ch) * 16u, 0, 0, 0);
   }
 }
 
@@ -121,7 +125,7 @@ __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   // branch (and the number of memory operations per step stays fixed).
   const uint32_t frame_bytes = uint32_t(R) * uint32_t(C) * 4u;
   const __amdgpu_buffer_rsrc_t phi_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(a.phi + size_t(unit) * lay.total_tokens + off, 0, frame_bytes, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc(a.phi + size_t(unit) * lay.total_tokens + off, 0, frame_bytes, kBufferFlags);
   const int ge = min(g + 1, kStripCells - 1), gw = max(g - 1, 0);
 
   // Every step issues one row (rows past the end repeat row R-1 and hit L2),

@@ -287,12 +287,13 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
   load_queries<RB, NW>(a, cp, unit, qa);
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  const TileDma<NW> dma;
   // Tiles that end before the window starts are visible to every row: no mask.
   const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
   const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
   constexpr int kLoads = 16 / NW;  // tile DMA wave-loads per wave
-  tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
-  if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
+  dma.issue(kseq, cp.c0, cp.c1 - 1, ks0);
+  if (ntiles > 1) dma.issue(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
 
   float o[RB][4], sum[RB][4], col_unused[4];
   {
@@ -310,7 +311,7 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
       if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
       barrier_lds();
     }
-    if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
+    if (n + 2 < ntiles) dma.issue(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
     const int32_t t0 = cp.c0 + n * kTileKeys;
     if (t0 + kTileKeys <= clean_end)
       score_tile<RB, NW, 1, false, kRowGroup>(a, t0, qa, tile, lim_s, o, sum, col_unused);
@@ -358,9 +359,10 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs
       sum[b][i] = 0.0f;
     }
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  const TileDma<NW> dma;
   for (int32_t t0 = cp.c0; t0 < cp.c1; t0 += kTileKeys) {
     __syncthreads();
-    tile_dma<NW>(kseq, t0, cp.c1 - 1, ks0);
+    dma.issue(kseq, t0, cp.c1 - 1, ks0);
     wait_vmcnt<0>();
     __syncthreads();
 #pragma unroll
@@ -453,6 +455,7 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
     for (int i = 0; i < 4; ++i) lse[b][i] = lrow[block_of<NW>(b) * 16 + (lane >> 4) * 4 + i];
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
+  const TileDma<NW> dma;
   float* aout = a.a_base + size_t(unit) * a.lay.total_tokens + cp.seq_start;
   const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
   const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
@@ -467,15 +470,15 @@ __global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
       if (j < cp.c1) aout[j] = s * inv_g;
     }
   };
-  tile_dma<NW>(kseq, cp.c0, cp.c1 - 1, ks0);
-  if (ntiles > 1) tile_dma<NW>(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
+  dma.issue(kseq, cp.c0, cp.c1 - 1, ks0);
+  if (ntiles > 1) dma.issue(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
   float sum_unused[RB][4];
   auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt, float (&r)[NW][kTileKeys],
                   const float (&rprev)[NW][kTileKeys]) {
     if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
     barrier_lds();
     if (n > 0) reduce(n - 1, rprev);
-    if (n + 2 < ntiles) tile_dma<NW>(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
+    if (n + 2 < ntiles) dma.issue(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
     const int32_t t0 = cp.c0 + n * kTileKeys;
     float col[4] = {0.f, 0.f, 0.f, 0.f};
     if (t0 + kTileKeys <= clean_end)

@@ -1,5 +1,5 @@
-// 64-key tiles of bf16 key rows staged in LDS by direct global->LDS DMA
-// (global_load_lds_dwordx4: lane j of a wave-load lands at LDS base + 16 j, no
+// 64-key tiles of bf16 key rows staged in LDS by direct memory->LDS DMA
+// (buffer_load_dwordx4 ... lds: lane j of a wave-load lands at LDS base + 16 j, no
 // VGPRs involved), shared by the window-score and rho GEMM kernels.
 //
 // Layout: 64 keys x 256 bytes, no padding.  The 16-byte chunk c (dims 8c..8c+7)
@@ -16,30 +16,59 @@ typedef __attribute__((address_space(3))) void* lds_void_t;
 
 constexpr int kTileKeys = 64;
 constexpr int kTileElems = kTileKeys * kHeadDim;  // 16 KB of bf16
+// Buffer descriptor flags of a raw (unswizzled, stride 0) buffer on gfx950.
+constexpr int kBufferFlags = 0x00020000;
 
-// Issue the DMA of keys first .. first+63 of `rows` ([.][128] bf16) into `tile`;
-// key indices past `last_valid` repeat key `last_valid`.  Every wave issues
-// 16 / NW wave-loads (4 keys each); wait for them with wait_vmcnt (and a
-// barrier for the other waves' rows) before reading the tile.  The LDS
-// address reaches the instruction through an opaque copy: the compiler then
-// inserts none of its own (full) waits before tile reads, which it would
-// otherwise add wherever it cannot count the loads still in flight.
+// DMA of 64-key tiles: keys first .. first+63 of `rows` ([.][128] bf16) into
+// an LDS tile; key indices past `last_valid` repeat key `last_valid`.  Every
+// wave issues 16 / NW wave-loads (4 keys each); wait for them with wait_vmcnt
+// (and a barrier for the other waves' rows) before reading the tile.
+//
+// The loads are buffer loads with the LDS bit (MUBUF encoding): the compiler
+// tracks them with the vector-memory counter only, so LDS reads issued while
+// they are in flight keep exact lgkmcnt waits (the flat-encoded global->LDS
+// form makes it wait for every LDS read instead).  The buffer's range ends at
+// key last_valid, so no load can reach past it.  Per-lane byte offsets are
+// computed once; a wave-load costs a clamp and an add.  The LDS address
+// reaches the instruction through an opaque copy: the compiler then inserts
+// none of its own (full) waits before tile reads, which it would otherwise
+// add wherever it cannot count the loads still in flight.
 template <int NW>
-__device__ inline void tile_dma(const uint16_t* rows, int32_t first, int32_t last_valid, uint16_t* tile) {
-  constexpr int kLoads = 16 / NW;
-  // The wave index selects the LDS rows through M0: keep it scalar.
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+struct TileDma {
+  static constexpr int kLoads = 16 / NW;
+  uint32_t row[kLoads];    // local key * 256 (the clamped part)
+  uint32_t chunk[kLoads];  // swizzled 16-byte slot * 16
+  int lds[kLoads];         // LDS byte offset of the wave-load within a tile (uniform)
+
+  __device__ TileDma() {
+    // The wave index selects the LDS rows through M0: keep it scalar.
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
 #pragma unroll
-  for (int m = 0; m < kLoads; ++m) {
-    const int grp = wave * kLoads + m;
-    const int kl = grp * 4 + (lane >> 4);
-    const int chunk = (lane & 15) ^ (kl & 15);
-    const int32_t key = min(first + kl, last_valid);
-    uint32_t dst = uint32_t(reinterpret_cast<uintptr_t>(tile + grp * 4 * kHeadDim));
-    asm volatile("" : "+s"(dst));
-    __builtin_amdgcn_global_load_lds(rows + size_t(key) * kHeadDim + chunk * 8, (lds_void_t)(uintptr_t)dst, 16, 0, 0);
+    for (int m = 0; m < kLoads; ++m) {
+      const int grp = wave * kLoads + m;
+      const int kl = grp * 4 + (lane >> 4);
+      row[m] = uint32_t(kl) * (kHeadDim * 2);
+      chunk[m] = uint32_t((lane & 15) ^ (kl & 15)) * 16u;
+      lds[m] = grp * 4 * kHeadDim * 2;
+    }
   }
-}
+
+  // The descriptor covers keys first .. min(first + 63, last_valid) only (at
+  // most 16 KB), so offsets stay small whatever the sequence length.
+  __device__ void issue(const uint16_t* rows, int32_t first, int32_t last_valid, uint16_t* tile) const {
+    const int32_t n_valid = min(last_valid - first + 1, kTileKeys);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(rows + size_t(first) * kHeadDim), 0, n_valid * (kHeadDim * 2), kBufferFlags);
+    const uint32_t bound = uint32_t(n_valid - 1) * (kHeadDim * 2);
+#pragma unroll
+    for (int m = 0; m < kLoads; ++m) {
+      const uint32_t off = min(row[m], bound) + chunk[m];
+      uint32_t dst = uint32_t(reinterpret_cast<uintptr_t>(tile)) + uint32_t(lds[m]);
+      asm volatile("" : "+s"(dst));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t)(uintptr_t)dst, 16, off, 0, 0, 0);
+    }
+  }
+};
 
 // 16x16x32 MFMA B operand for sub-tile t and k-step kk: lane l supplies dims
 // 32 kk + 8 (l >> 4) .. +7 of key 16 t + (l & 15).

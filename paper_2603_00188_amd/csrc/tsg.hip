@@ -130,11 +130,11 @@ __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
 
 // One work-group = 4 waves x 64 historical rows (the MFMA A operand, resident
 // in VGPRs).  The current frame streams through a three-stage ring of LDS
-// tiles filled by direct global->LDS DMA: tile n+2 is in flight while tile n
+// tiles filled by direct memory->LDS DMA: tile n+2 is in flight while tile n
 // feeds the matrix cores.  Key slots past the end of the frame repeat the
 // frame's last key, which leaves every row max unchanged and needs no mask.
 // The three stages are distinct LDS arrays and the loop is unrolled by three,
-// so that the compiler can tell which DMA a tile read depends on.
+// so that every tile read has a compile-time LDS address.
 __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
   __shared__ __attribute__((aligned(16))) float rn0[kTileKeys], rn1[kTileKeys], rn2[kTileKeys];
@@ -152,11 +152,19 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
   const uint16_t* kcur = kunit + size_t(cur_off) * kHeadDim;
   const float* rn_cur = a.rn_cur + size_t(unit) * lay.total_tokens + cur_off;
 
-  // Tile n: 4 key wave-loads per wave, plus the 64 inverse norms on wave 0.
+  const TileDma<4> dma;
+  const __amdgpu_buffer_rsrc_t rn_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(rn_cur), 0, n_cur * 4, kBufferFlags);
+  // Tile n: 4 key wave-loads per wave, plus the 64 inverse norms on wave 0 (a
+  // frame's norms are one small buffer; slots past its end repeat the last).
   auto issue = [&](int32_t n, uint16_t* tile, float* rn) {
-    tile_dma<4>(kcur, n * kTileKeys, n_cur - 1, tile);
-    if (wave == 0)
-      __builtin_amdgcn_global_load_lds(rn_cur + min(n * kTileKeys + lane, n_cur - 1), (lds_void_t)rn, 4, 0, 0);
+    dma.issue(kcur, n * kTileKeys, n_cur - 1, tile);
+    if (wave == 0) {
+      uint32_t dst = uint32_t(reinterpret_cast<uintptr_t>(rn));
+      asm volatile("" : "+s"(dst));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rn_rsrc, (lds_void_t)(uintptr_t)dst, 4,
+                                               uint32_t(min(n * kTileKeys + lane, n_cur - 1)) * 4u, 0, 0, 0);
+    }
   };
   issue(0, ks0, rn0);
   if (ntiles > 1) issue(1, ks1, rn1);
@@ -204,28 +212,29 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
   // 2-3); the 32 MFMAs of one half are issued among the scale-and-max
   // instructions of the other half (carried across the tile boundary), and
   // the B operand is read from LDS one k-step ahead of its MFMAs.
+  // The B fragments of the tile's eight k-steps (g = 4 h + kk: half h, k-step
+  // kk) go through a three-slot register ring, read two k-steps ahead of
+  // their MFMAs -- including the first two k-steps of the second half, which
+  // are read under the first half's MFMAs.
+  bf16x8_t kb[3][2];
+  auto read_b = [&](const uint16_t* tile, int g) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) kb[g % 3][t] = tile_b_operand(tile, 2 * (g / 4) + t, g % 4);
+  };
   auto mfma_half = [&](const uint16_t* tile, int h, f32x4_t (&acc)[4][2]) {
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int t = 0; t < 2; ++t) acc[b][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    bf16x8_t kb[3][2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      kb[0][t] = tile_b_operand(tile, 2 * h + t, 0);
-      kb[1][t] = tile_b_operand(tile, 2 * h + t, 1);
-    }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      if (kk + 2 < 4) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) kb[(kk + 2) % 3][t] = tile_b_operand(tile, 2 * h + t, kk + 2);
-      }
+      const int g = 4 * h + kk;
+      if (g + 2 < 8) read_b(tile, g + 2);
 #pragma unroll
       for (int b = 0; b < 4; ++b)
 #pragma unroll
         for (int t = 0; t < 2; ++t)
-          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[kk % 3][t], acc[b][t], 0, 0, 0);
+          acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[g % 3][t], acc[b][t], 0, 0, 0);
     }
   };
   auto max_half = [&](const f32x4_t (&acc)[4][2], float rn0, float rn1) {
@@ -235,13 +244,13 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
       for (int i = 0; i < 4; ++i)
         runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rn0), acc[b][1][i] * rn1);
   };
-  // Per half: the B fragments of k-step kk+2 are read while the MFMAs of
-  // k-step kk run (LDS latency stays off the MFMA stream).
-  auto interleave = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // B fragments of k-steps 0 and 1
+  // Per half: B fragments read under the MFMAs of earlier k-steps, 3 VALU
+  // (scale and max of the other half) per 2 MFMAs.
+  auto interleave = [&](int h) {
+    if (h == 0) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // k-steps 0 and 1
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      if (kk + 2 < 4) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // prefetch k-step kk+2
+      if (4 * h + kk + 2 < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // read ahead
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
@@ -269,13 +278,15 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
     barrier_lds();
     const float rnA0 = rn[0 * 16 + (lane & 15)], rnA1 = rn[1 * 16 + (lane & 15)];
     const float rnN0 = rn[2 * 16 + (lane & 15)], rnN1 = rn[3 * 16 + (lane & 15)];
-    if (n + 2 < ntiles) issue(n + 2, nxt, nxt_rn);
+    read_b(tile, 0);
+    read_b(tile, 1);
     mfma_half(tile, 0, accA);
     max_half(accB, rnB0, rnB1);
-    interleave();
+    interleave(0);
+    if (n + 2 < ntiles) issue(n + 2, nxt, nxt_rn);
     mfma_half(tile, 1, accB);
     max_half(accA, rnA0, rnA1);
-    interleave();
+    interleave(1);
     rnB0 = rnN0;
     rnB1 = rnN1;
   };
