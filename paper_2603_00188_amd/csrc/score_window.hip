@@ -4,15 +4,20 @@
 // A column sum of softmax rows needs every row's normaliser first, so the
 // logits Q K^T are formed twice on the matrix cores (bf16 MFMA, fp32
 // accumulate):
-//   pass 1  (rowstats) per key chunk: running (max, sum of 2^x) per window row,
-//   combine            per row: log2 of the softmax denominator over all chunks,
-//   pass 2  (colsum)   per key chunk: 2^(x - lse) summed over the G*window rows.
-// Both passes keep the whole GQA group's window queries resident in VGPRs as
-// the MFMA A operand (up to eight waves, each owning up to four 16-row blocks)
-// and stream 64-key tiles of K, DMA'd into a three-stage LDS ring, as the B
-// operand shared by all waves.  Inside a wave the MFMAs of one row block run
-// under the softmax arithmetic of the previous one.
+//   pass 1  per key chunk: per window row, sum of 2^(x - o) for a fixed
+//           offset o (the maximum over the chunk's first tile of the row's
+//           group of eight rows),
+//   combine per row: log2 of the softmax denominator over all chunks,
+//   pass 2  per key chunk: 2^(x - lse) summed over the G*window rows.
 // Logits are kept in log2 units: x = (q . k) * log2(e) / sqrt(d).
+//
+// Both passes use v_mfma_f32_32x32x16_bf16.  A work-group holds the whole
+// GQA group's window queries resident in VGPRs as the A operand (ceil(blocks
+// / 2) waves, each with up to two 32-row blocks) and streams 64-key tiles of K -- two 32-key blocks --
+// through a three-stage LDS ring filled by DMA; the tiles are the B operand
+// shared by all waves.  Every exponential and sum of one key block is issued
+// between the MFMAs of the other, in an order fixed in the source: the long
+// 32x32 MFMAs hide that vector work, which the short 16x16 forms cannot.
 #include "stlite_internal.h"
 #include "tile_lds.h"
 
@@ -20,6 +25,7 @@ namespace stlite {
 namespace {
 
 constexpr float kNegBig = -1.0e30f;
+constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
 struct ChunkPos {
   int32_t seq, seq_start, seq_len, c0, c1, gchunk;
@@ -46,317 +52,365 @@ __device__ inline ChunkPos locate_chunk(const Layout& lay, int32_t chunk, int32_
   return r;
 }
 
-__device__ inline bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// Row blocks are dealt to waves round-robin (wave w owns blocks w, w + NW, ...),
-// so that each SIMD of the CU gets the same number of real 16-row blocks.
+// 32-row blocks are dealt to waves round-robin: wave w owns blocks w, w + NW.
 template <int NW>
-__device__ inline int block_of(int j) { return (threadIdx.x >> 6) + j * NW; }
+__device__ inline int block_of(int j) { return wave_id() + j * NW; }
 
+// Window queries as the A operand: lane l holds row l & 31 of each block;
+// k-step kk takes dims 16 kk + 8 (l >> 5) .. +7.
 template <int RB, int NW>
-__device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int unit, bf16x8_t (&qa)[RB][4]) {
+__device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int unit, bf16x8_t (&qa)[RB][8]) {
   const int lane = threadIdx.x & 63;
   const int layer = unit / a.lay.n_kv_heads, kv = unit % a.lay.n_kv_heads;
   const uint16_t* qbase =
       a.q + ((size_t(layer) * a.lay.n_seqs + cp.seq) * a.n_q_heads + size_t(kv) * a.group) * a.window * kHeadDim;
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
-    const int row = block_of<NW>(b) * 16 + (lane & 15);
+    const int row = block_of<NW>(b) * 32 + (lane & 31);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    for (int kk = 0; kk < 8; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
       if (row < a.rows)
-        v = *reinterpret_cast<const uint4*>(qbase + size_t(row) * kHeadDim + kk * 32 + (lane >> 4) * 8);
-      qa[b][kk] = as_bf16x8(v);
+        v = *reinterpret_cast<const uint4*>(qbase + size_t(row) * kHeadDim + kk * 16 + (lane >> 5) * 8);
+      qa[b][kk] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 }
 
-// Q K^T of half a tile (32 keys: sub-tiles 2h and 2h+1) for row block b: two
-// 16x16 accumulators, two interleaved MFMA chains over the k-steps.
-template <int RB>
-__device__ inline void half_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[2][4], int b, f32x4_t (&acc)[2]) {
-#pragma unroll
-  for (int t = 0; t < 2; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-    for (int t = 0; t < 2; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[t], 0, 0, 0);
-}
-
-__device__ inline void load_half_b(const uint16_t* tile, int h, bf16x8_t (&kb)[2][4]) {
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) kb[t][kk] = tile_b_operand(tile, 2 * h + t, kk);
-}
-
-// Ask the scheduler to alternate one MFMA with `valu` vector instructions, so
-// that the softmax arithmetic of one group of blocks runs under the next
-// group's MFMAs (8 MFMAs per block).
-template <int valu, int GP>
-__device__ inline void interleave_mfma_valu() {
-#pragma unroll
-  for (int i = 0; i < 8 * GP; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, valu, 0);
-  }
-}
-
-// Masked tiles read each window row's last visible key (local index; -1 for
-// padding rows) from a small LDS table instead of keeping it in VGPRs.
+// Each window row's last visible key (local index; -1 for padding rows), in
+// LDS for the masked tiles.
 __device__ inline void fill_row_limits(const ScoreArgs& a, const ChunkPos& cp, int32_t* lim_s) {
   for (int r = threadIdx.x; r < a.rows_pad; r += blockDim.x)
     lim_s[r] = r < a.rows ? min(cp.seq_len - a.window + (r % a.window), cp.c1 - 1) : -1;
 }
 
-// Sets the two values of row i of block b (sub-tiles 2h, 2h+1) that the row
-// may not see to -inf.
-template <int NW, bool MASK>
-__device__ inline void mask_pair(int32_t t0, int h, int b, int i, const int32_t* lim_s, float (&v)[2]) {
-  if (MASK) {
-    const int lane = threadIdx.x & 63;
-    const int32_t lim = lim_s[block_of<NW>(b) * 16 + (lane >> 4) * 4 + i];
+// Accumulator start of a masked tile: -inf where the row may not see the key
+// (past its causal limit or past the chunk), 0 elsewhere.
+template <int NW>
+__device__ inline f32x16_t mask_init(int32_t t0, int kb, int rb, const int32_t* lim_s) {
+  const int lane = threadIdx.x & 63;
+  const int32_t key = t0 + kb * 32 + (lane & 31);
+  const int base = block_of<NW>(rb) * 32;
+  f32x16_t m;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-      if (t0 + (2 * h + t) * 16 + (lane & 15) > lim) v[t] = -INFINITY;
-  }
+  for (int i = 0; i < 16; ++i) m[i] = key > lim_s[base + acc32_row(i, lane)] ? -INFINITY : 0.0f;
+  return m;
 }
 
-// Pass 1 keeps, per lane and window row, an offset o (log2 units) and
-// sum = sum of 2^(x s - o) over the lane's keys, s = log2(e)/sqrt(d).  The
-// offsets are the lane's row maxima over the chunk's first tile; every tile
-// then only adds 2^(x s - o).  A logit more than ~128 above its offset
-// overflows the sum to +inf, and score_rowstats_exact_kernel recomputes that
-// chunk.
-constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
-// Row blocks whose MFMAs are issued together (2 accumulators each).
-constexpr int kRowGroup = 2;
-constexpr int kColGroup = 2;
-
-template <int RB, int NW, bool MASK>
-__device__ inline void rowstats_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
-                                     const float (&o)[RB][4], float (&sum)[RB][4]) {
+// Butterfly over the 32 lanes that hold the same rows (xor 1 .. 16).
+__device__ inline float row_max32(float v) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float v[2] = {acc[0][i], acc[1][i]};
-    mask_pair<NW, MASK>(t0, h, b, i, lim_s, v);
-    sum[b][i] += __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -o[b][i])) +
-                 __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -o[b][i]));
-  }
+  for (int o = 1; o < 32; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
 }
 
-template <int RB, int NW, bool MASK>
-__device__ inline void colsum_half(int32_t t0, int h, int b, const f32x4_t (&acc)[2], const int32_t* lim_s,
-                                   const float (&lse)[RB][4], float (&col)[2]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float v[2] = {acc[0][i], acc[1][i]};
-    mask_pair<NW, MASK>(t0, h, b, i, lim_s, v);
-    col[0] += __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -lse[b][i]));
-    col[1] += __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -lse[b][i]));
-  }
-}
-
-// Q K^T of half a tile for the blocks of group g (GP blocks from block g*GP):
-// 2*GP independent 16x16 accumulators, interleaved over the k-steps.
-template <int RB, int GP>
-__device__ inline void group_logits(const bf16x8_t (&qa)[RB][4], const bf16x8_t (&kb)[2][4], int g, bool last_real,
-                                    f32x4_t (&acc)[GP][2]) {
-#pragma unroll
-  for (int j = 0; j < GP; ++j)
-#pragma unroll
-    for (int t = 0; t < 2; ++t) acc[j][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-    for (int j = 0; j < GP; ++j) {
-      const int b = g * GP + j;
-      if (b < RB - 1 || (b == RB - 1 && last_real))
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[b][kk], kb[t][kk], acc[j][t], 0, 0, 0);
-    }
-}
-
-// One tile of pass 1 (PASS == 1) or pass 2 (PASS == 2), as two 32-key halves;
-// within a half the blocks go in groups of GP, and the MFMAs of group g+1 are
-// issued among the vector instructions of group g.
-template <int RB, int NW, int PASS, bool MASK, int GP>
-__device__ inline void score_tile(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4], const uint16_t* tile,
-                                  const int32_t* lim_s, const float (&o)[RB][4], float (&sum)[RB][4],
-                                  float (&col)[4]) {
-  constexpr int NG = (RB + GP - 1) / GP;
-  const bool last_real = block_of<NW>(RB - 1) < a.blocks;  // wave-uniform
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    bf16x8_t kb[2][4];
-    load_half_b(tile, h, kb);
-    f32x4_t acc[2][GP][2];
-    group_logits<RB, GP>(qa, kb, 0, last_real, acc[0]);
-    float c2[2] = {0.f, 0.f};
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      if (g + 1 < NG) group_logits<RB, GP>(qa, kb, g + 1, last_real, acc[(g + 1) & 1]);
-#pragma unroll
-      for (int j = 0; j < GP; ++j) {
-        const int b = g * GP + j;
-        if (b < RB - 1 || (b == RB - 1 && last_real)) {
-          if (PASS == 1)
-            rowstats_half<RB, NW, MASK>(t0, h, b, acc[g & 1][j], lim_s, o, sum);
-          else
-            colsum_half<RB, NW, MASK>(t0, h, b, acc[g & 1][j], lim_s, o, c2);
-        }
-      }
-      interleave_mfma_valu<3, GP>();
-      __builtin_amdgcn_sched_barrier(0);  // at most two groups' accumulators live
-    }
-    if (PASS == 2) {
-      col[2 * h] += c2[0];
-      col[2 * h + 1] += c2[1];
-    }
-  }
-}
-
-// Merge the 16 lanes that hold the same rows (different key columns) and
-// write the chunk's (offset, sum) per window row; log2 units.
-template <int RB, int NW>
-__device__ inline void write_partials(const ScoreArgs& a, const ChunkPos& cp, int unit, const float (&o)[RB][4],
-                                      const float (&sum)[RB][4]) {
+// Sum of v over the 32 lanes holding the same rows, for all 16 registers at
+// once: a reduce-scatter that halves the registers each level (xor 16 .. 1).
+// On return v[0] of lane l holds the total of register reg_of(l) where
+// reg_of(l) = 8 b4 + 4 b3 + 2 b2 + b1 + ... (the lane's bits 4..1 pick it).
+__device__ inline float sum32_scatter(float (&v)[16]) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int b = 0; b < RB; ++b)
+  for (int lvl = 0; lvl < 4; ++lvl) {
+    const int half = 8 >> lvl;            // registers kept after this level
+    const int bit = (lane >> (4 - lvl)) & 1;  // lane bit 4, 3, 2, 1
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float mm = o[b][i], ss = sum[b][i];
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const float mo = __shfl_xor(mm, off);
-        const float so = __shfl_xor(ss, off);
-        const float mx = fmaxf(mm, mo);
-        ss = ss * __builtin_amdgcn_exp2f(mm - mx) + so * __builtin_amdgcn_exp2f(mo - mx);
-        mm = mx;
-      }
-      if ((lane & 15) == 0) {
-        const int r = block_of<NW>(b) * 16 + (lane >> 4) * 4 + i;
-        a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(mm, ss);
-      }
+    for (int j = 0; j < half; ++j) {
+      const float send = bit ? v[j] : v[j + half];
+      const float keep = bit ? v[j + half] : v[j];
+      v[j] = keep + __shfl_xor(send, 16 >> lvl);
     }
-}
-
-// Pass 1 offsets: the lane's maximum of each row over the first tile (raw
-// logits of masked-out keys excluded; a row that sees none of them sees none
-// of the chunk's later keys either and gets kNegBig).
-template <int RB, int NW>
-__device__ inline void first_tile_offsets(const ScoreArgs& a, int32_t t0, const bf16x8_t (&qa)[RB][4],
-                                          const uint16_t* tile, const int32_t* lim_s, float (&o)[RB][4]) {
-#pragma unroll
-  for (int b = 0; b < RB; ++b) {
-    float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-    if (block_of<NW>(b) < a.blocks) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        bf16x8_t kb[2][4];
-        load_half_b(tile, h, kb);
-        f32x4_t acc[2];
-        half_logits<RB>(qa, kb, b, acc);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v[2] = {acc[0][i], acc[1][i]};
-          mask_pair<NW, true>(t0, h, b, i, lim_s, v);
-          mx[i] = __builtin_fmaxf(__builtin_fmaxf(mx[i], v[0]), v[1]);
-        }
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[b][i] = mx[i] == -INFINITY ? kNegBig : mx[i] * kScale2;
   }
+  return v[0] + __shfl_xor(v[0], 1);
 }
 
-template <int RB, int NW>
-__global__ __launch_bounds__(NW * 64) void score_rowstats_kernel(ScoreArgs a) {
+// Register that sum32_scatter leaves in lane l.
+__device__ inline int scatter_reg(int lane) {
+  return 8 * ((lane >> 4) & 1) + 4 * ((lane >> 3) & 1) + 2 * ((lane >> 2) & 1) + ((lane >> 1) & 1);
+}
+
+// One pass over a chunk of keys.  PASS 1 writes per-row (offset, sum) for the
+// chunk (and flags the chunk if a sum overflowed); PASS 2 writes A for the
+// chunk's keys.
+template <int PASS, int RB, int NW>
+__global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_pass_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
-  __shared__ int32_t lim_s[NW * RB * 16];
+  __shared__ int32_t lim_s[NW * RB * 32];
+  __shared__ float red_s[2][NW][kTileKeys];
   __shared__ int32_t risky;
   const int unit = blockIdx.y;
   const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
   if (cp.seq < 0) return;
-  if (threadIdx.x == 0) risky = 0;
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_id();
+  if (PASS == 1 && threadIdx.x == 0) risky = 0;
   fill_row_limits(a, cp, lim_s);
-  bf16x8_t qa[RB][4];
+  // The wave's last block may lie past the real rows (uniform).
+  const bool last_real = block_of<NW>(RB - 1) < a.blocks;
+
+  bf16x8_t qa[RB][8];
   load_queries<RB, NW>(a, cp, unit, qa);
+  // Pass 1: offsets o of the row groups g = i >> 2 (rows 8 g .. 8 g + 7 of a
+  // block); pass 2: row log-normalisers lse.  Both in log2 units.
+  float ofs[RB][4];
+  float lse[RB][16];
+  if (PASS == 2) {
+    const float* lrow = a.lse2 + (size_t(unit) * a.lay.n_seqs + cp.seq) * a.rows_pad;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) lse[rb][i] = lrow[block_of<NW>(rb) * 32 + acc32_row(i, lane)];
+  }
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
   const TileDma<NW> dma;
   // Tiles that end before the window starts are visible to every row: no mask.
   const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
   const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
-  constexpr int kLoads = 16 / NW;  // tile DMA wave-loads per wave
   dma.issue(kseq, cp.c0, cp.c1 - 1, ks0);
   if (ntiles > 1) dma.issue(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
 
-  float o[RB][4], sum[RB][4], col_unused[4];
-  {
-    if (ntiles > 1) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
-    barrier_lds();
-    first_tile_offsets<RB, NW>(a, cp.c0, qa, ks0, lim_s, o);
-  }
-#pragma unroll
-  for (int b = 0; b < RB; ++b)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sum[b][i] = 0.0f;
+  f32x16_t acc[2][RB];  // [key block][row block]
+  bf16x8_t kbuf[4];     // B fragments g = 8 kb + kk, read three MFMA groups ahead
+  float sum[RB][16];    // pass 1
+  float col[2];         // pass 2: two partial column sums of the block being summed
+  const float inv_g = 1.0f / float(a.group);
+  float* aout = a.a_base + size_t(unit) * a.lay.total_tokens + cp.seq_start;
 
-  auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt) {
-    if (n > 0) {
-      if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
-      barrier_lds();
-    }
-    if (n + 2 < ntiles) dma.issue(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
-    const int32_t t0 = cp.c0 + n * kTileKeys;
-    if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 1, false, kRowGroup>(a, t0, qa, tile, lim_s, o, sum, col_unused);
+  auto read_b = [&](const uint16_t* tile, int g) { kbuf[g % 4] = tile_b32_operand(tile, g / 8, g % 8); };
+  // Rows of a padded block are zero queries: their MFMAs run (which keeps the
+  // loop free of branches) but nothing of them is written.
+  auto real = [&](int rb) { return rb < RB - 1 || last_real; };
+  // Tiles before clean_end need no mask; only the chunk's last tiles can.
+  const int32_t n_clean = max(0, min(ntiles, (clean_end - cp.c0) / kTileKeys));
+
+  // Tile 0 (and tile 1) landed.
+  wait_vmcnt<0>();
+  barrier_lds();
+
+  if (PASS == 1) {
+    // Offsets: each row group's maximum over the first tile (masked keys
+    // excluded; a group that sees none of them sees none of the chunk and
+    // gets kNegBig).  A row far below its group's offset can underflow its
+    // sum; the chunk is then flagged for the exact pass.
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        read_b(ks0, 8 * kb + kk);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              qa[rb][kk], kbuf[(8 * kb + kk) % 4], kk == 0 ? mask_init<NW>(cp.c0, kb, rb, lim_s) : acc[kb][rb], 0, 0,
+              0);
+      }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 4 * g; i < 4 * g + 4; ++i) m = fmaxf(m, fmaxf(acc[0][rb][i], acc[1][rb][i]));
+        m = row_max32(m);
+        m = fmaxf(m, __shfl_xor(m, 32));
+        ofs[rb][g] = m == -INFINITY ? kNegBig : m * kScale2;
+      }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sum[rb][i] = 0.0f;
+  }
+
+  // Vector work on element i of row block rb of key block kb's accumulators.
+  auto elem = [&](int kb, int rb, int i) {
+    if (PASS == 1)
+      sum[rb][i] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i], kScale2, -ofs[rb][i >> 2]));
     else
-      score_tile<RB, NW, 1, true, kRowGroup>(a, t0, qa, tile, lim_s, o, sum, col_unused);
+      col[i & 1] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i], kScale2, -lse[rb][i]));
   };
-  for (int32_t n = 0; n < ntiles; n += 3) {
-    step(n, ks0, ks2);
-    if (n + 1 < ntiles) step(n + 1, ks1, ks0);
-    if (n + 2 < ntiles) step(n + 2, ks2, ks1);
+  // The same for two elements at a fixed place in the instruction stream:
+  // the scale reaches them through an empty volatile asm on a scalar copy
+  // and their results feed another, and such statements keep their order
+  // relative to the scheduling barriers -- so the arithmetic can be neither
+  // hoisted above the preceding MFMA nor sunk below the next one.
+  auto elem_pinned = [&](int kb, int rb, int i) {
+    float sc = kScale2;
+    asm volatile("" : "+s"(sc));
+    if (PASS == 1) {
+      sum[rb][i] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i], sc, -ofs[rb][i >> 2]));
+      sum[rb][i + 1] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i + 1], sc, -ofs[rb][i >> 2]));
+      asm volatile("" ::"v"(sum[rb][i]), "v"(sum[rb][i + 1]));
+    } else {
+      col[0] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i], sc, -lse[rb][i]));
+      col[1] += __builtin_amdgcn_exp2f(fmaf(acc[kb][rb][i + 1], sc, -lse[rb][i + 1]));
+      asm volatile("" ::"v"(col[0]), "v"(col[1]));
+    }
+  };
+  // Pass 2: the wave's column sums of key block kb of tile n go to LDS.
+  auto put_cols = [&](int32_t n, int kb) {
+    float c = col[0] + col[1];
+    c += __shfl_xor(c, 32);
+    if (lane < 32) red_s[n & 1][wave][kb * 32 + lane] = c;
+  };
+  // Pass 2: A of tile n's keys, once every wave's column sums are in LDS.
+  auto reduce = [&](int32_t n) {
+    if (threadIdx.x < kTileKeys) {
+      float s = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red_s[n & 1][w][threadIdx.x];
+      const int32_t j = cp.c0 + n * kTileKeys + threadIdx.x;
+      if (j < cp.c1) aout[j] = s * inv_g;
+    }
+  };
+  // Section kb of a clean tile: the MFMAs of key block kb, each MFMA followed
+  // by the vector work on two elements of key block kb ^ 1 (i and i + 1 of
+  // the same row group, i even), in that order.
+  // B fragments past the tile's sixteen are the next tile's first three.
+  auto section = [&](int kb, const uint16_t* tile, const uint16_t* next) {
+    col[0] = 0.0f;
+    col[1] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const int g = 8 * kb + kk;
+      if (g + 3 < 16)
+        read_b(tile, g + 3);
+      else
+        read_b(next, g + 3 - 16);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[rb][kk], kbuf[g % 4],
+                                                              kk == 0 ? f32x16_t{} : acc[kb][rb], 0, 0, 0);
+        elem_pinned(kb ^ 1, rb, 2 * kk);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  if (n_clean > 0) {
+    // The "previous key block 1" before the first tile contributes nothing.
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[1][rb][i] = -INFINITY;
+    read_b(ks0, 0);
+    read_b(ks0, 1);
+    read_b(ks0, 2);
+    // One clean tile.  Between its sections: wait for tile n+1's DMA, barrier
+    // (every wave is past tile n-1, whose stage the DMA of tile n+2 then
+    // overwrites), and in pass 2 the finished column sums of tile n-1.
+    auto step = [&](int32_t n, const uint16_t* tile, const uint16_t* next, uint16_t* nxt2) {
+      section(0, tile, next);
+      if (PASS == 2) put_cols(n - 1, 1);
+      wait_vmcnt<0>();
+      barrier_lds();
+      if (PASS == 2 && n > 0) reduce(n - 1);
+      if (n + 2 < ntiles) dma.issue(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt2);
+      __builtin_amdgcn_sched_barrier(0);
+      section(1, tile, next);
+      if (PASS == 2) put_cols(n, 0);
+    };
+    for (int32_t n = 0; n < n_clean; n += 3) {
+      step(n, ks0, ks1, ks2);
+      if (n + 1 < n_clean) step(n + 1, ks1, ks2, ks0);
+      if (n + 2 < n_clean) step(n + 2, ks2, ks0, ks1);
+    }
+    // Key block 1 of the last clean tile.
+    col[0] = 0.0f;
+    col[1] = 0.0f;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) elem(1, rb, i);
+    if (PASS == 2) {
+      put_cols(n_clean - 1, 1);
+      barrier_lds();
+      reduce(n_clean - 1);
+    }
   }
 
-  write_partials<RB, NW>(a, cp, unit, o, sum);
-  bool bad = false;
+  // The masked tiles at the end of the chunk, one at a time.
+  auto stage = [&](int32_t n) { return n % 3 == 0 ? ks0 : (n % 3 == 1 ? ks1 : ks2); };
+  for (int32_t n = n_clean; n < ntiles; ++n) {
+    const int32_t t0 = cp.c0 + n * kTileKeys;
+    wait_vmcnt<0>();
+    barrier_lds();
+    if (n + 2 < ntiles) dma.issue(kseq, t0 + 2 * kTileKeys, cp.c1 - 1, stage(n + 2));
+    const uint16_t* tile = stage(n);
 #pragma unroll
-  for (int b = 0; b < RB; ++b)
+    for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) bad |= !(sum[b][i] < INFINITY);
-  if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(&risky, 1);
-  __syncthreads();
-  if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = risky;
+      for (int kk = 0; kk < 8; ++kk) {
+        read_b(tile, 8 * kb + kk);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              qa[rb][kk], kbuf[(8 * kb + kk) % 4], kk == 0 ? mask_init<NW>(t0, kb, rb, lim_s) : acc[kb][rb], 0, 0,
+              0);
+      }
+      col[0] = 0.0f;
+      col[1] = 0.0f;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) elem(kb, rb, i);
+      if (PASS == 2) put_cols(n, kb);
+    }
+    if (PASS == 2) {
+      barrier_lds();
+      reduce(n);
+    }
+  }
+
+  if (PASS == 1) {
+    // (offset, sum) per row: the offset is common to the 32 lanes of a row, so
+    // the chunk's sum is a plain sum over them.  A row that sees a key of the
+    // chunk but whose sum overflowed, or underflowed below 2^-60 (its logits
+    // far under its group's offset), sends the chunk to the exact pass.
+    bool bad = false;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float s = sum32_scatter(sum[rb]);
+      const int i = scatter_reg(lane);
+      const int r = block_of<NW>(rb) * 32 + acc32_row(i, lane);
+      float o = ofs[rb][0];
+#pragma unroll
+      for (int g = 1; g < 4; ++g) o = (i >> 2) == g ? ofs[rb][g] : o;
+      if ((lane & 1) == 0 && real(rb)) {
+        a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(o, s);
+        bad |= r < a.rows && lim_s[r] >= cp.c0 && !(s >= 0x1.0p-60f && s < INFINITY);
+      }
+    }
+    if (__ballot(bad) != 0 && lane == 0) atomicOr(&risky, 1);
+    __syncthreads();
+    if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = risky;
+  }
 }
 
-// Exact pass 1 for the chunks flagged by score_rowstats_kernel: a running row
-// max per lane with the sums rescaled on every tile (plain staging; it only
-// runs when a chunk's logits rise far enough above the first tile's to overflow the
-// lean pass's sums).
+// Exact pass 1 for the chunks flagged by the lean pass: a running row max per
+// lane with the sums rescaled on every tile (plain staging; it only runs when
+// a chunk's logits rise far enough above the first tile's to overflow the lean
+// pass's sums).
 template <int RB, int NW>
-__global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_rowstats_exact_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems];
-  __shared__ int32_t lim_s[NW * RB * 16];
+  __shared__ int32_t lim_s[NW * RB * 32];
   const int unit = blockIdx.y;
   if (a.redo[size_t(unit) * a.total_chunks + blockIdx.x] == 0) return;
   const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
   if (cp.seq < 0) return;
+  const int lane = threadIdx.x & 63;
   fill_row_limits(a, cp, lim_s);
-  bf16x8_t qa[RB][4];
+  bf16x8_t qa[RB][8];
   load_queries<RB, NW>(a, cp, unit, qa);
-  float m[RB][4], sum[RB][4];
+  float m[RB][16], sum[RB][16];
 #pragma unroll
-  for (int b = 0; b < RB; ++b)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      m[b][i] = kNegBig;
-      sum[b][i] = 0.0f;
+    for (int i = 0; i < 16; ++i) {
+      m[rb][i] = kNegBig;
+      sum[rb][i] = 0.0f;
     }
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
   const TileDma<NW> dma;
@@ -366,34 +420,43 @@ __global__ __launch_bounds__(NW * 64) void score_rowstats_exact_kernel(ScoreArgs
     wait_vmcnt<0>();
     __syncthreads();
 #pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      if (block_of<NW>(b) >= a.blocks) break;
+    for (int rb = 0; rb < RB; ++rb) {
+      if (block_of<NW>(rb) >= a.blocks) break;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        bf16x8_t kb[2][4];
-        load_half_b(ks0, h, kb);
-        f32x4_t acc[2];
-        half_logits<RB>(qa, kb, b, acc);
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16_t acc = mask_init<NW>(t0, kb, rb, lim_s);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v[2] = {acc[0][i], acc[1][i]};
-          mask_pair<NW, true>(t0, h, b, i, lim_s, v);
-          const float mx = __builtin_fmaxf(__builtin_fmaxf(m[b][i], v[0]), v[1]);
-          const float ms = mx * kScale2;
-          sum[b][i] = sum[b][i] * __builtin_amdgcn_exp2f(fmaf(m[b][i], kScale2, -ms)) +
-                      __builtin_amdgcn_exp2f(fmaf(v[0], kScale2, -ms)) +
-                      __builtin_amdgcn_exp2f(fmaf(v[1], kScale2, -ms));
-          m[b][i] = mx;
+        for (int kk = 0; kk < 8; ++kk)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[rb][kk], tile_b32_operand(ks0, kb, kk), acc, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float mx = __builtin_fmaxf(m[rb][i], acc[i]);
+          sum[rb][i] = sum[rb][i] * __builtin_amdgcn_exp2f((m[rb][i] - mx) * kScale2) +
+                       __builtin_amdgcn_exp2f((acc[i] - mx) * kScale2);
+          m[rb][i] = mx;
         }
       }
     }
   }
-  float o[RB][4];
+  // Merge the 32 lanes of each row: (max, sum) pairs in log2 units.
 #pragma unroll
-  for (int b = 0; b < RB; ++b)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[b][i] = m[b][i] * kScale2;
-  write_partials<RB, NW>(a, cp, unit, o, sum);
+    for (int i = 0; i < 16; ++i) {
+      float mm = m[rb][i] * kScale2, ss = sum[rb][i];
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) {
+        const float mo = __shfl_xor(mm, off);
+        const float so = __shfl_xor(ss, off);
+        const float mx = fmaxf(mm, mo);
+        ss = ss * __builtin_amdgcn_exp2f(mm - mx) + so * __builtin_amdgcn_exp2f(mo - mx);
+        mm = mx;
+      }
+      if ((lane & 31) == 0 && block_of<NW>(rb) < a.blocks) {
+        const int r = block_of<NW>(rb) * 32 + acc32_row(i, lane);
+        a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(mm, ss);
+      }
+    }
 }
 
 // Per (sequence, row): lse = log2 of the softmax denominator over the
@@ -428,88 +491,11 @@ __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
   }
 }
 
-// Pass 2 on one tile: col[t] += 2^(x s - lse) over the lane's rows, for the
-// lane's key column of sub-tile t.
-// Pass 2.  A_j = (1/G) sum over rows of 2^(x_rj - lse_r): the lane's four
-// rows per block are summed in registers, then across the four lane groups
-// that share a key column, then across waves in LDS.
-template <int RB, int NW>
-__global__ __launch_bounds__(NW * 64) void score_colsum_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
-  __shared__ float red0[NW][kTileKeys], red1[NW][kTileKeys], red2[NW][kTileKeys];
-  __shared__ int32_t lim_s[NW * RB * 16];
-  const int unit = blockIdx.y;
-  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
-  if (cp.seq < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float inv_g = 1.0f / float(a.group);
-
-  fill_row_limits(a, cp, lim_s);
-  bf16x8_t qa[RB][4];
-  load_queries<RB, NW>(a, cp, unit, qa);
-  float lse[RB][4];
-  const float* lrow = a.lse2 + (size_t(unit) * a.lay.n_seqs + cp.seq) * a.rows_pad;
-#pragma unroll
-  for (int b = 0; b < RB; ++b)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) lse[b][i] = lrow[block_of<NW>(b) * 16 + (lane >> 4) * 4 + i];
-
-  const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
-  const TileDma<NW> dma;
-  float* aout = a.a_base + size_t(unit) * a.lay.total_tokens + cp.seq_start;
-  const int32_t clean_end = min(cp.c1, cp.seq_len - a.window + 1);
-  const int32_t ntiles = (cp.c1 - cp.c0 + kTileKeys - 1) / kTileKeys;
-  constexpr int kLoads = 16 / NW;
-  // Column sums of tile n are reduced across waves after the barrier of step n+1.
-  auto reduce = [&](int32_t n, const float (&r)[NW][kTileKeys]) {
-    if (threadIdx.x < kTileKeys) {
-      float s = 0.0f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) s += r[w][threadIdx.x];
-      const int32_t j = cp.c0 + n * kTileKeys + threadIdx.x;
-      if (j < cp.c1) aout[j] = s * inv_g;
-    }
-  };
-  dma.issue(kseq, cp.c0, cp.c1 - 1, ks0);
-  if (ntiles > 1) dma.issue(kseq, cp.c0 + kTileKeys, cp.c1 - 1, ks1);
-  float sum_unused[RB][4];
-  auto step = [&](int32_t n, const uint16_t* tile, uint16_t* nxt, float (&r)[NW][kTileKeys],
-                  const float (&rprev)[NW][kTileKeys]) {
-    if (n + 1 < ntiles) wait_vmcnt<kLoads>(); else wait_vmcnt<0>();
-    barrier_lds();
-    if (n > 0) reduce(n - 1, rprev);
-    if (n + 2 < ntiles) dma.issue(kseq, cp.c0 + (n + 2) * kTileKeys, cp.c1 - 1, nxt);
-    const int32_t t0 = cp.c0 + n * kTileKeys;
-    float col[4] = {0.f, 0.f, 0.f, 0.f};
-    if (t0 + kTileKeys <= clean_end)
-      score_tile<RB, NW, 2, false, kColGroup>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
-    else
-      score_tile<RB, NW, 2, true, kColGroup>(a, t0, qa, tile, lim_s, lse, sum_unused, col);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      col[t] += __shfl_xor(col[t], 16);
-      col[t] += __shfl_xor(col[t], 32);
-    }
-    if (lane < 16) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t) r[wave][t * 16 + lane] = col[t];
-    }
-  };
-  for (int32_t n = 0; n < ntiles; n += 3) {
-    step(n, ks0, ks2, red0, red2);
-    if (n + 1 < ntiles) step(n + 1, ks1, ks0, red1, red0);
-    if (n + 2 < ntiles) step(n + 2, ks2, ks1, red2, red1);
-  }
-  barrier_lds();
-  const int last = (ntiles - 1) % 3;
-  reduce(ntiles - 1, last == 0 ? red0 : (last == 1 ? red1 : red2));
-}
-
 template <int RB, int NW>
 hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   const dim3 grid(a.total_chunks, a.lay.n_units);
   const dim3 block(64 * NW);
-  hipLaunchKernelGGL((score_rowstats_kernel<RB, NW>), grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_pass_kernel<1, RB, NW>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((score_rowstats_exact_kernel<RB, NW>), grid, block, 0, stream, a);
@@ -518,7 +504,7 @@ hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(score_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((score_colsum_kernel<RB, NW>), grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_pass_kernel<2, RB, NW>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
@@ -527,8 +513,6 @@ hipError_t launch_nw(const ScoreArgs& a, hipStream_t stream) {
   switch (a.row_blocks) {
     case 1: return launch_rb<1, NW>(a, stream);
     case 2: return launch_rb<2, NW>(a, stream);
-    case 3: return launch_rb<3, NW>(a, stream);
-    case 4: return launch_rb<4, NW>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -539,7 +523,11 @@ hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream) {
   switch (a.waves) {
     case 1: return launch_nw<1>(a, stream);
     case 2: return launch_nw<2>(a, stream);
+    case 3: return launch_nw<3>(a, stream);
     case 4: return launch_nw<4>(a, stream);
+    case 5: return launch_nw<5>(a, stream);
+    case 6: return launch_nw<6>(a, stream);
+    case 7: return launch_nw<7>(a, stream);
     case 8: return launch_nw<8>(a, stream);
     default: return hipErrorInvalidValue;
   }

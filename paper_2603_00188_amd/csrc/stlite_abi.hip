@@ -50,13 +50,13 @@ Facts derive(const stlite_problem* p) {
   f.units = int64_t(p->n_layers) * p->n_kv_heads;
   const int32_t G = p->n_q_heads / p->n_kv_heads;
   f.rows = G * p->window;
-  const int nb = (f.rows + 15) / 16;
-  // 1, 2, 4 or 8 waves, each holding at most four resident 16-row blocks.
+  const int nb = (f.rows + 31) / 32;
+  // ceil(nb / 2) waves (1..8), each holding at most two resident 32-row
+  // blocks: at most one padded block.
   f.blocks = nb;
-  f.waves = 1;
-  while (f.waves * 4 < nb) f.waves *= 2;
-  f.row_blocks = (nb + f.waves - 1) / f.waves;
-  f.rows_pad = f.waves * f.row_blocks * 16;
+  f.row_blocks = nb >= 2 ? 2 : 1;
+  f.waves = (nb + f.row_blocks - 1) / f.row_blocks;
+  f.rows_pad = f.waves * f.row_blocks * 32;
   // Key chunk per work-group: aim for >= 2048 work-groups so that all 256 CUs
   // stay busy, while keeping each chunk long enough to amortise the Q load.
   const int64_t work = f.units * p->total_tokens;

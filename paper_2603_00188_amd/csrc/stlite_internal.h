@@ -39,10 +39,10 @@ struct ScoreArgs {
   int32_t group;         // G
   int32_t window;
   int32_t rows;          // G * window
-  int32_t rows_pad;      // waves * row_blocks * 16
-  int32_t blocks;        // ceil(rows / 16) real 16-row blocks
-  int32_t waves;         // 1, 2, 4 or 8
-  int32_t row_blocks;    // 16-row MFMA blocks per wave (1..4)
+  int32_t rows_pad;      // waves * row_blocks * 32
+  int32_t blocks;        // ceil(rows / 32) real 32-row blocks
+  int32_t waves;         // 1 .. 8
+  int32_t row_blocks;    // 32-row MFMA blocks per wave (1 or 2)
   int32_t chunk;         // keys per work-group (multiple of 64)
   int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
 };
@@ -162,6 +162,7 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Total order of fp32 values as unsigned integers (ascending key = ascending
 // value); -0 is folded onto +0 so that the two zeros tie.
