@@ -79,6 +79,11 @@ SMALL = {
     "beta_one": _small([[(F, 4, 5), (T, 10), (F, 4, 5), (T, 10)], [(T, 25)]], beta=(1, 1)),
     "beta_tiny": _small([[(F, 4, 5), (T, 10), (F, 4, 5), (T, 10)], [(T, 25)]], beta=(1, 30)),
     "alpha2": _small([[(F, 7, 9), (T, 20), (F, 7, 9), (T, 20)]], alpha=2.0),
+    # window rows over 2, 3, 5 and 6 waves of 32-row blocks, with padding rows in the last block
+    "g2w40": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 60)]], G=2, Hkv=2, window=40, layers=1),
+    "g3w60": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=3, Hkv=2, window=60, layers=1),
+    "g5w60": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=5, Hkv=1, window=60, layers=1),
+    "g6w64": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=6, Hkv=1, window=64, layers=1),
 }
 
 
@@ -275,3 +280,26 @@ def test_logit_spike_takes_exact_pass(torch_cuda):
         H.compare_unit(case, res, 0, kv, 0)
     A = res["a_base"][0]
     assert A[200] > 0.2 and A[460] > 0.2, "spike keys should carry most of head 0's window mass"
+
+
+def test_logit_spike_in_first_tile_takes_exact_pass(torch_cuda):
+    """A key aligned with one window query, inside the first tile of its chunk,
+    lifts the lean first pass's offset of that query's group of eight rows
+    about 150 log2 units above the other seven rows' logits: their sums
+    underflow, the chunk is flagged and the exact pass recomputes it."""
+    import torch
+    H = _H()
+    from oracle import stlite_oracle as O
+    from paper_2603_00188_amd import workload as W2
+    w = _small([[(F, 12, 21), (T, 37), (F, 12, 21), (T, 37), (F, 12, 21), (T, 150)]],
+               G=4, Hkv=3, window=16, beta=(3, 10), layers=1)
+    case = H.Case(w)
+    q = O.bf16_to_f64(case.q[0, 0, 0, 3])           # head 0, window position 3 (row 3)
+    unit_dir = q / np.linalg.norm(q)
+    spike = W2.to_bf16_bits((700.0 * unit_dir).astype(np.float32))
+    for j in (10, 270):                             # first tile of chunks 0 and 1
+        case.k[0, 0, j] = spike
+    case.dk.copy_(torch.from_numpy(case.k.view(np.int16)))
+    res = case.run()
+    for kv in range(w.n_kv_heads):
+        H.compare_unit(case, res, 0, kv, 0)
