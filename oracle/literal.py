@@ -13,6 +13,8 @@ so that a vectorisation slip in the NumPy oracle shows up as a disagreement:
                                                                         temporal_mask; R7)
   S         = A (text) | M (A + alpha Phi) (visual)  (Eq. modal_scoring)
   I_keep    = first B by (S descending, index ascending), ascending  (Top_B; R16)
+  out_g     = sum_j exp(z_gj) v_j / sum_j exp(z_gj), z = q_g . k_j / sqrt(d)
+                                                    (decode attention over a cache)
 
 It reuses nothing from the NumPy oracle except the bf16 widening rule, which it
 restates with ``struct``.
@@ -146,3 +148,23 @@ def compress(Q, K, frames, B, alpha=1.0, use_css=True, use_tsg=True):
     g = gate(r, hist, L, B) if use_tsg else [1] * L
     S = scores(A, phi, g, visual, alpha if use_css else 0.0)
     return dict(A=A, phi=phi, rho=r, gate=g, S=S, kept=top_b(S, B))
+
+
+def decode_attention(Q, K, V):
+    """Q: list[G][d], K, V: list[n][d] floats; out: list[G][d] (zeros if n = 0)."""
+    G = len(Q)
+    d = len(Q[0])
+    n = len(K)
+    out = [[0.0] * d for _ in range(G)]
+    if n == 0:
+        return out
+    for g in range(G):
+        z = [dot(Q[g], K[j]) / math.sqrt(d) for j in range(n)]
+        m = max(z)
+        e = [math.exp(x - m) for x in z]
+        tot = sum(e)
+        for j in range(n):
+            w = e[j] / tot
+            for c in range(d):
+                out[g][c] += w * V[j][c]
+    return out

@@ -19,6 +19,8 @@ takes them:
   integrate        S = A (text), M (A + alpha Phi) (visual)   (Eq. modal_scoring)
   select_topk      I_keep = Top_B(S)                          (Sec. integrated scoring)
   compact          K' = K[I_keep], V' = V[I_keep]             (algorithm's return value)
+  decode_attention softmax(q K^T / sqrt(d)) V over a cache    (problem setup: the decoding
+                   phase that consumes K', V')
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -273,6 +275,29 @@ def compress_unit(Q_bits: np.ndarray, K_bits: np.ndarray, V_bits: np.ndarray,
     k_out, v_out = compact(K_bits, V_bits, kept)
     return dict(B=B, A=A, phi=phi, hist=hist, cur=cur, rho=rho, gate=gate, tau=tau,
                 S=S, kept=kept, k_out=k_out, v_out=v_out, visual=visual)
+
+
+# ---------------------------------------------------------------------------
+# Decode attention over a cache (problem setup: after prefill, the decoding
+# phase attends each new query over the cached keys and values; the
+# compression procedure hands K', V' to that phase)
+# ---------------------------------------------------------------------------
+
+def decode_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """out_g = sum_j softmax_j(q_g . k_j / sqrt(d)) v_j for every query row g.
+
+    Q [G, d], K and V [n, d] as float64; the decode query follows every cached
+    row, so no row is masked.  A cache with no rows gives zeros."""
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    if K.shape[0] == 0:
+        return np.zeros((Q.shape[0], V.shape[1]))
+    z = (Q @ K.T) / math.sqrt(K.shape[1])
+    z = z - z.max(axis=1, keepdims=True)
+    p = np.exp(z)
+    p = p / p.sum(axis=1, keepdims=True)
+    return p @ V
 
 
 def seq_frames_local(cu_seqlens, cu_frames, frame_meta, s: int):

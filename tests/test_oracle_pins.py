@@ -398,3 +398,80 @@ def test_bf16_widening_matches_torch():
     finite = ((bits >> 7) & 0xFF) != 0xFF
     want = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
     np.testing.assert_array_equal(O.bf16_to_f64(bits)[finite], want[finite])
+
+
+# ------------------------------------------- decode attention over a cache --
+
+def test_decode_single_row_and_empty_cache():
+    rng = np.random.default_rng(21)
+    Q = rng.standard_normal((3, 128))
+    K = rng.standard_normal((1, 128))
+    V = rng.standard_normal((1, 128))
+    # softmax over one row is 1: every query returns that row's value
+    np.testing.assert_array_equal(O.decode_attention(Q, K, V), np.repeat(V, 3, axis=0))
+    assert not O.decode_attention(Q, K[:0], V[:0]).any()
+
+
+def test_decode_uniform_logits_is_mean_of_values():
+    rng = np.random.default_rng(22)
+    K = rng.standard_normal((37, 128))
+    V = rng.standard_normal((37, 128))
+    out = O.decode_attention(np.zeros((2, 128)), K, V)
+    np.testing.assert_allclose(out, np.repeat(V.mean(axis=0, keepdims=True), 2, axis=0), rtol=1e-13, atol=1e-15)
+
+
+def test_decode_two_level_logits_closed_form():
+    """Keys along e1 give logits a (rows in A) and b (rows in B): the output is
+    the mean of A's values weighted e^a against B's weighted e^b."""
+    rng = np.random.default_rng(23)
+    d, a, b = 128, 2.5, -1.0
+    inA = rng.random(40) < 0.3
+    K = np.zeros((40, d))
+    K[:, 0] = np.where(inA, a, b)
+    Q = np.zeros((1, d))
+    Q[0, 0] = math.sqrt(d)
+    V = rng.standard_normal((40, d))
+    want = (math.exp(a) * V[inA].sum(0) + math.exp(b) * V[~inA].sum(0)) / (
+        math.exp(a) * inA.sum() + math.exp(b) * (~inA).sum())
+    np.testing.assert_allclose(O.decode_attention(Q, K, V)[0], want, rtol=1e-12, atol=1e-14)
+
+
+def test_decode_library_softmax_and_invariants():
+    rng = np.random.default_rng(24)
+    Q = rng.standard_normal((7, 128)) * 0.5
+    K = rng.standard_normal((50, 128))
+    V = rng.standard_normal((50, 128))
+    out = O.decode_attention(Q, K, V)
+    P = scipy.special.softmax(Q @ K.T / math.sqrt(128), axis=1)
+    np.testing.assert_allclose(out, P @ V, rtol=1e-12, atol=1e-13)
+    # permuting the cached rows changes nothing; shifting every value by c shifts the output by c
+    perm = rng.permutation(50)
+    np.testing.assert_allclose(O.decode_attention(Q, K[perm], V[perm]), out, rtol=1e-12, atol=1e-13)
+    c = rng.standard_normal(128)
+    np.testing.assert_allclose(O.decode_attention(Q, K, V + c), out + c, rtol=1e-12, atol=1e-12)
+    # a convex combination of the values: inside their per-dimension range
+    assert (out <= V.max(0) + 1e-12).all() and (out >= V.min(0) - 1e-12).all()
+
+
+def test_decode_literal_twin_agrees():
+    rng = np.random.default_rng(25)
+    Q = rng.standard_normal((3, 16))
+    K = rng.standard_normal((11, 16))
+    V = rng.standard_normal((11, 16))
+    lit = O1.decode_attention(Q.tolist(), K.tolist(), V.tolist())
+    np.testing.assert_allclose(O.decode_attention(Q, K, V), lit, rtol=1e-12, atol=1e-14)
+
+
+def test_decode_over_compacted_cache_at_beta_one_is_full_decode():
+    """At beta = 1 the compacted cache is the full cache in token order."""
+    rng = np.random.default_rng(26)
+    L, d = 40, 128
+    Kb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(L, d)), np.uint16)
+    Kb[1::3] |= 0x8000
+    Vb = np.asarray(rng.integers(0x3000, 0x4000, size=(L, d)), np.uint16)
+    Qb = np.asarray(rng.integers(0x3c00, 0x3f80, size=(1, 3, d)), np.uint16)
+    res = O.compress_unit(Qb, Kb, Vb, [(0, 3, 4), (16, 3, 4)], (1, 1))
+    Qd = O.bf16_to_f64(Qb[0, :2])
+    full = O.decode_attention(Qd, O.bf16_to_f64(Kb), O.bf16_to_f64(Vb))
+    comp = O.decode_attention(Qd, O.bf16_to_f64(res["k_out"]), O.bf16_to_f64(res["v_out"]))
+    np.testing.assert_array_equal(full, comp)
