@@ -172,6 +172,41 @@ def cpu_baseline(w, case_inputs, budget_s=12.0, max_units=8):
                       f"({t_total:.1f} s measured)"}
 
 
+def decode_timing(prob, w, q, dk, dv, out, stream, reps=20):
+    """Decode attention (the decoding phase the compression serves) over the
+    full cache and over the compacted cache the last step wrote, timed apart
+    from the pass: one decode query per head, HIP events on the launch
+    stream.  Both are HBM-bound: the bytes are the K and V rows read."""
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    from paper_2603_00188_amd import workload as W
+    q_dec = torch.from_numpy(W.decode_queries(q).view(np.int16)).cuda()
+    res = torch.empty((prob.n_layers, prob.n_seqs, prob.n_q_heads, 128), dtype=torch.float32, device="cuda")
+    units = prob.units
+    entry = {}
+    for name, cache, kk, vv, call, rows in (
+            ("full", S.CACHE_FULL, dk, dv, S.CALL_DECODE_FULL, prob.total_tokens),
+            ("compact", S.CACHE_COMPACT, out.k_out, out.v_out, S.CALL_DECODE_COMPACT, prob.total_budget)):
+        ws = torch.empty(max(prob.workspace_size(call), 256), dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            S.stlite_decode_attention(prob, cache, q_dec, kk, vv, res, ws, stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            S.stlite_decode_attention(prob, cache, q_dec, kk, vv, res, ws, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        e = roofline_entry({"bound": "hbm", "bytes": units * rows * 128 * 2 * 2.0}, ms)
+        e["rows_per_unit"] = int(rows)
+        entry[name] = e
+    entry["speedup"] = round(entry["full"]["ms"] / entry["compact"]["ms"], 3)
+    log(f"decode attention: full cache {entry['full']['ms']:.3f} ms, compacted {entry['compact']['ms']:.3f} ms, "
+        f"speedup {entry['speedup']:.2f}x")
+    return entry
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,7 +311,7 @@ def main():
     model = work_model(w, lay, cu_budget)
     stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
     dom = max(names, key=lambda n: per_call[n])
-    kernel_of = {"score_window": "score_rowstats_kernel + score_colsum_kernel",
+    kernel_of = {"score_window": "score_pass_kernel<1> + score_pass_kernel<2>",
                  "tsg_rho": "rho_kernel", "tsg_threshold": "gate_keys/segsel/gate_emit kernels",
                  "css_saliency": "css_kernel", "select_topk": "select_keys/segsel/select_emit kernels",
                  "compact_kv": "compact_kernel"}
@@ -313,6 +348,7 @@ def main():
         "roofline": roof,
         "stages": stages,
     }
+    result["decode"] = decode_timing(prob, w, q, dk, dv, out, stream)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host (cpu baseline)")
         result["cpu_baseline"] = cpu_baseline(w, inputs)

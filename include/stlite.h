@@ -14,6 +14,11 @@
  *   stlite_select_topk   S and the retained set I_keep = Top_B(S) (Eq. modal_scoring)
  *   stlite_compact_kv    K' = K[I_keep], V' = V[I_keep]           (the algorithm's result)
  *
+ * and, for the decoding phase that consumes the cache,
+ *
+ *   stlite_decode_attention  softmax(q K^T / sqrt(d)) V over the full or the
+ *                            compacted cache                  (problem setup)
+ *
  * Conventions shared by every call
  * --------------------------------
  * Pointers are DEVICE pointers unless their name starts with h_ (host).  bf16
@@ -82,8 +87,18 @@ typedef enum stlite_call {
   STLITE_CALL_SELECT_TOPK = 3,
   STLITE_CALL_COMPACT_KV = 4,
   STLITE_CALL_TSG_THRESHOLD = 5,
-  STLITE_CALL_TSG_RHO = 6
+  STLITE_CALL_TSG_RHO = 6,
+  STLITE_CALL_DECODE_FULL = 7,    /* stlite_decode_attention on STLITE_CACHE_FULL */
+  STLITE_CALL_DECODE_COMPACT = 8  /* stlite_decode_attention on STLITE_CACHE_COMPACT */
 } stlite_call;
+
+/* Which cache a decode call reads. */
+typedef enum stlite_cache {
+  STLITE_CACHE_FULL = 0,    /* k, v [n_layers][n_kv_heads][total_tokens][d]: sequence s owns
+                               rows cu_seqlens[s] .. cu_seqlens[s+1]-1 */
+  STLITE_CACHE_COMPACT = 1  /* k_out, v_out [n_layers][n_kv_heads][total_budget][d]: sequence s
+                               owns rows cu_budget[s] .. cu_budget[s+1]-1 */
+} stlite_cache;
 
 /*
  * The packed problem: model shape, window and the varlen layout.
@@ -214,6 +229,26 @@ stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base,
 stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
                                 const int32_t* kept, uint16_t* k_out, uint16_t* v_out,
                                 void* stream);
+
+/*
+ * Decode attention over a cache: the decoding phase of the problem setup,
+ * which attends each new query over the cached keys and values -- the full
+ * prefill cache, or the compacted K', V' that stlite_compact_kv writes (the
+ * compression procedure returns them for that phase).  For every layer,
+ * sequence s and query head g (kv head g / G):
+ *   out_g = sum_j softmax_j(q_g . k_j / sqrt(d)) v_j
+ * over all of sequence s's rows of the chosen cache (the decode query follows
+ * every cached token: no mask); a sequence with no rows gets out = 0.
+ *   q_dec  bf16 [n_layers][n_seqs][n_q_heads][d]   one decode query per head
+ *   k, v   bf16, the layout of `cache` (see stlite_cache)
+ *   out    fp32 [n_layers][n_seqs][n_q_heads][d]
+ * bf16 operands, fp32 logits, softmax and accumulation.  Needs G <= 16 and the
+ * workspace of STLITE_CALL_DECODE_FULL / _COMPACT.
+ */
+stlite_status stlite_decode_attention(const stlite_problem* p, stlite_cache cache,
+                                      const uint16_t* q_dec, const uint16_t* k,
+                                      const uint16_t* v, float* out, void* workspace,
+                                      size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

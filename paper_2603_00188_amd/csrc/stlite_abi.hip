@@ -179,6 +179,33 @@ stlite_status check_ws(const stlite_problem* p, stlite_call call, const void* ws
 
 bool aligned16(const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 16 == 0; }
 
+// Decode attention: rows per work-group (aim for >= 2048 work-groups) and the
+// chunk count over all sequences of a cache.
+struct DecodePlan {
+  const int32_t* h_cu_rows;
+  int64_t total_rows;
+  int32_t chunk;
+  int64_t total_chunks;
+};
+
+DecodePlan decode_plan(const stlite_problem* p, bool compact) {
+  DecodePlan d;
+  d.h_cu_rows = compact ? p->h_cu_budget : p->h_cu_seqlens;
+  d.total_rows = compact ? p->total_budget : p->total_tokens;
+  const int64_t units = int64_t(p->n_layers) * p->n_kv_heads;
+  int64_t ch = ceil_div(std::max<int64_t>(units * d.total_rows, 1), 2048);
+  ch = ceil_div(ch, 64) * 64;
+  d.chunk = int32_t(std::min<int64_t>(4096, std::max<int64_t>(256, ch)));
+  d.total_chunks = 0;
+  for (int s = 0; s < p->n_seqs; ++s) d.total_chunks += ceil_div(d.h_cu_rows[s + 1] - d.h_cu_rows[s], d.chunk);
+  return d;
+}
+
+size_t decode_bytes(const stlite_problem* p, const DecodePlan& d) {
+  const size_t parts = size_t(p->n_layers) * p->n_kv_heads * size_t(d.total_chunks) * 16;
+  return 2 * align_up(parts * sizeof(float)) + align_up(parts * kHeadDim * sizeof(float));
+}
+
 }  // namespace
 
 extern "C" {
@@ -296,6 +323,10 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
     case STLITE_CALL_CSS_SALIENCY:
     case STLITE_CALL_COMPACT_KV:
       *bytes = 0;
+      break;
+    case STLITE_CALL_DECODE_FULL:
+    case STLITE_CALL_DECODE_COMPACT:
+      *bytes = decode_bytes(p, decode_plan(p, call == STLITE_CALL_DECODE_COMPACT));
       break;
     default:
       return fail(STLITE_ERR_INVALID_ARG, "unknown call %d", int(call));
@@ -444,6 +475,40 @@ stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, cons
   a.k_out = k_out;
   a.v_out = v_out;
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)), "compact_kv launch");
+}
+
+stlite_status stlite_decode_attention(const stlite_problem* p, stlite_cache cache, const uint16_t* q_dec,
+                                      const uint16_t* k, const uint16_t* v, float* out, void* ws,
+                                      size_t ws_bytes, void* stream) {
+  if (cache != STLITE_CACHE_FULL && cache != STLITE_CACHE_COMPACT)
+    return fail(STLITE_ERR_INVALID_ARG, "cache must be STLITE_CACHE_FULL or STLITE_CACHE_COMPACT");
+  const bool compact = cache == STLITE_CACHE_COMPACT;
+  stlite_status st = check_ws(p, compact ? STLITE_CALL_DECODE_COMPACT : STLITE_CALL_DECODE_FULL, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  const int32_t G = p->n_q_heads / p->n_kv_heads;
+  if (G > 16) return fail(STLITE_ERR_UNSUPPORTED, "decode attention needs G <= 16 (G = %d)", G);
+  const DecodePlan d = decode_plan(p, compact);
+  if (!q_dec || !out || (d.total_rows > 0 && (!k || !v)))
+    return fail(STLITE_ERR_INVALID_ARG, "q_dec, out, k and v must be non-NULL");
+  if (!aligned16(q_dec) || !aligned16(k) || !aligned16(v))
+    return fail(STLITE_ERR_INVALID_ARG, "q_dec, k and v must be 16-byte aligned");
+  DecodeArgs a;
+  a.lay = make_layout(p);
+  a.q = q_dec;
+  a.k = k;
+  a.v = v;
+  a.cu_rows = compact ? p->cu_budget : p->cu_seqlens;
+  a.total_rows = d.total_rows;
+  a.out = out;
+  const size_t parts = size_t(a.lay.n_units) * size_t(d.total_chunks) * 16;
+  a.pm = static_cast<float*>(ws);
+  a.pl = reinterpret_cast<float*>(static_cast<char*>(ws) + align_up(parts * sizeof(float)));
+  a.po = reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * align_up(parts * sizeof(float)));
+  a.n_q_heads = p->n_q_heads;
+  a.group = G;
+  a.chunk = d.chunk;
+  a.total_chunks = int32_t(d.total_chunks);
+  return hip_status(launch_decode(a, static_cast<hipStream_t>(stream)), "decode_attention launch");
 }
 
 }  // extern "C"

@@ -147,7 +147,25 @@ struct CompactArgs {
   uint16_t* v_out;
 };
 
+struct DecodeArgs {
+  Layout lay;
+  const uint16_t* q;       // [layers][seqs][Hq][d]: one decode query per head
+  const uint16_t* k;       // [units][total_rows][d]
+  const uint16_t* v;
+  const int32_t* cu_rows;  // [n_seqs + 1]: the sequences' rows in this cache
+  int64_t total_rows;
+  float* out;              // [layers][seqs][Hq][d]
+  float* pm;               // workspace [units][total_chunks][16]: chunk max (log2 units)
+  float* pl;               // workspace [units][total_chunks][16]: chunk sum
+  float* po;               // workspace [units][total_chunks][16][d]: chunk O, unnormalised
+  int32_t n_q_heads;
+  int32_t group;           // G <= 16
+  int32_t chunk;           // rows per work-group
+  int32_t total_chunks;
+};
+
 hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);

@@ -17,12 +17,14 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstlite.s
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 (CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD,
- CALL_TSG_RHO) = range(7)
+ CALL_TSG_RHO, CALL_DECODE_FULL, CALL_DECODE_COMPACT) = range(9)
+CACHE_FULL, CACHE_COMPACT = 0, 1
 
 EXPORTS = (
     "stlite_abi_version", "stlite_status_string", "stlite_last_error", "stlite_budget",
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
+    "stlite_decode_attention",
 )
 
 
@@ -74,6 +76,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_tsg_threshold": (st, [P, vp, vp, vp, vp, sz, vp]),
         "stlite_select_topk": (st, [P, vp, vp, vp, f32, vp, vp, vp, sz, vp]),
         "stlite_compact_kv": (st, [P, vp, vp, vp, vp, vp, vp]),
+        "stlite_decode_attention": (st, [P, st, vp, vp, vp, vp, vp, sz, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -199,6 +202,25 @@ def stlite_select_topk(p: Problem, a_base, phi, gate, alpha: float, kept, score,
 def stlite_compact_kv(p: Problem, k, v, kept, k_out, v_out, stream=None) -> None:
     _check(load().stlite_compact_kv(p.ref, _ptr(k), _ptr(v), _ptr(kept), _ptr(k_out), _ptr(v_out),
                                     _stream(stream)), "stlite_compact_kv")
+
+
+def stlite_decode_attention(p: Problem, cache: int, q_dec, k, v, out, workspace, stream=None) -> None:
+    _check(load().stlite_decode_attention(p.ref, int(cache), _ptr(q_dec), _ptr(k), _ptr(v), _ptr(out),
+                                          _ptr(workspace), _nbytes(workspace), _stream(stream)),
+           "stlite_decode_attention")
+
+
+def decode(p: Problem, q_dec, k, v, cache: int, out=None, workspace=None, stream=None):
+    """Decode attention over the full (CACHE_FULL: k, v) or compacted
+    (CACHE_COMPACT: k_out, v_out) cache; returns out [layers, seqs, Hq, 128] fp32."""
+    import torch
+    if out is None:
+        out = torch.empty((p.n_layers, p.n_seqs, p.n_q_heads, 128), dtype=torch.float32, device=q_dec.device)
+    if workspace is None:
+        n = p.workspace_size(CALL_DECODE_COMPACT if cache == CACHE_COMPACT else CALL_DECODE_FULL)
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_dec.device)
+    stlite_decode_attention(p, cache, q_dec, k, v, out, workspace, stream)
+    return out
 
 
 class Buffers:

@@ -392,3 +392,11 @@ def make_inputs(w: Workload, layers: Optional[Sequence[int]] = None, workers: in
         for i in range(len(layers)):
             one(i)
     return scene, k, v, q
+
+
+def decode_queries(q: np.ndarray) -> np.ndarray:
+    """Decode queries [layers, seqs, Hq, d] (bf16 bits) for the decoding phase
+    that follows the compression: each head's window query at the last window
+    position, i.e. the query the model formed at the end of prefill, which the
+    first decode step's query resembles."""
+    return np.ascontiguousarray(q[:, :, :, -1, :])

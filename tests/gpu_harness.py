@@ -11,6 +11,10 @@ Tolerances (bf16 inputs, fp32 accumulation in the kernels):
                     B-th score s_B (oracle S recomputed with the GPU gate when
                     a gate flip inside the band occurred)
   K', V'            bit-exact copies of the rows the GPU kept
+  decode out        |d| <= 1e-4 sum_j p_j |v_j| + 1e-7 per element: the logits
+                    are exact bf16 products summed in fp32, softmax and P V run
+                    in fp32 over up to ~1.5e5 rows in chunks, an error of order
+                    1e-6 .. 1e-5 of that scale
 """
 from __future__ import annotations
 
@@ -26,6 +30,7 @@ from paper_2603_00188_amd import workload as W
 A_RTOL = 1e-3
 COS_TOL = 1e-3
 BAND = 1e-4
+DECODE_TOL = 1e-4
 
 
 def log(msg: str):
@@ -144,3 +149,44 @@ def compare_unit(case: Case, res, layer: int, kv: int, s: int, alpha=None, css=T
     assert (res["k_out"][u, cb[s]:cb[s + 1]] == kb).all(), f"{where}: K' not an exact copy"
     assert (res["v_out"][u, cb[s]:cb[s + 1]] == vb).all(), f"{where}: V' not an exact copy"
     return stats
+
+
+def run_decode(case: Case):
+    """Decode attention over the full and the compacted cache of the last run
+    (the decode query of each head: its last window query)."""
+    import torch
+    q_dec = W.decode_queries(case.q)
+    dq = torch.from_numpy(q_dec.view(np.int16)).to(case.dk.device)
+    full = S.decode(case.prob, dq, case.dk, case.dv, S.CACHE_FULL)
+    comp = S.decode(case.prob, dq, case.out.k_out, case.out.v_out, S.CACHE_COMPACT)
+    torch.cuda.synchronize()
+    return q_dec, full.cpu().numpy(), comp.cpu().numpy()
+
+
+def compare_decode(case: Case, res, dec, layer: int, kv: int, s: int):
+    """Both decode outputs of one (layer, kv head, sequence) against the oracle,
+    the compacted one over the rows the GPU kept (their copies are checked
+    bit-exact elsewhere).  Returns the worst error in units of the tolerance."""
+    q_dec, full, comp = dec
+    G = case.w.group
+    heads = slice(kv * G, (kv + 1) * G)
+    Q = O.bf16_to_f64(q_dec[layer, s, heads])
+    a, b = int(case.lay.cu_seqlens[s]), int(case.lay.cu_seqlens[s + 1])
+    u = layer * case.w.n_kv_heads + kv
+    ba, bb = int(case.cu_budget[s]), int(case.cu_budget[s + 1])
+    worst = 0.0
+    for name, got, Kb, Vb in (("full", full, case.k[layer, kv, a:b], case.v[layer, kv, a:b]),
+                              ("compact", comp, res["k_out"][u, ba:bb], res["v_out"][u, ba:bb])):
+        K, V = O.bf16_to_f64(Kb), O.bf16_to_f64(Vb)
+        ref = O.decode_attention(Q, K, V)
+        scale = O.decode_attention(Q, K, np.abs(V))
+        g = got[layer, s, heads].astype(np.float64)
+        lim = DECODE_TOL * scale + 1e-7
+        err = np.abs(g - ref)
+        bad = err > lim
+        if bad.any():
+            i = np.argwhere(bad)[0]
+            raise AssertionError(f"decode {name} unit ({layer},{kv},{s}) head {i[0]} dim {i[1]}: "
+                                 f"got {g[tuple(i)]!r} ref {ref[tuple(i)]!r} tol {lim[tuple(i)]:.3g}")
+        worst = max(worst, float((err / lim).max()) if err.size else 0.0)
+    return worst

@@ -151,3 +151,28 @@ def test_budgets_helper_matches_oracle():
     got = S.budgets(cu, 1, 5)
     want = np.concatenate([[0], np.cumsum([O.budget(int(l), 1, 5) for l in np.diff(cu)])])
     assert got.tolist() == want.tolist()
+
+
+def test_decode_workspace_and_rejections():
+    """Decode attention: workspace per cache, and every malformed call fails
+    before anything is enqueued."""
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    n_full, n_comp = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(ref, S.CALL_DECODE_FULL, ctypes.byref(n_full)) == S.OK
+    assert lib.stlite_workspace_size(ref, S.CALL_DECODE_COMPACT, ctypes.byref(n_comp)) == S.OK
+    assert n_full.value > 0 and n_full.value % 256 == 0 and 0 < n_comp.value <= n_full.value
+    call = lambda cache, q, k, v, out, ws, nb: lib.stlite_decode_attention(ref, cache, q, k, v, out, ws, nb, None)
+    assert call(S.CACHE_FULL, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, None, 0) == S.ERR_WORKSPACE
+    assert call(S.CACHE_FULL, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, n_full.value - 1) == S.ERR_WORKSPACE
+    assert call(2, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, n_full.value) == S.ERR_INVALID_ARG
+    assert call(S.CACHE_FULL, None, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, n_full.value) == S.ERR_INVALID_ARG
+    assert call(S.CACHE_COMPACT, FAKE_DEV, FAKE_DEV + 4, FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                n_comp.value) == S.ERR_INVALID_ARG
+    # more than 16 query heads per kv head
+    wide = HostProblem([0, 72, 102], [[(0, 4, 5), (30, 4, 5)], []], [14, 6], n_q_heads=68, n_kv_heads=4, window=4)
+    nw = ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(ctypes.byref(wide.c), S.CALL_DECODE_FULL, ctypes.byref(nw)) == S.OK
+    assert lib.stlite_decode_attention(ctypes.byref(wide.c), S.CACHE_FULL, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                       FAKE_DEV, nw.value, None) == S.ERR_UNSUPPORTED

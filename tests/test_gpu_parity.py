@@ -249,12 +249,24 @@ def test_config2_sampled(torch_cuda):
 
 @pytest.mark.timeout(900)
 def test_config3_sampled(torch_cuda):
-    _full(3)
+    """The 150,528-token trajectory in the benchmark's launch configuration,
+    and decode attention over its full and compacted caches."""
+    H = _H()
+    case, res = _full(3)
+    dec = H.run_decode(case)
+    for unit in ((0, 0, 0), (13, 2, 0), (27, 3, 0)):
+        H.log(f"config 3 decode unit {unit}: worst error / tolerance {H.compare_decode(case, res, dec, *unit):.3g}")
 
 
 @pytest.mark.timeout(900)
 def test_config4_sampled(torch_cuda):
-    _full(4, samples=((0, 0, 0), (13, 2, 4), (27, 3, 7)))
+    """The ragged batch of 8 trajectories, and decode attention over its caches."""
+    H = _H()
+    samples = ((0, 0, 0), (13, 2, 4), (27, 3, 7))
+    case, res = _full(4, samples=samples)
+    dec = H.run_decode(case)
+    for unit in samples:
+        H.log(f"config 4 decode unit {unit}: worst error / tolerance {H.compare_decode(case, res, dec, *unit):.3g}")
 
 
 def test_logit_spike_takes_exact_pass(torch_cuda):
