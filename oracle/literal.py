@@ -8,7 +8,8 @@ so that a vectorisation slip in the NumPy oracle shows up as a disagreement:
   A_base^(i) = (1/G) sum_g sum_{p in window} exp(z_{g,p,i}) / sum_{j<=p} exp(z_{g,p,j}),
       z = q . k / sqrt(d)                               (Eq. base_attention; readings R1, R2)
   H_{u,v}   = (1/|N|) sum_{n in N(u,v)} cos(h_{u,v}, h_n), Phi = 1 - H   (Eq. css_calc)
-  rho_i     = max_{j in current frame} cos(h_i, h_j)  (Sec. TSG)
+  rho_i     = max_{j in current frame} cos(h_i, h_j)  (Sec. TSG); with k_i . k_j or
+              -||k_i - k_j|| in place of the cosine (similarity-metric ablation; R8b)
   gate      = the m = min(B, |pool|) smallest rho by (rho, index)       (Eqs. budget_threshold,
                                                                         temporal_mask; R7)
   S         = A (text) | M (A + alpha Phi) (visual)  (Eq. modal_scoring)
@@ -167,4 +168,25 @@ def decode_attention(Q, K, V):
             w = e[j] / tot
             for c in range(d):
                 out[g][c] += w * V[j][c]
+    return out
+
+
+def tsg_similarity(K, hist, cur, sim):
+    """rho_i = max over current j of dot(k_i, k_j) or of -sqrt(sum_c (k_ic - k_jc)^2)
+    (the squared distance snapped to 0 when <= 1e-5 ||k_i||^2); cosine as tsg_rho."""
+    out = []
+    for i in hist:
+        best = None
+        for j in cur:
+            if sim == "dot":
+                v = dot(K[i], K[j])
+            else:
+                d2 = 0.0
+                for a, b in zip(K[i], K[j]):
+                    d2 += (a - b) * (a - b)
+                if d2 <= 1e-5 * dot(K[i], K[i]):
+                    d2 = 0.0
+                v = -math.sqrt(d2)
+            best = v if best is None or v > best else best
+        out.append(best)
     return out

@@ -14,8 +14,10 @@ takes them:
   base_score       A_base, window voting of softmax rows      (Eq. base_attention)
   css_saliency     H = mean Moore-neighbour cosine, Phi = 1-H (Eq. css_calc, Sec. CSS)
   tsg_rho          rho_i = max cosine to the current frame    (Sec. TSG)
+  tsg_similarity   the same maximum for dot product or -L2    (similarity ablation)
   tsg_gate         tau_red = min(B,|pool|)-th smallest rho,
                    M_time = 1[rho <= tau_red]                 (Eqs. budget_threshold, temporal_mask)
+  tsg_fixed_gate   M_time = 1[rho <= tau] for a fixed tau     (component-necessity control)
   integrate        S = A (text), M (A + alpha Phi) (visual)   (Eq. modal_scoring)
   select_topk      I_keep = Top_B(S)                          (Sec. integrated scoring)
   compact          K' = K[I_keep], V' = V[I_keep]             (algorithm's return value)
@@ -34,6 +36,8 @@ Readings where the paper is silent (each is also listed in the design notes):
   R7  ties at tau_red: the gate admits exactly m = min(B, |pool|) historical
       tokens, taken in (rho ascending, index ascending) order;
   R8  rho >= 1 - 1e-4 is snapped to exactly 1 (duplicate class);
+  R8b under the negative-L2 similarity, a squared distance <= 1e-5 ||k_i||^2
+      is snapped to 0 (the same duplicate class);
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
   R11 no forced keep of the window; R13 gated-out visual tokens score 0;
   R16 I_keep is emitted in ascending token order;
@@ -58,6 +62,7 @@ from typing import Dict, List, Sequence, Tuple
 import numpy as np
 
 SNAP_EPS = 1e-4          # reading R8
+L2_SNAP = 1e-5           # reading R8b
 DECIDE_DTYPE = np.float32  # reading R-dec
 
 
@@ -198,6 +203,53 @@ def tsg_rho(K: np.ndarray, hist: np.ndarray, cur: np.ndarray, chunk: int = 4096)
         rho[a:a + chunk] = _cos_matrix(K[hist[a:a + chunk]], Kc).max(axis=1)
     rho = np.clip(rho, -1.0, 1.0)
     return np.where(rho >= 1.0 - SNAP_EPS, 1.0, rho)
+
+
+def tsg_similarity(K: np.ndarray, hist: np.ndarray, cur: np.ndarray, sim: str = "cosine",
+                   chunk: int = 4096) -> np.ndarray:
+    """rho_i = max over current-frame j of sim(k_i, k_j), for the similarity
+    functions of the paper's similarity-metric ablation (appendix Similarity
+    Metric Ablation; Sec. TSG for the cosine):
+
+      cosine   cos(k_i, k_j) with the clamp and snap of tsg_rho (R8);
+      dot      k_i . k_j;
+      neg_l2   -||k_i - k_j||, the squared distance snapped to 0 when it is
+               at most L2_SNAP ||k_i||^2 (reading R8b: the duplicate class of
+               the distance, as R8 is for the cosine).
+    """
+    if sim == "cosine":
+        return tsg_rho(K, hist, cur, chunk)
+    rho = np.zeros(len(hist))
+    if len(hist) == 0:
+        return rho
+    if len(cur) == 0:
+        raise ValueError("historical tokens need a current frame")
+    Kc = K[cur]
+    for a in range(0, len(hist), chunk):
+        Kh = K[hist[a:a + chunk]]
+        if sim == "dot":
+            rho[a:a + chunk] = (Kh @ Kc.T).max(axis=1)
+        elif sim == "neg_l2":
+            # ||a - b||^2 = ||a||^2 + ||b||^2 - 2 a.b in float64 (cancellation ~1e-16 of
+            # the norms, far below the snap); the literal twin sums (a - b)^2 directly.
+            n2 = (Kh * Kh).sum(axis=1)
+            d2 = n2[:, None] + (Kc * Kc).sum(axis=1)[None, :] - 2.0 * (Kh @ Kc.T)
+            d2 = np.maximum(d2.min(axis=1), 0.0)
+            d2 = np.where(d2 <= L2_SNAP * n2, 0.0, d2)
+            rho[a:a + chunk] = -np.sqrt(d2)
+        else:
+            raise ValueError(f"unknown similarity {sim!r}")
+    return rho
+
+
+def tsg_fixed_gate(rho: np.ndarray, hist: np.ndarray, L: int, tau: float) -> np.ndarray:
+    """The fixed-threshold control of the paper's Component Necessity Controls:
+    a historical token is gated out when its rho exceeds tau, whatever the
+    distribution (decided on float32 rho, R-dec); text and the current frame
+    get 1."""
+    gate = np.ones(L, dtype=np.uint8)
+    gate[hist] = (rho.astype(DECIDE_DTYPE) <= DECIDE_DTYPE(tau)).astype(np.uint8)
+    return gate
 
 
 def tsg_gate(rho: np.ndarray, hist: np.ndarray, L: int, B: int):

@@ -243,6 +243,88 @@ def test_tsg_rho_brute_force_and_snap():
     assert rho[3] == 1.0 and rho[4] == 1.0
 
 
+
+# ------------------------------------------------ TSG similarity variants ----
+
+def test_tsg_similarity_literal_twin_and_cosine_route():
+    rng = np.random.default_rng(21)
+    K = rng.standard_normal((24, 16)) * rng.uniform(0.2, 3.0, (24, 1))  # mixed magnitudes
+    K[2] = K[20]                                # exact duplicate of a current-frame key
+    K[5] = K[21] + 1e-4 * rng.standard_normal(16)   # d^2 ~ 1.6e-7, well inside the snap
+    hist, cur = np.arange(0, 16), np.arange(16, 24)
+    for sim in ("dot", "neg_l2"):
+        got = O.tsg_similarity(K, hist, cur, sim)
+        want = O1.tsg_similarity(K.tolist(), hist.tolist(), cur.tolist(), sim)
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(O.tsg_similarity(K, hist, cur, "cosine"), O.tsg_rho(K, hist, cur))
+    nl2 = O.tsg_similarity(K, hist, cur, "neg_l2")
+    assert nl2[2] == 0.0 and nl2[5] == 0.0 and (nl2 <= 0).all()
+    # the dot product is not magnitude invariant: a longer current key can beat the duplicate
+    dot = O.tsg_similarity(K, hist, cur, "dot")
+    assert dot[2] >= K[20] @ K[20]
+    assert dot[2] == pytest.approx(max(K[20] @ K[j] for j in cur), rel=1e-15)
+    with pytest.raises(ValueError):
+        O.tsg_similarity(K, hist, cur, "manhattan")
+    assert O.tsg_similarity(K, hist[:0], cur, "dot").shape == (0,)
+
+
+def test_tsg_similarity_closed_forms():
+    """Orthonormal keys: dot = 0 and -L2 = -sqrt(2) between distinct axes; k_i = c e_j
+    gives dot = c and -L2 = -|c - 1|.  On unit-norm keys the three metrics order
+    tokens alike: dot = cos and -L2 = -sqrt(2 - 2 cos)."""
+    E = np.eye(8)
+    K = np.vstack([E[4], E[5], 3.0 * E[0], 0.5 * E[1], E[0], E[1]])
+    hist, cur = np.arange(0, 4), np.arange(4, 6)
+    np.testing.assert_allclose(O.tsg_similarity(K, hist, cur, "dot"), [0, 0, 3.0, 0.5], atol=0)
+    np.testing.assert_allclose(O.tsg_similarity(K, hist, cur, "neg_l2"),
+                               [-math.sqrt(2), -math.sqrt(2), -2.0, -0.5], rtol=1e-15)
+    rng = np.random.default_rng(22)
+    U = rng.standard_normal((40, 32))
+    U /= np.linalg.norm(U, axis=1, keepdims=True)
+    hist, cur = np.arange(0, 30), np.arange(30, 40)
+    cosr = O.tsg_rho(U, hist, cur)
+    assert (cosr < 1 - 1e-4).all()
+    np.testing.assert_allclose(O.tsg_similarity(U, hist, cur, "dot"), cosr, atol=1e-14)
+    np.testing.assert_allclose(O.tsg_similarity(U, hist, cur, "neg_l2"),
+                               -np.sqrt(2 - 2 * cosr), atol=1e-12)
+
+
+def test_tsg_similarity_scale_behaviour_and_l2_snap_edge():
+    """Dot scales with c^2 and -L2 with |c| when all keys are scaled by c; the cosine
+    is scale free.  The negative-L2 snap fires at d^2 <= 1e-5 ||k_i||^2 exactly."""
+    rng = np.random.default_rng(23)
+    K = rng.standard_normal((20, 16))
+    hist, cur = np.arange(0, 12), np.arange(12, 20)
+    c = 2.0 ** 3
+    np.testing.assert_allclose(O.tsg_similarity(c * K, hist, cur, "dot"),
+                               c * c * O.tsg_similarity(K, hist, cur, "dot"), rtol=1e-14)
+    np.testing.assert_allclose(O.tsg_similarity(c * K, hist, cur, "neg_l2"),
+                               c * O.tsg_similarity(K, hist, cur, "neg_l2"), rtol=1e-12)
+    np.testing.assert_allclose(O.tsg_rho(c * K, hist, cur), O.tsg_rho(K, hist, cur), atol=1e-14)
+    # k_i = (1, 0, ...), current key (1, t, 0, ...): d^2 = t^2, ||k_i||^2 = 1
+    for t, snapped in ((math.sqrt(0.9e-5), True), (math.sqrt(1.1e-5), False)):
+        K2 = np.zeros((2, 4))
+        K2[0, 0] = 1.0
+        K2[1, 0], K2[1, 1] = 1.0, t
+        r = O.tsg_similarity(K2, np.array([0]), np.array([1]), "neg_l2")[0]
+        assert (r == 0.0) if snapped else r == pytest.approx(-t, rel=1e-9)
+
+
+def test_tsg_fixed_gate_hand_example():
+    """tau = 0.85, the fixed-threshold control of the necessity table: a historical
+    token is kept iff float32(rho) <= float32(0.85); text and current frame keep 1."""
+    L = 9
+    hist = np.array([0, 1, 2, 3, 5, 6])
+    rho = np.array([0.2, 0.85, 0.8500001, 1.0, 0.85 + 1e-12, -0.3])
+    gate = O.tsg_fixed_gate(rho, hist, L, 0.85)
+    # 0.85 + 1e-12 rounds to float32(0.85) and is kept (decided in float32, R-dec);
+    # 0.8500001 is a distinct float32 above it and is dropped.
+    assert gate.tolist() == [1, 1, 0, 0, 1, 1, 1, 1, 1]
+    assert O.tsg_fixed_gate(rho, hist, L, 1.0).tolist() == [1] * L
+    assert O.tsg_fixed_gate(rho, hist, L, -1.0).tolist() == [0, 0, 0, 0, 1, 0, 0, 1, 1]
+    assert O.tsg_fixed_gate(rho[:0], hist[:0], 4, 0.5).tolist() == [1] * 4
+
+
 def _frames_seq(rng, n_frames, rows, cols, text, dup_of_last=None):
     """Build a small sequence (keys fp32-representable as bf16) with frames+text."""
     d = 128
