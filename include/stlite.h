@@ -100,6 +100,13 @@ typedef enum stlite_cache {
                                owns rows cu_budget[s] .. cu_budget[s+1]-1 */
 } stlite_cache;
 
+/* Similarity of the TSG frame-similarity maximum (stlite_tsg_similarity). */
+typedef enum stlite_similarity {
+  STLITE_SIM_COSINE = 0,  /* cos(k_i, k_j): the method's choice (Sec. TSG) */
+  STLITE_SIM_DOT = 1,     /* k_i . k_j                  (similarity-metric ablation) */
+  STLITE_SIM_NEG_L2 = 2   /* -||k_i - k_j||             (similarity-metric ablation) */
+} stlite_similarity;
+
 /*
  * The packed problem: model shape, window and the varlen layout.
  *
@@ -197,6 +204,37 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
  */
 stlite_status stlite_tsg_rho(const stlite_problem* p, const uint16_t* k, float* rho,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * rho under another similarity, for the paper's similarity-metric ablation
+ * (appendix Similarity Metric Ablation): rho_i = max over the current frame j of
+ *   STLITE_SIM_COSINE  cos(k_i, k_j) with the clamp and snap above (the same
+ *                      result as stlite_tsg_rho);
+ *   STLITE_SIM_DOT     k_i . k_j, unclamped;
+ *   STLITE_SIM_NEG_L2  -||k_i - k_j||, the squared distance snapped to 0 when it
+ *                      is at most 1e-5 ||k_i||^2 (the duplicate class, as the
+ *                      cosine snap is for the cosine).
+ * bf16 operands, fp32 accumulation; -||k_i - k_j||^2 is formed as
+ * 2 k_i.k_j - ||k_j||^2 - ||k_i||^2, so its absolute error scales with the
+ * squared norms.  Writes rho [units][total_tokens] (0 off the history); needs
+ * the workspace of STLITE_CALL_TSG_RHO.  An unknown `sim` is
+ * STLITE_ERR_INVALID_ARG.  Feed the result to stlite_tsg_threshold for the
+ * adaptive gate.
+ */
+stlite_status stlite_tsg_similarity(const stlite_problem* p, stlite_similarity sim,
+                                    const uint16_t* k, float* rho, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/*
+ * The fixed-threshold gate of the paper's component-necessity controls
+ * (appendix Component Necessity Controls), in place of the adaptive percentile
+ * threshold: gate_i = 1[float32 rho_i <= tau] on historical tokens (rho as
+ * written by stlite_tsg_rho or stlite_tsg_similarity; a NaN rho gates 0),
+ * gate = 1 on text and the current frame.  tau must not be NaN.  Writes gate
+ * [units][total_tokens]; needs no workspace.
+ */
+stlite_status stlite_tsg_fixed_gate(const stlite_problem* p, const float* rho, float tau,
+                                    uint8_t* gate, void* stream);
 
 /*
  * The threshold-and-gate half of stlite_tsg_gate on a caller-supplied rho

@@ -137,6 +137,7 @@ RhoArgs rho_args(const stlite_problem* p, const Facts& f, const uint16_t* k, flo
                  const GateArgs& g) {
   RhoArgs r;
   r.lay = g.lay;
+  r.sim = kSimCosine;
   r.k = k;
   r.rn_cur = rn_cur;
   r.rho = rho;
@@ -402,6 +403,13 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
 
 stlite_status stlite_tsg_rho(const stlite_problem* p, const uint16_t* k, float* rho, void* ws, size_t ws_bytes,
                              void* stream) {
+  return stlite_tsg_similarity(p, STLITE_SIM_COSINE, k, rho, ws, ws_bytes, stream);
+}
+
+stlite_status stlite_tsg_similarity(const stlite_problem* p, stlite_similarity sim, const uint16_t* k, float* rho,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  if (sim != STLITE_SIM_COSINE && sim != STLITE_SIM_DOT && sim != STLITE_SIM_NEG_L2)
+    return fail(STLITE_ERR_INVALID_ARG, "sim must be STLITE_SIM_COSINE, _DOT or _NEG_L2");
   stlite_status st = check_ws(p, STLITE_CALL_TSG_RHO, ws, ws_bytes);
   if (st != STLITE_OK) return st;
   if (!k || !rho) return fail(STLITE_ERR_INVALID_ARG, "k and rho must be non-NULL");
@@ -415,8 +423,23 @@ stlite_status stlite_tsg_rho(const stlite_problem* p, const uint16_t* k, float* 
   g.rho_zero_fill = rho;
   g.gate = nullptr;
   gate_carve(p, f, w + slab, false, g);
-  const RhoArgs r = rho_args(p, f, k, rho, reinterpret_cast<float*>(w), g);
+  RhoArgs r = rho_args(p, f, k, rho, reinterpret_cast<float*>(w), g);
+  r.sim = int32_t(sim);
   return hip_status(launch_tsg_rho(r, g, static_cast<hipStream_t>(stream)), "tsg_rho launch");
+}
+
+stlite_status stlite_tsg_fixed_gate(const stlite_problem* p, const float* rho, float tau, uint8_t* gate,
+                                    void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (!rho || !gate) return fail(STLITE_ERR_INVALID_ARG, "rho and gate must be non-NULL");
+  if (std::isnan(tau)) return fail(STLITE_ERR_INVALID_ARG, "tau must not be NaN");
+  GateArgs g{};
+  g.lay = make_layout(p);
+  g.rho = rho;
+  g.rho_zero_fill = nullptr;
+  g.gate = gate;
+  return hip_status(launch_tsg_fixed_gate(g, tau, static_cast<hipStream_t>(stream)), "tsg_fixed_gate launch");
 }
 
 stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, float* tau, uint8_t* gate,

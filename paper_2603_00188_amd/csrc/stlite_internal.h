@@ -97,10 +97,14 @@ struct HistBlock {
   int32_t seq, hb, n_hist, hist_base;
 };
 
+// Similarity of the frame-similarity maximum (values of stlite_similarity).
+enum Sim : int32_t { kSimCosine = 0, kSimDot = 1, kSimNegL2 = 2 };
+
 struct RhoArgs {
   Layout lay;
+  int32_t sim;           // Sim
   const uint16_t* k;
-  float* rn_cur;         // workspace [units][L]: inverse norms of current-frame keys
+  float* rn_cur;         // workspace [units][L], per current-frame key: 1/||k|| (cosine, dot) or -||k||^2 (-L2)
   float* rho;            // [units][L]; written on historical tokens
   int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
   HistBlock* blocks;     // workspace [total_hist_blocks]
@@ -169,6 +173,8 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
+// gate = 1[float32(rho) <= tau] on historical tokens, 1 elsewhere (g.gate, g.rho, g.lay).
+hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream);
 hipError_t launch_css(const CssArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);

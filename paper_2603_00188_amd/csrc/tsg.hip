@@ -10,6 +10,16 @@
 // the current frame streamed through LDS in 64-key tiles (B operand).  The
 // epilogue never stores the logits: each lane scales its column by the key's
 // inverse norm and keeps a running row max; 16-lane butterflies finish the max.
+//
+// The similarity-metric ablation swaps the cosine for the dot product (the
+// running max of the raw products) or the negative L2 distance: since
+// -||a - b||^2 = 2 a.b - ||b||^2 - ||a||^2, the running max of 2 a.b - ||b||^2
+// (one fma per product, as the cosine's one multiply) gives the smallest
+// distance, and rho = -sqrt(max(||a||^2 - max, 0)), snapped to 0 when the
+// squared distance is at most 1e-5 ||a||^2.
+//
+// The fixed-threshold control of the component-necessity study replaces the
+// rank gate with gate = 1[rho <= tau] for a fixed tau.
 #include <algorithm>
 
 #include "segsel.h"
@@ -21,6 +31,7 @@ namespace {
 
 
 constexpr float kSnap = 1.0f - 1.0e-4f;
+constexpr float kL2Snap = 1.0e-5f;
 
 __device__ inline int32_t frame_size(const Layout& lay, int32_t f) {
   return lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
@@ -106,9 +117,11 @@ __device__ inline float sumsq8(uint4 v) {
   return s;
 }
 
-// Inverse norms of the current-frame keys: rn[unit][token] = 1/||k|| (0 for a
-// zero key).  Work-group (x, seq, unit) covers keys 64 x .. 64 x + 63 of the
-// sequence's current frame, 16 lanes per key.
+// Column factors of the current-frame keys: rn[unit][token] = 1/||k|| (0 for a
+// zero key), or -||k||^2 under the negative L2 distance.  Work-group
+// (x, seq, unit) covers keys 64 x .. 64 x + 63 of the sequence's current
+// frame, 16 lanes per key.
+template <int SIM>
 __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
   const int s = blockIdx.y, unit = blockIdx.z;
   const Layout& lay = a.lay;
@@ -124,7 +137,7 @@ __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
     float ss = sumsq8(v);
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
-    if (gl == 0) rn[off + j] = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+    if (gl == 0) rn[off + j] = SIM == kSimNegL2 ? -ss : (ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f);
   }
 }
 
@@ -135,6 +148,7 @@ __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
 // frame's last key, which leaves every row max unchanged and needs no mask.
 // The three stages are distinct LDS arrays and the loop is unrolled by three,
 // so that every tile read has a compile-time LDS address.
+template <int SIM>
 __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
   __shared__ __attribute__((aligned(16))) float rn0[kTileKeys], rn1[kTileKeys], rn2[kTileKeys];
@@ -198,7 +212,8 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
     x += __shfl_xor(x, 32);
     if (lane < 16) {
       tok_s[wave * 64 + b * 16 + lane] = tok[b];
-      rnrow_s[wave * 64 + b * 16 + lane] = x > 0.0f ? 1.0f / sqrtf(x) : 0.0f;
+      // cosine: 1/||a||; -L2: ||a||^2; unused by the dot product
+      rnrow_s[wave * 64 + b * 16 + lane] = SIM == kSimNegL2 ? x : (x > 0.0f ? 1.0f / sqrtf(x) : 0.0f);
     }
   }
 
@@ -237,12 +252,18 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
           acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[b][kk], kb[g % 3][t], acc[b][t], 0, 0, 0);
     }
   };
+  auto column = [&](float x, float rn) {
+    if constexpr (SIM == kSimCosine) return x * rn;
+    else if constexpr (SIM == kSimDot) return x;
+    else return fmaf(x, 2.0f, rn);
+  };
   auto max_half = [&](const f32x4_t (&acc)[4][2], float rn0, float rn1) {
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        runmax[b][i] = __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], acc[b][0][i] * rn0), acc[b][1][i] * rn1);
+        runmax[b][i] =
+            __builtin_fmaxf(__builtin_fmaxf(runmax[b][i], column(acc[b][0][i], rn0)), column(acc[b][1][i], rn1));
   };
   // Per half: B fragments read under the MFMAs of earlier k-steps, 3 VALU
   // (scale and max of the other half) per 2 MFMAs.
@@ -309,8 +330,18 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
         const int r = wave * 64 + b * 16 + (lane >> 4) * 4 + i;
         const int32_t t = tok_s[r];
         if (t >= 0) {
-          float x = fminf(fmaxf(mx * rnrow_s[r], -1.0f), 1.0f);
-          if (x >= kSnap) x = 1.0f;
+          float x;
+          if constexpr (SIM == kSimCosine) {
+            x = fminf(fmaxf(mx * rnrow_s[r], -1.0f), 1.0f);
+            if (x >= kSnap) x = 1.0f;
+          } else if constexpr (SIM == kSimDot) {
+            x = mx;
+          } else {
+            const float n = rnrow_s[r];
+            float d2 = fmaxf(n - mx, 0.0f);
+            if (d2 <= kL2Snap * n) d2 = 0.0f;
+            x = -sqrtf(d2);
+          }
           rho[t] = x + 0.0f;
         }
       }
@@ -360,6 +391,22 @@ __global__ __launch_bounds__(kSegThreads) void gate_emit_kernel(GateArgs a) {
     if (i0 + i < cr.end) gate[htok[i0 + i]] = tc.take[i] ? 1 : 0;
 }
 
+// Fixed-threshold gate of frame blockIdx.x in unit blockIdx.y: every token of a
+// historical frame gets 1[rho <= tau]; the current frame keeps the 1 of the fill.
+__global__ __launch_bounds__(256) void fixed_gate_kernel(GateArgs a, float tau) {
+  const Layout& lay = a.lay;
+  const int32_t f = blockIdx.x;
+  int32_t lo = 0, hi = lay.n_seqs - 1;
+  while (lo < hi) {  // the sequence whose frames f lies in
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (lay.cu_frames[mid] <= f) lo = mid; else hi = mid - 1;
+  }
+  if (f == lay.cu_frames[lo + 1] - 1) return;  // current frame
+  const size_t base = size_t(blockIdx.y) * lay.total_tokens;
+  const int32_t off = lay.frame_meta[3 * f], n = frame_size(lay, f);
+  for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.gate[base + off + j] = a.rho[base + off + j] <= tau ? 1 : 0;
+}
+
 hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
   hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs + g.lay.n_frames), dim3(256), 0, stream, g);
   hipError_t e = hipGetLastError();
@@ -398,11 +445,33 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) {
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
   hipError_t e = launch_gate_prologue(g, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(cur_norms_kernel, dim3((std::max(r.max_cur, 1) + 63) / 64, r.lay.n_seqs, r.lay.n_units), dim3(256),
-                     0, stream, r);
-  e = hipGetLastError();
-  if (e != hipSuccess || r.total_hist_blocks == 0) return e;
-  hipLaunchKernelGGL(rho_kernel, dim3(r.total_hist_blocks, r.lay.n_units), dim3(256), 0, stream, r);
+  const dim3 norm_grid((std::max(r.max_cur, 1) + 63) / 64, r.lay.n_seqs, r.lay.n_units);
+  const dim3 rho_grid(r.total_hist_blocks, r.lay.n_units);
+  switch (r.sim) {
+    case kSimCosine:
+      hipLaunchKernelGGL(cur_norms_kernel<kSimCosine>, norm_grid, dim3(256), 0, stream, r);
+      if (r.total_hist_blocks > 0) hipLaunchKernelGGL(rho_kernel<kSimCosine>, rho_grid, dim3(256), 0, stream, r);
+      break;
+    case kSimDot:  // the dot product needs no column factors
+      if (r.total_hist_blocks > 0) hipLaunchKernelGGL(rho_kernel<kSimDot>, rho_grid, dim3(256), 0, stream, r);
+      break;
+    case kSimNegL2:
+      hipLaunchKernelGGL(cur_norms_kernel<kSimNegL2>, norm_grid, dim3(256), 0, stream, r);
+      if (r.total_hist_blocks > 0) hipLaunchKernelGGL(rho_kernel<kSimNegL2>, rho_grid, dim3(256), 0, stream, r);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream) {
+  const size_t n = size_t(g.lay.n_units) * g.lay.total_tokens;
+  const unsigned blocks = unsigned(std::min<size_t>((n / 4 + 255) / 256 + 1, 8192));
+  hipLaunchKernelGGL(gate_fill_kernel, dim3(blocks), dim3(256), 0, stream, g, n);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.lay.n_frames == 0 || g.lay.n_units == 0) return e;
+  hipLaunchKernelGGL(fixed_gate_kernel, dim3(g.lay.n_frames, g.lay.n_units), dim3(256), 0, stream, g, tau);
   return hipGetLastError();
 }
 

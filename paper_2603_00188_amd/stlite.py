@@ -19,12 +19,13 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 (CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD,
  CALL_TSG_RHO, CALL_DECODE_FULL, CALL_DECODE_COMPACT) = range(9)
 CACHE_FULL, CACHE_COMPACT = 0, 1
+SIM_COSINE, SIM_DOT, SIM_NEG_L2 = 0, 1, 2
 
 EXPORTS = (
     "stlite_abi_version", "stlite_status_string", "stlite_last_error", "stlite_budget",
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
-    "stlite_decode_attention",
+    "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
 )
 
 
@@ -77,6 +78,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_select_topk": (st, [P, vp, vp, vp, f32, vp, vp, vp, sz, vp]),
         "stlite_compact_kv": (st, [P, vp, vp, vp, vp, vp, vp]),
         "stlite_decode_attention": (st, [P, st, vp, vp, vp, vp, vp, sz, vp]),
+        "stlite_tsg_similarity": (st, [P, st, vp, vp, vp, sz, vp]),
+        "stlite_tsg_fixed_gate": (st, [P, vp, f32, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -185,6 +188,16 @@ def stlite_tsg_gate(p: Problem, k, rho, tau, gate, workspace, stream=None) -> No
 def stlite_tsg_rho(p: Problem, k, rho, workspace, stream=None) -> None:
     _check(load().stlite_tsg_rho(p.ref, _ptr(k), _ptr(rho), _ptr(workspace), _nbytes(workspace), _stream(stream)),
            "stlite_tsg_rho")
+
+
+def stlite_tsg_similarity(p: Problem, sim: int, k, rho, workspace, stream=None) -> None:
+    _check(load().stlite_tsg_similarity(p.ref, int(sim), _ptr(k), _ptr(rho), _ptr(workspace), _nbytes(workspace),
+                                        _stream(stream)), "stlite_tsg_similarity")
+
+
+def stlite_tsg_fixed_gate(p: Problem, rho, tau: float, gate, stream=None) -> None:
+    _check(load().stlite_tsg_fixed_gate(p.ref, _ptr(rho), float(tau), _ptr(gate), _stream(stream)),
+           "stlite_tsg_fixed_gate")
 
 
 def stlite_tsg_threshold(p: Problem, rho, tau, gate, workspace, stream=None) -> None:

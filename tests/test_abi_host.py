@@ -176,3 +176,28 @@ def test_decode_workspace_and_rejections():
     assert lib.stlite_workspace_size(ctypes.byref(wide.c), S.CALL_DECODE_FULL, ctypes.byref(nw)) == S.OK
     assert lib.stlite_decode_attention(ctypes.byref(wide.c), S.CACHE_FULL, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
                                        FAKE_DEV, nw.value, None) == S.ERR_UNSUPPORTED
+
+
+def test_tsg_variant_rejections():
+    """The similarity and fixed-threshold gate entry points reject malformed
+    calls before anything is enqueued."""
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    n = ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(ref, S.CALL_TSG_RHO, ctypes.byref(n)) == S.OK
+    sim = lambda s, k, rho, ws, nb: lib.stlite_tsg_similarity(ref, s, k, rho, ws, nb, None)
+    assert sim(3, FAKE_DEV, FAKE_DEV, FAKE_DEV, n.value) == S.ERR_INVALID_ARG
+    assert sim(-1, FAKE_DEV, FAKE_DEV, FAKE_DEV, n.value) == S.ERR_INVALID_ARG
+    assert sim(S.SIM_DOT, FAKE_DEV, FAKE_DEV, FAKE_DEV, n.value - 1) == S.ERR_WORKSPACE
+    assert sim(S.SIM_NEG_L2, None, FAKE_DEV, FAKE_DEV, n.value) == S.ERR_INVALID_ARG
+    assert sim(S.SIM_NEG_L2, FAKE_DEV, None, FAKE_DEV, n.value) == S.ERR_INVALID_ARG
+    assert sim(S.SIM_DOT, FAKE_DEV + 2, FAKE_DEV, FAKE_DEV, n.value) == S.ERR_INVALID_ARG
+    fixed = lambda rho, tau, gate: lib.stlite_tsg_fixed_gate(ref, rho, tau, gate, None)
+    assert fixed(None, 0.85, FAKE_DEV) == S.ERR_INVALID_ARG
+    assert fixed(FAKE_DEV, 0.85, None) == S.ERR_INVALID_ARG
+    assert fixed(FAKE_DEV, float("nan"), FAKE_DEV) == S.ERR_INVALID_ARG
+    assert b"NaN" in lib.stlite_last_error()
+    bad = good()
+    bad.c.n_layers = 0
+    assert lib.stlite_tsg_fixed_gate(ctypes.byref(bad.c), FAKE_DEV, 0.85, FAKE_DEV, None) != S.OK
