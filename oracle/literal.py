@@ -7,7 +7,8 @@ so that a vectorisation slip in the NumPy oracle shows up as a disagreement:
 
   A_base^(i) = (1/G) sum_g sum_{p in window} exp(z_{g,p,i}) / sum_{j<=p} exp(z_{g,p,j}),
       z = q . k / sqrt(d)                               (Eq. base_attention; readings R1, R2)
-  H_{u,v}   = (1/|N|) sum_{n in N(u,v)} cos(h_{u,v}, h_n), Phi = 1 - H   (Eq. css_calc)
+  H_{u,v}   = (1/|N|) sum_{n in N(u,v)} cos(h_{u,v}, h_n), Phi = 1 - H   (Eq. css_calc;
+              N the in-grid cells of the k x k square around (u, v), k = 3 by default)
   rho_i     = max_{j in current frame} cos(h_i, h_j)  (Sec. TSG); with k_i . k_j or
               -||k_i - k_j|| in place of the cosine (similarity-metric ablation; R8b)
   gate      = the m = min(B, |pool|) smallest rho by (rho, index)       (Eqs. budget_threshold,
@@ -70,17 +71,18 @@ def base_score(Q, K):
     return [a / G for a in A]
 
 
-def css(K, frames):
+def css(K, frames, k=3):
     L = len(K)
     phi = [0.0] * L
+    r = k // 2
     for off, rows, cols in frames:
         for u in range(rows):
             for v in range(cols):
                 centre = K[off + u * cols + v]
                 total = 0.0
                 count = 0
-                for du in (-1, 0, 1):
-                    for dv in (-1, 0, 1):
+                for du in range(-r, r + 1):
+                    for dv in range(-r, r + 1):
                         if du == 0 and dv == 0:
                             continue
                         uu, vv = u + du, v + dv

@@ -12,7 +12,8 @@ takes them:
 
   budget           B = floor(beta * L)                      (problem setup)
   base_score       A_base, window voting of softmax rows      (Eq. base_attention)
-  css_saliency     H = mean Moore-neighbour cosine, Phi = 1-H (Eq. css_calc, Sec. CSS)
+  css_saliency     H = mean Moore-neighbour cosine, Phi = 1-H (Eq. css_calc, Sec. CSS);
+                   k x k neighbourhoods for the neighbourhood-size ablation
   tsg_rho          rho_i = max cosine to the current frame    (Sec. TSG)
   tsg_similarity   the same maximum for dot product or -L2    (similarity ablation)
   tsg_gate         tau_red = min(B,|pool|)-th smallest rho,
@@ -36,6 +37,8 @@ Readings where the paper is silent (each is also listed in the design notes):
   R7  ties at tau_red: the gate admits exactly m = min(B, |pool|) historical
       tokens, taken in (rho ascending, index ascending) order;
   R8  rho >= 1 - 1e-4 is snapped to exactly 1 (duplicate class);
+  R5b a k x k neighbourhood (k = 5, 7, 9) keeps R5's rule: its in-grid cells
+      other than the centre, equally weighted;
   R8b under the negative-L2 similarity, a squared distance <= 1e-5 ||k_i||^2
       is snapped to 0 (the same duplicate class);
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
@@ -141,15 +144,26 @@ def _cos_rows(X: np.ndarray, Y: np.ndarray) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 MOORE = [(-1, -1), (-1, 0), (-1, 1), (0, -1), (0, 1), (1, -1), (1, 0), (1, 1)]
+CSS_SIZES = (3, 5, 7, 9)   # the neighbourhood sizes of the CSS neighbourhood-size ablation
 
 
-def css_frame(X: np.ndarray, rows: int, cols: int) -> np.ndarray:
+def neighbourhood(k: int):
+    """Offsets (du, dv) of a k x k neighbourhood without its centre; k = 3 is the
+    Moore neighbourhood of Eq. css_calc, k = 5, 7, 9 the ablation's wider ones
+    (reading R5b: the same in-grid rule at every size)."""
+    if k not in CSS_SIZES:
+        raise ValueError(f"neighbourhood size {k} not in {CSS_SIZES}")
+    r = k // 2
+    return [(du, dv) for du in range(-r, r + 1) for dv in range(-r, r + 1) if (du, dv) != (0, 0)]
+
+
+def css_frame(X: np.ndarray, rows: int, cols: int, k: int = 3) -> np.ndarray:
     """Phi for one frame.  X: [rows*cols, d] keys in row-major grid order."""
     d = X.shape[1]
     grid = X.reshape(rows, cols, d)
     acc = np.zeros((rows, cols))
     cnt = np.zeros((rows, cols))
-    for du, dv in MOORE:
+    for du, dv in neighbourhood(k):
         # centre cells whose neighbour (u+du, v+dv) is inside the grid (R5)
         u0, u1 = max(0, -du), min(rows, rows - du)
         v0, v1 = max(0, -dv), min(cols, cols - dv)
@@ -163,11 +177,12 @@ def css_frame(X: np.ndarray, rows: int, cols: int) -> np.ndarray:
     return (1.0 - H).reshape(-1)
 
 
-def css_saliency(K: np.ndarray, frames: Sequence[Tuple[int, int, int]]) -> np.ndarray:
-    """Phi_space over one sequence (0 on text tokens).  frames: local (offset, rows, cols)."""
+def css_saliency(K: np.ndarray, frames: Sequence[Tuple[int, int, int]], k: int = 3) -> np.ndarray:
+    """Phi_space over one sequence (0 on text tokens).  frames: local (offset, rows, cols);
+    k: neighbourhood size (3 = Eq. css_calc; 5, 7, 9 = the neighbourhood-size ablation)."""
     phi = np.zeros(K.shape[0])
     for off, r, c in frames:
-        phi[off:off + r * c] = css_frame(K[off:off + r * c], r, c)
+        phi[off:off + r * c] = css_frame(K[off:off + r * c], r, c, k)
     return phi
 
 

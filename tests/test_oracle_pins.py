@@ -244,6 +244,88 @@ def test_tsg_rho_brute_force_and_snap():
 
 
 
+
+# ------------------------------------------- CSS neighbourhood-size ablation ----
+
+def _span(x, n, r):
+    """(length, position of x) of the in-grid window [x - r, x + r] of a size-n axis."""
+    lo, hi = max(0, x - r), min(n - 1, x + r)
+    return hi - lo + 1, x - lo
+
+
+@pytest.mark.parametrize("k", [5, 7, 9])
+def test_css_wide_literal_twin(k):
+    rng = np.random.default_rng(30 + k)
+    frames = [(0, 1, 1), (1, 2, 3), (7, 6, 7), (49, 10, 4), (89, 3, 11)]
+    K = rng.standard_normal((89 + 33 + 5, 8))
+    K[3] = 0.0                       # a zero key: its cosines are 0 (R6)
+    got = O.css_saliency(K, frames, k)
+    want = O1.css(K.tolist(), frames, k)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+    assert got[0] == 0.0 and (got[-5:] == 0).all()   # 1x1 frame and text
+
+
+@pytest.mark.parametrize("k", [5, 7, 9])
+def test_css_wide_spike_closed_form(k):
+    """A grid of e2 with one cell e1: that cell has Phi = 1; a cell whose k x k
+    window holds it has Phi = 1/n (n = its in-grid neighbour count: one
+    orthogonal neighbour among n); every other cell has Phi = 0."""
+    rows, cols, u0, v0, r = 9, 13, 3, 9, k // 2
+    K = np.tile(np.eye(4)[1], (rows * cols, 1))
+    K[u0 * cols + v0] = np.eye(4)[0]
+    phi = O.css_frame(K, rows, cols, k).reshape(rows, cols)
+    for u in range(rows):
+        for v in range(cols):
+            n = _span(u, rows, r)[0] * _span(v, cols, r)[0] - 1
+            if (u, v) == (u0, v0):
+                want = 1.0
+            elif abs(u - u0) <= r and abs(v - v0) <= r:
+                want = 1.0 / n
+            else:
+                want = 0.0
+            assert phi[u, v] == pytest.approx(want, abs=1e-15), (u, v)
+
+
+@pytest.mark.parametrize("k", [3, 5, 7, 9])
+def test_css_wide_checkerboard_closed_form(k):
+    """+-e1 checkerboard: cos = +1 with cells of the centre's parity, -1 with the
+    others.  Over an a x b window with the centre at (i, j), the cells of parity
+    p number ceil(a/2) ceil(b/2) + floor(a/2) floor(b/2) for p = 0, so
+    Phi = 1 - (same - opp) / (a b - 1) with same = (count of the centre's parity) - 1."""
+    rows, cols, r = 7, 10, k // 2
+    sign = np.array([[1.0 if (u + v) % 2 == 0 else -1.0 for v in range(cols)] for u in range(rows)])
+    K = sign.reshape(-1, 1) * np.eye(3)[0]
+    phi = O.css_frame(K, rows, cols, k).reshape(rows, cols)
+    for u in range(rows):
+        for v in range(cols):
+            (a, i), (b, j) = _span(u, rows, r), _span(v, cols, r)
+            even = -(-a // 2) * -(-b // 2) + (a // 2) * (b // 2)
+            same = (even if (i + j) % 2 == 0 else a * b - even) - 1
+            opp = a * b - 1 - same
+            assert phi[u, v] == pytest.approx(1 - (same - opp) / (a * b - 1), abs=1e-14), (k, u, v)
+
+
+def test_css_wide_whole_grid_and_defaults():
+    """k at least twice the grid's extent: every cell averages its cosines with
+    all other cells (full Gram matrix less the diagonal); a uniform frame has
+    Phi = 0 at every k; k = 3 is the default; other sizes are rejected."""
+    rng = np.random.default_rng(33)
+    X = rng.standard_normal((12, 16))
+    U = X / np.linalg.norm(X, axis=1, keepdims=True)
+    G = U @ U.T
+    want = 1 - (G.sum(axis=1) - np.diag(G)) / 11
+    np.testing.assert_allclose(O.css_frame(X, 3, 4, 9), want, atol=1e-14)
+    np.testing.assert_allclose(O.css_frame(X, 3, 4, 7), want, atol=1e-14)
+    Y = np.tile(rng.standard_normal(16), (30, 1))
+    for k in (3, 5, 7, 9):
+        np.testing.assert_allclose(O.css_frame(Y, 5, 6, k), 0.0, atol=1e-15)
+    frames = [(0, 4, 5), (20, 3, 3)]
+    Z = rng.standard_normal((35, 16))
+    np.testing.assert_array_equal(O.css_saliency(Z, frames, 3), O.css_saliency(Z, frames))
+    for bad in (1, 4, 11):
+        with pytest.raises(ValueError):
+            O.css_frame(Z[:20], 4, 5, bad)
+
 # ------------------------------------------------ TSG similarity variants ----
 
 def test_tsg_similarity_literal_twin_and_cosine_route():
