@@ -207,6 +207,49 @@ def decode_timing(prob, w, q, dk, dv, out, stream, reps=20):
     return entry
 
 
+def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
+    """The paper's ablation variants on the same workload, each timed apart
+    (HIP events on the launch stream) against its own roofline: rho under the
+    dot product and the negative L2 distance (the rho contraction's work),
+    the fixed-threshold gate (rho of the history read, the gate written) and
+    CSS over 5x5, 7x7 and 9x9 neighbourhoods (every visual key read once and
+    Phi written; the (k^2 - 1)/2 cosines per token are far below the MFMA
+    roofline at these sizes)."""
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    model = work_model(w, lay, cu_budget)
+    units = prob.units
+    n_vis = sum(int(r) * int(c) for _, r, c in lay.frame_meta)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    tmp = torch.empty_like(rho)
+    entry = {}
+    for name, sim in (("tsg_rho_dot", S.SIM_DOT), ("tsg_rho_neg_l2", S.SIM_NEG_L2)):
+        ms = timed(lambda: S.stlite_tsg_similarity(prob, sim, dk, tmp, out.ws_tsg, stream))
+        entry[name] = roofline_entry(model["tsg_rho"], ms)
+    S.stlite_tsg_rho(prob, dk, rho, out.ws_tsg, stream)
+    ms = timed(lambda: S.stlite_tsg_fixed_gate(prob, rho, 0.85, out.gate, stream))
+    entry["tsg_fixed_gate"] = roofline_entry(model["tsg_threshold"], ms)
+    for k in (5, 7, 9):
+        ms = timed(lambda: S.stlite_css_saliency_nbhd(prob, k, dk, out.phi, stream))
+        e = roofline_entry({"bound": "hbm", "bytes": model["css_saliency"]["bytes"]}, ms)
+        e["mfma_tflops"] = round(units * 2.0 * ((k * k - 1) // 2 + 1) * n_vis * w.head_dim / (ms * 1e-3) / 1e12, 2)
+        entry[f"css_saliency_{k}x{k}"] = e
+    log("variants: " + ", ".join(f"{n} {e['ms']:.3f} ms ({e['frac']:.2f})" for n, e in entry.items()))
+    return entry
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -349,6 +392,7 @@ def main():
         "stages": stages,
     }
     result["decode"] = decode_timing(prob, w, q, dk, dv, out, stream)
+    result["variants"] = variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host (cpu baseline)")
         result["cpu_baseline"] = cpu_baseline(w, inputs)

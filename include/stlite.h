@@ -182,6 +182,18 @@ stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, fl
                                   void* stream);
 
 /*
+ * CSS under a wider neighbourhood, for the paper's neighbourhood-size ablation
+ * (appendix CSS Neighborhood Size Ablation): H = mean over the in-grid cells of
+ * the nbhd x nbhd square centred on the token, other than the token itself, of
+ * the key cosine; phi = 1 - H (0 when the square holds no other in-grid cell,
+ * and on text).  nbhd = 3 is exactly stlite_css_saliency; 5, 7 and 9 run on the
+ * matrix cores (bf16 products, fp32 sums).  Any other nbhd is
+ * STLITE_ERR_INVALID_ARG.  Writes phi [units][total_tokens]; no workspace.
+ */
+stlite_status stlite_css_saliency_nbhd(const stlite_problem* p, int32_t nbhd, const uint16_t* k,
+                                       float* phi, void* stream);
+
+/*
  * Trajectory-aware Semantic Gating (Sec. TSG): for every historical visual
  * token i, rho_i = max over the current frame j of cos(k_i, k_j), clamped to
  * [-1, 1] and snapped to 1 when >= 1 - 1e-4.  Then, with m = min(B_s, |hist|),

@@ -16,6 +16,18 @@
 // ahead of the row being combined, so every key is read from HBM once per
 // strip.  The strips of one frame are given to work-groups that land on the
 // same XCD, where the halo columns hit the shared L2.
+//
+// The neighbourhood-size ablation widens the window to k x k, k = 2 KR + 1 in
+// {5, 7, 9} (css_wide_kernel): H = mean over the in-grid cells of the square
+// other than the centre.  There the cosines form a small dense contraction,
+// which runs on the matrix cores: a wave owns a 4-row x 16-column output tile
+// whose 64 keys stay in VGPRs as MFMA A operands, and walks the 4 + 2 KR
+// neighbour rows.  Each neighbour row's 16 + 2 KR columns (two 16-key B
+// blocks) are multiplied with every output row within KR of it; a per-lane
+// mask keeps the products with |dc| <= KR, scales them by the neighbour's
+// inverse norm and adds them in the accumulator lanes, and one 16-lane
+// reduction per output finishes the sum.  Halo rows shared by neighbouring
+// tiles are re-read through L2 (the tiles of one frame go to one XCD).
 #include "stlite_internal.h"
 #include "tile_lds.h"
 
@@ -189,6 +201,132 @@ __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   wait_vmcnt<0>();  // no DMA into LDS may outlive the work-group
 }
 
+constexpr int kWideRows = 4;   // output rows of a wave tile
+constexpr int kWideCols = 16;  // output columns of a wave tile
+
+__device__ inline float sumsq8(uint4 v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xffff0000u);
+    s = fmaf(lo, lo, s);
+    s = fmaf(hi, hi, s);
+  }
+  return s;
+}
+
+// Loads the MFMA operand fragments of key (row, col) of a frame: lane (n, q)
+// holds dims 32 kk + 8 q .. 32 kk + 8 q + 7 for kk = 0..3, and returns the
+// key's inverse norm (the same on the four lanes that share n).
+__device__ inline float load_key_operand(const uint16_t* kframe, int32_t row, int32_t col, int32_t C, int q,
+                                         bf16x8_t (&frag)[4]) {
+  const uint16_t* src = kframe + (size_t(row) * C + col) * kHeadDim + q * 8;
+  float ss = 0.0f;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const uint4 v = *reinterpret_cast<const uint4*>(src + kk * 32);
+    ss += sumsq8(v);
+    frag[kk] = __builtin_bit_cast(bf16x8_t, v);
+  }
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  return inv_norm(ss);
+}
+
+// Grid: x = work-groups of four wave tiles, in XCD-aware order; a.strips is
+// the largest number of 4 x 16 tiles of a frame; y = unit.
+template <int KR>
+__global__ __launch_bounds__(256) void css_wide_kernel(CssArgs a) {
+  const Layout& lay = a.lay;
+  const int unit = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t per_xcd = int32_t(gridDim.x) >> 3;
+  const int32_t logical = (int32_t(blockIdx.x & 7) * per_xcd + int32_t(blockIdx.x >> 3)) * 4 + wave;
+  const int32_t f = logical / a.strips, t = logical - f * a.strips;
+  if (f >= lay.n_frames) return;
+  const int32_t off = lay.frame_meta[3 * f], R = lay.frame_meta[3 * f + 1], C = lay.frame_meta[3 * f + 2];
+  const int32_t tiles_c = (C + kWideCols - 1) / kWideCols;
+  const int32_t tr = t / tiles_c;
+  const int32_t r0 = tr * kWideRows, c0 = (t - tr * tiles_c) * kWideCols;
+  if (r0 >= R) return;  // (also covers t beyond this frame's tiles)
+  const uint16_t* kframe = a.k + (size_t(unit) * lay.total_tokens + off) * kHeadDim;
+  const int n = lane & 15, q = lane >> 4;
+
+  // Output keys (row r0 + o, column c0 + n), clamped into the frame; the
+  // clamped copies are never stored.
+  bf16x8_t ha[kWideRows][4];
+  float rnA[kWideRows];
+#pragma unroll
+  for (int o = 0; o < kWideRows; ++o)
+    rnA[o] = load_key_operand(kframe, min(r0 + o, R - 1), min(c0 + n, C - 1), C, q, ha[o]);
+
+  // Accumulator element (i, n) of block nb pairs output column c0 + 4 q + i
+  // with neighbour column c0 - KR + 16 nb + n: dc = 16 nb + n - KR - 4 q - i.
+  uint32_t near = 0, self = 0;  // bit 4 nb + i
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int32_t d = 16 * nb + n - 4 * q - i;  // dc + KR
+      const int32_t cc = c0 - KR + 16 * nb + n;
+      if (d >= 0 && d <= 2 * KR && cc >= 0 && cc < C) near |= 1u << (4 * nb + i);
+      if (d == KR) self |= 1u << (4 * nb + i);
+    }
+
+  float psum[kWideRows][4];
+#pragma unroll
+  for (int o = 0; o < kWideRows; ++o)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) psum[o][i] = 0.0f;
+
+  const int32_t rr0 = max(r0 - KR, 0), rr1 = min(r0 + kWideRows - 1 + KR, R - 1);
+  for (int32_t rr = rr0; rr <= rr1; ++rr) {
+    bf16x8_t hb[2][4];
+    float rnB[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+      rnB[nb] = load_key_operand(kframe, rr, min(max(c0 - KR + 16 * nb + n, 0), C - 1), C, q, hb[nb]);
+#pragma unroll
+    for (int o = 0; o < kWideRows; ++o) {
+      const int32_t ro = r0 + o;
+      if (ro >= R || rr < ro - KR || rr > ro + KR) continue;  // wave-uniform
+      const uint32_t keep = rr == ro ? near & ~self : near;
+      f32x4_t acc[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[o][kk], hb[nb][kk], acc[nb], 0, 0, 0);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          psum[o][i] += (keep >> (4 * nb + i)) & 1u ? acc[nb][i] * rnB[nb] : 0.0f;
+    }
+  }
+
+  float* phi = a.phi + size_t(unit) * lay.total_tokens + off;
+#pragma unroll
+  for (int o = 0; o < kWideRows; ++o)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float h = psum[o][i];
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1) h += __shfl_xor(h, m);
+      const float rn_out = __shfl(rnA[o], 4 * q + i);  // inverse norm of output column c0 + 4 q + i
+      const int32_t r = r0 + o, c = c0 + 4 * q + i;
+      if (n == 0 && r < R && c < C) {
+        const int32_t rows_in = min(r + KR, R - 1) - max(r - KR, 0) + 1;
+        const int32_t cols_in = min(c + KR, C - 1) - max(c - KR, 0) + 1;
+        const int32_t nn = rows_in * cols_in - 1;
+        phi[size_t(r) * C + c] = nn > 0 ? 1.0f - h * rn_out / float(nn) : 0.0f;
+      }
+    }
+}
+
 __global__ __launch_bounds__(256) void css_text_kernel(CssArgs a) {
   const Layout& lay = a.lay;
   const int s = blockIdx.x, unit = blockIdx.y;
@@ -203,6 +341,22 @@ __global__ __launch_bounds__(256) void css_text_kernel(CssArgs a) {
 }
 
 }  // namespace
+
+hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream) {
+  hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.lay.n_frames == 0) return e;
+  const int64_t logical = int64_t(a.lay.n_frames) * a.strips;  // a.strips: max over frames of 4 x 16 tiles
+  const int64_t grid_x = ((logical + 3) / 4 + 7) / 8 * 8;
+  const dim3 grid(unsigned(grid_x), a.lay.n_units);
+  switch (nbhd) {
+    case 5: hipLaunchKernelGGL(css_wide_kernel<2>, grid, dim3(256), 0, stream, a); break;
+    case 7: hipLaunchKernelGGL(css_wide_kernel<3>, grid, dim3(256), 0, stream, a); break;
+    case 9: hipLaunchKernelGGL(css_wide_kernel<4>, grid, dim3(256), 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_css(const CssArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);

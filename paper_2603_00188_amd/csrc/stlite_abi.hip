@@ -366,6 +366,13 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
 }
 
 stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, float* phi, void* stream) {
+  return stlite_css_saliency_nbhd(p, 3, k, phi, stream);
+}
+
+stlite_status stlite_css_saliency_nbhd(const stlite_problem* p, int32_t nbhd, const uint16_t* k, float* phi,
+                                       void* stream) {
+  if (nbhd != 3 && nbhd != 5 && nbhd != 7 && nbhd != 9)
+    return fail(STLITE_ERR_INVALID_ARG, "nbhd must be 3, 5, 7 or 9 (got %d)", int(nbhd));
   stlite_status st = stlite_validate(p);
   if (st != STLITE_OK) return st;
   if (!k || !phi) return fail(STLITE_ERR_INVALID_ARG, "k and phi must be non-NULL");
@@ -375,10 +382,16 @@ stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, fl
   a.k = k;
   a.phi = phi;
   int32_t strips = 1;
-  for (int32_t fi = 0; fi < p->n_frames; ++fi)
-    strips = std::max<int32_t>(strips, (p->h_frame_meta[3 * fi + 2] + 13) / 14);
+  if (nbhd == 3) {
+    for (int32_t fi = 0; fi < p->n_frames; ++fi)
+      strips = std::max<int32_t>(strips, (p->h_frame_meta[3 * fi + 2] + 13) / 14);
+    a.strips = strips;
+    return hip_status(launch_css(a, static_cast<hipStream_t>(stream)), "css_saliency launch");
+  }
+  for (int32_t fi = 0; fi < p->n_frames; ++fi)  // 4 x 16 output tiles of the widest frame
+    strips = std::max<int32_t>(strips, ((p->h_frame_meta[3 * fi + 1] + 3) / 4) * ((p->h_frame_meta[3 * fi + 2] + 15) / 16));
   a.strips = strips;
-  return hip_status(launch_css(a, static_cast<hipStream_t>(stream)), "css_saliency launch");
+  return hip_status(launch_css_wide(a, nbhd, static_cast<hipStream_t>(stream)), "css_saliency launch");
 }
 
 stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float* rho, float* tau,

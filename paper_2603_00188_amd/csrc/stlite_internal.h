@@ -127,7 +127,7 @@ struct CssArgs {
   Layout lay;
   const uint16_t* k;
   float* phi;
-  int32_t strips;        // largest number of 14-column strips in a frame
+  int32_t strips;        // largest number of 14-column strips in a frame (3 x 3), or of 4 x 16 tiles (k x k)
 };
 
 struct SelectArgs {
@@ -176,6 +176,8 @@ hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t strea
 // gate = 1[float32(rho) <= tau] on historical tokens, 1 elsewhere (g.gate, g.rho, g.lay).
 hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream);
 hipError_t launch_css(const CssArgs& a, hipStream_t stream);
+// Phi under a k x k neighbourhood, nbhd = k in {5, 7, 9}.
+hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 

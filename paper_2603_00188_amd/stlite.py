@@ -26,6 +26,7 @@ EXPORTS = (
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
+    "stlite_css_saliency_nbhd",
 )
 
 
@@ -80,6 +81,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_decode_attention": (st, [P, st, vp, vp, vp, vp, vp, sz, vp]),
         "stlite_tsg_similarity": (st, [P, st, vp, vp, vp, sz, vp]),
         "stlite_tsg_fixed_gate": (st, [P, vp, f32, vp, vp]),
+        "stlite_css_saliency_nbhd": (st, [P, ctypes.c_int32, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -178,6 +180,11 @@ def stlite_score_window(p: Problem, q_win, k, a_base, workspace, stream=None) ->
 
 def stlite_css_saliency(p: Problem, k, phi, stream=None) -> None:
     _check(load().stlite_css_saliency(p.ref, _ptr(k), _ptr(phi), _stream(stream)), "stlite_css_saliency")
+
+
+def stlite_css_saliency_nbhd(p: Problem, nbhd: int, k, phi, stream=None) -> None:
+    _check(load().stlite_css_saliency_nbhd(p.ref, int(nbhd), _ptr(k), _ptr(phi), _stream(stream)),
+           "stlite_css_saliency_nbhd")
 
 
 def stlite_tsg_gate(p: Problem, k, rho, tau, gate, workspace, stream=None) -> None:

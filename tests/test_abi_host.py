@@ -201,3 +201,14 @@ def test_tsg_variant_rejections():
     bad = good()
     bad.c.n_layers = 0
     assert lib.stlite_tsg_fixed_gate(ctypes.byref(bad.c), FAKE_DEV, 0.85, FAKE_DEV, None) != S.OK
+
+
+def test_css_nbhd_rejections():
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    for bad in (0, 1, 2, 4, 6, 11, -3):
+        assert lib.stlite_css_saliency_nbhd(ref, bad, FAKE_DEV, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert b"nbhd" in lib.stlite_last_error()
+    assert lib.stlite_css_saliency_nbhd(ref, 5, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_css_saliency_nbhd(ref, 9, FAKE_DEV + 8, FAKE_DEV, None) == S.ERR_INVALID_ARG
