@@ -192,3 +192,29 @@ def tsg_similarity(K, hist, cur, sim):
             best = v if best is None or v > best else best
         out.append(best)
     return out
+
+
+def decode_scores(Q, K):
+    """a_i = (1/G) sum_g exp(z_gi) / sum_j exp(z_gj), z = q_g . k / sqrt(d), over all rows."""
+    G, L, d = len(Q), len(K), len(K[0])
+    a = [0.0] * L
+    for g in range(G):
+        z = [dot(Q[g], K[i]) / math.sqrt(d) for i in range(L)]
+        zm = max(z)
+        den = 0.0
+        for i in range(L):
+            den += math.exp(z[i] - zm)
+        for i in range(L):
+            a[i] += math.exp(z[i] - zm) / den / G
+    return a
+
+
+def hit_rate(kept, oracle):
+    """Fraction of the oracle set found in kept (both lists of token indices)."""
+    if not oracle:
+        return float("nan")
+    hits = 0
+    for t in oracle:
+        if t in kept:
+            hits += 1
+    return hits / len(oracle)

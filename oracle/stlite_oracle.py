@@ -24,6 +24,8 @@ takes them:
   compact          K' = K[I_keep], V' = V[I_keep]             (algorithm's return value)
   decode_attention softmax(q K^T / sqrt(d)) V over a cache    (problem setup: the decoding
                    phase that consumes K', V')
+  cache_hit_rate   |I_keep cap I*| / |I*|, I* = Top_B of the first decode
+                   query's attention over the full cache      (Eq. chr)
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -39,6 +41,9 @@ Readings where the paper is silent (each is also listed in the design notes):
   R8  rho >= 1 - 1e-4 is snapped to exactly 1 (duplicate class);
   R5b a k x k neighbourhood (k = 5, 7, 9) keeps R5's rule: its in-grid cells
       other than the centre, equally weighted;
+  R-chr the attention of the first decode query that defines the oracle set
+      is averaged over the kv head's query heads (as R2 does for A_base), so
+      that I* and I_keep are sets of the same (layer, kv head) unit;
   R8b under the negative-L2 similarity, a squared distance <= 1e-5 ||k_i||^2
       is snapped to 0 (the same duplicate class);
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
@@ -365,6 +370,37 @@ def decode_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
     p = np.exp(z)
     p = p / p.sum(axis=1, keepdims=True)
     return p @ V
+
+
+# ---------------------------------------------------------------------------
+# Cache hit rate (Sec. cache hit rate evaluation, Eq. chr)
+# ---------------------------------------------------------------------------
+
+def decode_attention_scores(Q: np.ndarray, K: np.ndarray) -> np.ndarray:
+    """a_i = (1/G) sum_g softmax_j(q_g . k_j / sqrt(d))_i over all L cached positions:
+    the attention distribution of the first decode query over the full cache,
+    averaged over the kv head's G query heads (reading R-chr, as R2 for A_base).
+    Q [G, d], K [L, d] float64."""
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    z = (Q @ K.T) / math.sqrt(K.shape[1])
+    z = z - z.max(axis=1, keepdims=True)
+    p = np.exp(z)
+    p = p / p.sum(axis=1, keepdims=True)
+    return p.mean(axis=0)
+
+
+def chr_oracle_set(a_dec: np.ndarray, B: int) -> np.ndarray:
+    """I* = Top_B of the decode attention (same order and tie-break as select_topk)."""
+    return select_topk(a_dec, B)
+
+
+def cache_hit_rate(kept: np.ndarray, oracle: np.ndarray) -> float:
+    """|I_keep cap I*| / |I*| for one step and unit (Eq. chr before the average
+    over steps); NaN when I* is empty (B = 0)."""
+    if len(oracle) == 0:
+        return float("nan")
+    return len(np.intersect1d(kept, oracle)) / len(oracle)
 
 
 def seq_frames_local(cu_seqlens, cu_frames, frame_meta, s: int):

@@ -639,3 +639,60 @@ def test_decode_over_compacted_cache_at_beta_one_is_full_decode():
     full = O.decode_attention(Qd, O.bf16_to_f64(Kb), O.bf16_to_f64(Vb))
     comp = O.decode_attention(Qd, O.bf16_to_f64(res["k_out"]), O.bf16_to_f64(res["v_out"]))
     np.testing.assert_array_equal(full, comp)
+
+
+# ------------------------------------------------------- cache hit rate ----
+
+def test_decode_attention_scores_definition():
+    rng = np.random.default_rng(40)
+    G, L, d = 3, 17, 8
+    Q, K = rng.standard_normal((G, d)), rng.standard_normal((L, d))
+    a = O.decode_attention_scores(Q, K)
+    np.testing.assert_allclose(a, O1.decode_scores(Q.tolist(), K.tolist()), atol=1e-15)
+    # the decode query sees every cached key: window scoring with delta = 1 at
+    # the last position is the same distribution
+    np.testing.assert_allclose(a, O.base_score(Q[:, None, :], K), atol=1e-15)
+    np.testing.assert_allclose(a, scipy.special.softmax(Q @ K.T / math.sqrt(d), axis=1).mean(axis=0), atol=1e-15)
+    assert a.sum() == pytest.approx(1.0, abs=1e-14)
+    np.testing.assert_allclose(O.decode_attention_scores(np.zeros((2, d)), K), np.full(L, 1 / L), atol=1e-16)
+    # two logit levels: keys e1 (logit x) and 0 (logit 0) under q = x sqrt(d) e1
+    K2 = np.zeros((5, d))
+    K2[[1, 3], 0] = 1.0
+    x = 0.7
+    q = np.zeros((1, d))
+    q[0, 0] = x * math.sqrt(d)
+    hi = math.exp(x) / (2 * math.exp(x) + 3)
+    np.testing.assert_allclose(O.decode_attention_scores(q, K2), [(1 - 2 * hi) / 3, hi, (1 - 2 * hi) / 3, hi,
+                                                                  (1 - 2 * hi) / 3], atol=1e-15)
+
+
+def test_cache_hit_rate_definition_and_random_expectation():
+    assert O.cache_hit_rate(np.array([1, 2, 3]), np.array([2, 3, 4])) == pytest.approx(2 / 3)
+    assert O.cache_hit_rate(np.array([5, 6]), np.array([5, 6])) == 1.0
+    assert O.cache_hit_rate(np.array([0, 1]), np.array([5, 6])) == 0.0
+    assert math.isnan(O.cache_hit_rate(np.array([], int), np.array([], int)))
+    assert O1.hit_rate([1, 2, 3], [2, 3, 4]) == O.cache_hit_rate(np.array([1, 2, 3]), np.array([2, 3, 4]))
+    # the paper's footnote: random selection hits beta in expectation (hypergeometric mean B^2/L / B)
+    rng = np.random.default_rng(41)
+    L, B = 500, 100
+    oracle = O.chr_oracle_set(rng.uniform(size=L), B)
+    rates = [O.cache_hit_rate(np.sort(rng.choice(L, B, replace=False)), oracle) for _ in range(4000)]
+    sd = math.sqrt((B / L) * (1 - B / L) * (L - B) / (L - 1) / B) / math.sqrt(len(rates))
+    assert abs(np.mean(rates) - B / L) < 5 * sd
+
+
+def test_chr_oracle_set_brute_force_and_snapkv_identity():
+    """I* is the top-B by (attention desc, index asc); SnapKV voting with a
+    one-query window equal to the decode query keeps exactly I* (CHR = 1)."""
+    rng = np.random.default_rng(42)
+    a = np.round(rng.uniform(size=40), 1)      # many ties
+    for B in (0, 1, 7, 40):
+        want = sorted(sorted(range(40), key=lambda i: (-np.float32(a[i]), i))[:B])
+        assert O.chr_oracle_set(a, B).tolist() == want
+    G, L, d = 4, 60, 16
+    Q, K = rng.standard_normal((G, d)), rng.standard_normal((L, d))
+    B = O.budget(L, 1, 5)
+    oracle = O.chr_oracle_set(O.decode_attention_scores(Q, K), B)
+    snap = O.select_topk(O.base_score(Q[:, None, :], K), B)
+    assert O.cache_hit_rate(snap, oracle) == 1.0
+
