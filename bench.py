@@ -250,6 +250,36 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
     return entry
 
 
+def chr_harness(prob, q, dk, a_base, out, stream):
+    """Cache hit rate (Eq. chr) of the pass's kept sets and of SnapKV mode (the
+    same window score, flat top-B, no CSS or gate) against I*, the top-B of the
+    first decode query's attention over the full cache.  On this generator the
+    decode query is the last window query, so window voting is close to I* by
+    construction: these values describe the generator, not GUI traces."""
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    from paper_2603_00188_amd import workload as W
+    q_dec = torch.from_numpy(np.ascontiguousarray(W.decode_queries(q)).view(np.int16)).cuda()
+    p1 = S.decode_problem(prob)
+    snap = torch.empty_like(out.kept)
+    S.stlite_select_topk(prob, a_base, None, None, 0.0, snap, None, out.ws, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    star, _ = S.oracle_set(p1, q_dec, dk, stream=stream)  # warm-up and allocation
+    torch.cuda.synchronize()
+    e0.record(stream)
+    S.oracle_set(p1, q_dec, dk, kept=star, stream=stream)
+    hits_st = S.kept_overlap(prob, out.kept, star, stream=stream)
+    e1.record(stream)
+    hits_sn = S.kept_overlap(prob, snap, star, stream=stream)
+    torch.cuda.synchronize()
+    B = np.diff(prob.h["cu_budget"]).astype(np.float64)
+    entry = {"st_lite": round(float((hits_st.cpu().numpy() / B).mean()), 4),
+             "snapkv": round(float((hits_sn.cpu().numpy() / B).mean()), 4),
+             "units": prob.units, "ms_oracle_set_and_overlap": round(e0.elapsed_time(e1), 3)}
+    log(f"cache hit rate: ST-Lite {entry['st_lite']:.4f}, SnapKV mode {entry['snapkv']:.4f}")
+    return entry
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -393,6 +423,8 @@ def main():
     }
     result["decode"] = decode_timing(prob, w, q, dk, dv, out, stream)
     result["variants"] = variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream)
+    step()  # the pass's kept sets again (the variants overwrote phi and gate)
+    result["chr"] = chr_harness(prob, q, dk, out.a_base, out, stream)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host (cpu baseline)")
         result["cpu_baseline"] = cpu_baseline(w, inputs)

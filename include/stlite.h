@@ -19,6 +19,16 @@
  *   stlite_decode_attention  softmax(q K^T / sqrt(d)) V over the full or the
  *                            compacted cache                  (problem setup)
  *
+ * the variants of the paper's ablations,
+ *
+ *   stlite_tsg_similarity    rho under the dot product or -L2 (similarity ablation)
+ *   stlite_tsg_fixed_gate    gate = 1[rho <= tau] for a fixed tau (necessity controls)
+ *   stlite_css_saliency_nbhd CSS over 5x5, 7x7, 9x9 windows (neighbourhood ablation)
+ *
+ * and, for the cache hit rate evaluation,
+ *
+ *   stlite_kept_overlap      |I_keep cap I*| per unit and sequence (Eq. chr)
+ *
  * Conventions shared by every call
  * --------------------------------
  * Pointers are DEVICE pointers unless their name starts with h_ (host).  bf16
@@ -299,6 +309,21 @@ stlite_status stlite_decode_attention(const stlite_problem* p, stlite_cache cach
                                       const uint16_t* q_dec, const uint16_t* k,
                                       const uint16_t* v, float* out, void* workspace,
                                       size_t workspace_bytes, void* stream);
+
+/*
+ * Cache hit rate numerator (Sec. cache hit rate evaluation, Eq. chr):
+ *   hits[u][s] = |kept_a[u] cap kept_b[u]| over sequence s's entries
+ * for two retained sets in the layout stlite_select_topk writes (B_s strictly
+ * ascending absolute token indices of sequence s per unit).  With kept_b the
+ * oracle set I* -- the top-B_s of the first decode query's attention over the
+ * full cache, which stlite_score_window with window 1 and that query followed
+ * by stlite_select_topk with no phi and no gate computes -- hits / B_s is the
+ * CHR of kept_a for that unit and step.  hits int32 [units][n_seqs]; no
+ * workspace.  Lists that break the ordering contract give a wrong count but
+ * no out-of-range access.
+ */
+stlite_status stlite_kept_overlap(const stlite_problem* p, const int32_t* kept_a,
+                                  const int32_t* kept_b, int32_t* hits, void* stream);
 
 #ifdef __cplusplus
 }

@@ -208,11 +208,8 @@ __device__ inline float sumsq8(uint4 v) {
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
   float s = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xffff0000u);
-    s = fmaf(lo, lo, s);
-    s = fmaf(hi, hi, s);
-  }
+  for (int j = 0; j < 4; ++j)
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[j]), __builtin_bit_cast(bf16x2_t, w[j]), s, false);
   return s;
 }
 
@@ -280,18 +277,45 @@ __global__ __launch_bounds__(256) void css_wide_kernel(CssArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) psum[o][i] = 0.0f;
 
+  const uint32_t off_self = near & ~self;
   const int32_t rr0 = max(r0 - KR, 0), rr1 = min(r0 + kWideRows - 1 + KR, R - 1);
-  for (int32_t rr = rr0; rr <= rr1; ++rr) {
-    bf16x8_t hb[2][4];
-    float rnB[2];
+  // Neighbour row rr's B fragments: strip keys c0 - KR + 16 nb + n (clamped).
+  auto fetch = [&](int32_t rr, uint4 (&v)[2][4]) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-      rnB[nb] = load_key_operand(kframe, rr, min(max(c0 - KR + 16 * nb + n, 0), C - 1), C, q, hb[nb]);
+    for (int nb = 0; nb < 2; ++nb) {
+      const uint16_t* src =
+          kframe + (size_t(rr) * C + min(max(c0 - KR + 16 * nb + n, 0), C - 1)) * kHeadDim + q * 8;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) v[nb][kk] = *reinterpret_cast<const uint4*>(src + kk * 32);
+    }
+  };
+  // One neighbour row; the next row's loads are issued first and stay in
+  // flight under this row's matrix work.
+  auto row = [&](int32_t rr, const uint4 (&v)[2][4], uint4 (&next)[2][4]) {
+    if (rr < rr1) fetch(rr + 1, next);
+    bf16x8_t hb[2][4];
+    float sc_near[2][4], sc_off[2][4];  // the neighbour's inverse norm where the product counts, else 0
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float ss = 0.0f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        ss += sumsq8(v[nb][kk]);
+        hb[nb][kk] = __builtin_bit_cast(bf16x8_t, v[nb][kk]);
+      }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      const float rn = inv_norm(ss);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sc_near[nb][i] = (near >> (4 * nb + i)) & 1u ? rn : 0.0f;
+        sc_off[nb][i] = (off_self >> (4 * nb + i)) & 1u ? rn : 0.0f;
+      }
+    }
 #pragma unroll
     for (int o = 0; o < kWideRows; ++o) {
       const int32_t ro = r0 + o;
       if (ro >= R || rr < ro - KR || rr > ro + KR) continue;  // wave-uniform
-      const uint32_t keep = rr == ro ? near & ~self : near;
       f32x4_t acc[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
@@ -300,12 +324,24 @@ __global__ __launch_bounds__(256) void css_wide_kernel(CssArgs a) {
         for (int kk = 0; kk < 4; ++kk)
           acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ha[o][kk], hb[nb][kk], acc[nb], 0, 0, 0);
       }
+      if (rr == ro) {
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          psum[o][i] += (keep >> (4 * nb + i)) & 1u ? acc[nb][i] * rnB[nb] : 0.0f;
+          for (int i = 0; i < 4; ++i) psum[o][i] = fmaf(acc[nb][i], sc_off[nb][i], psum[o][i]);
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) psum[o][i] = fmaf(acc[nb][i], sc_near[nb][i], psum[o][i]);
+      }
     }
+  };
+  uint4 bufA[2][4], bufB[2][4];
+  fetch(rr0, bufA);
+  for (int32_t rr = rr0; rr <= rr1; rr += 2) {
+    row(rr, bufA, bufB);
+    if (rr + 1 <= rr1) row(rr + 1, bufB, bufA);
   }
 
   float* phi = a.phi + size_t(unit) * lay.total_tokens + off;

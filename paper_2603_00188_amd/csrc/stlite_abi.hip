@@ -513,6 +513,25 @@ stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, cons
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)), "compact_kv launch");
 }
 
+stlite_status stlite_kept_overlap(const stlite_problem* p, const int32_t* kept_a, const int32_t* kept_b,
+                                  int32_t* hits, void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (!hits) return fail(STLITE_ERR_INVALID_ARG, "hits must be non-NULL");
+  if (p->total_budget > 0 && (!kept_a || !kept_b))
+    return fail(STLITE_ERR_INVALID_ARG, "kept_a and kept_b must be non-NULL");
+  OverlapArgs a;
+  a.lay = make_layout(p);
+  a.kept_a = kept_a;
+  a.kept_b = kept_b;
+  a.hits = hits;
+  int64_t spans = 1;
+  for (int32_t s = 0; s < p->n_seqs; ++s)
+    spans = std::max<int64_t>(spans, (int64_t(p->h_cu_seqlens[s + 1]) - p->h_cu_seqlens[s] + 65535) / 65536);
+  a.spans_per_seq = int32_t(spans);
+  return hip_status(launch_kept_overlap(a, static_cast<hipStream_t>(stream)), "kept_overlap launch");
+}
+
 stlite_status stlite_decode_attention(const stlite_problem* p, stlite_cache cache, const uint16_t* q_dec,
                                       const uint16_t* k, const uint16_t* v, float* out, void* ws,
                                       size_t ws_bytes, void* stream) {

@@ -130,6 +130,14 @@ struct CssArgs {
   int32_t strips;        // largest number of 14-column strips in a frame (3 x 3), or of 4 x 16 tiles (k x k)
 };
 
+struct OverlapArgs {
+  Layout lay;
+  const int32_t* kept_a;  // [units][total_budget], ascending per sequence
+  const int32_t* kept_b;
+  int32_t* hits;          // [units][n_seqs]
+  int32_t spans_per_seq;  // 65,536-token spans of the longest sequence
+};
+
 struct SelectArgs {
   Layout lay;
   const float* a_base;
@@ -175,6 +183,8 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 // gate = 1[float32(rho) <= tau] on historical tokens, 1 elsewhere (g.gate, g.rho, g.lay).
 hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream);
+// hits[u][s] = |kept_a cap kept_b| of sequence s in unit u.
+hipError_t launch_kept_overlap(const OverlapArgs& a, hipStream_t stream);
 hipError_t launch_css(const CssArgs& a, hipStream_t stream);
 // Phi under a k x k neighbourhood, nbhd = k in {5, 7, 9}.
 hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream);

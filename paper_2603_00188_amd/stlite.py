@@ -26,7 +26,7 @@ EXPORTS = (
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
-    "stlite_css_saliency_nbhd",
+    "stlite_css_saliency_nbhd", "stlite_kept_overlap",
 )
 
 
@@ -82,6 +82,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_tsg_similarity": (st, [P, st, vp, vp, vp, sz, vp]),
         "stlite_tsg_fixed_gate": (st, [P, vp, f32, vp, vp]),
         "stlite_css_saliency_nbhd": (st, [P, ctypes.c_int32, vp, vp, vp]),
+        "stlite_kept_overlap": (st, [P, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -224,6 +225,11 @@ def stlite_compact_kv(p: Problem, k, v, kept, k_out, v_out, stream=None) -> None
                                     _stream(stream)), "stlite_compact_kv")
 
 
+def stlite_kept_overlap(p: Problem, kept_a, kept_b, hits, stream=None) -> None:
+    _check(load().stlite_kept_overlap(p.ref, _ptr(kept_a), _ptr(kept_b), _ptr(hits), _stream(stream)),
+           "stlite_kept_overlap")
+
+
 def stlite_decode_attention(p: Problem, cache: int, q_dec, k, v, out, workspace, stream=None) -> None:
     _check(load().stlite_decode_attention(p.ref, int(cache), _ptr(q_dec), _ptr(k), _ptr(v), _ptr(out),
                                           _ptr(workspace), _nbytes(workspace), _stream(stream)),
@@ -271,6 +277,42 @@ class Buffers:
         self.ws_tsg = torch.empty(max(ws_tsg, 256), dtype=torch.uint8, device=device)
         # side streams at the default priority
         self.side = (torch.cuda.Stream(device=device), torch.cuda.Stream(device=device))
+
+
+def decode_problem(p: Problem) -> Problem:
+    """The same layout and budgets with a one-query window: the problem on which
+    stlite_score_window scores the first decode query over the full cache."""
+    h = p.h
+    return Problem(p.n_layers, p.n_q_heads, p.n_kv_heads, 1, h["cu_seqlens"], h["cu_frames"], h["frame_meta"],
+                   h["cu_budget"], device=p.d["cu_seqlens"].device)
+
+
+def oracle_set(p1: Problem, q_dec, k, kept=None, a_dec=None, stream=None):
+    """I* of the cache hit rate (Eq. chr) for every unit and sequence: the top-B_s
+    of the first decode query's attention over the full cache.  p1 is
+    decode_problem(p); q_dec [n_layers][n_seqs][n_q_heads][d] bf16 (the one-query
+    window).  Two C calls: stlite_score_window, then stlite_select_topk with no
+    phi and no gate.  Returns (kept [units][total_budget] int32, a_dec)."""
+    import torch
+    dev = q_dec.device
+    if a_dec is None:
+        a_dec = torch.empty((p1.units, p1.total_tokens), dtype=torch.float32, device=dev)
+    if kept is None:
+        kept = torch.empty((p1.units, max(p1.total_budget, 1)), dtype=torch.int32, device=dev)
+    n = max(p1.workspace_size(CALL_SCORE_WINDOW), p1.workspace_size(CALL_SELECT_TOPK), 256)
+    ws = torch.empty(n, dtype=torch.uint8, device=dev)
+    stlite_score_window(p1, q_dec, k, a_dec, ws, stream)
+    stlite_select_topk(p1, a_dec, None, None, 0.0, kept, None, ws, stream)
+    return kept, a_dec
+
+
+def kept_overlap(p: Problem, kept_a, kept_b, hits=None, stream=None):
+    """hits [units][n_seqs] int32 = |kept_a cap kept_b| per unit and sequence."""
+    import torch
+    if hits is None:
+        hits = torch.empty((p.units, p.n_seqs), dtype=torch.int32, device=kept_a.device)
+    stlite_kept_overlap(p, kept_a, kept_b, hits, stream)
+    return hits
 
 
 def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: bool = True,

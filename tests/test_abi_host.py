@@ -212,3 +212,15 @@ def test_css_nbhd_rejections():
     assert b"nbhd" in lib.stlite_last_error()
     assert lib.stlite_css_saliency_nbhd(ref, 5, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
     assert lib.stlite_css_saliency_nbhd(ref, 9, FAKE_DEV + 8, FAKE_DEV, None) == S.ERR_INVALID_ARG
+
+
+def test_kept_overlap_rejections():
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    assert lib.stlite_kept_overlap(ref, FAKE_DEV, FAKE_DEV, None, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_kept_overlap(ref, None, FAKE_DEV, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_kept_overlap(ref, FAKE_DEV, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    bad = good()
+    bad.c.n_seqs = 0
+    assert lib.stlite_kept_overlap(ctypes.byref(bad.c), FAKE_DEV, FAKE_DEV, FAKE_DEV, None) != S.OK
