@@ -226,3 +226,35 @@ def test_similarity_variants_trajectory_sampled(torch_cuda):
             rows = np.sort(rng.choice(len(hist), size=min(1024, len(hist)), replace=False))
             r = check_similarity(case, rho, sim, layer, kv, 0, rows=rows)
             H.log(f"tsg similarity trajectory {sim} layer {layer} kv {kv}: worst err/tol {r:.3g}")
+
+
+@pytest.mark.parametrize("name", ["ragged", "dups"])
+def test_uniform_base_prior(torch_cuda, name):
+    """The uniform base prior: stlite_select_topk with a constant a_base, on the
+    GPU's own Phi and gate, against the oracle's top-B of the same scores."""
+    import torch
+    O, S, H, SMALL = _mods()
+    case = H.Case(SMALL[name])
+    res = case.run()
+    out = case.out
+    const = torch.full_like(out.a_base, 0.125)
+    kept = torch.empty_like(out.kept)
+    S.stlite_select_topk(case.prob, const, out.phi, out.gate, case.w.alpha, kept, None, out.ws)
+    torch.cuda.synchronize()
+    kept = kept[:, :case.prob.total_budget].cpu().numpy()
+    cb = case.cu_budget
+    for u, layer, kv, s, a, L, hist, cur in _units(case):
+        frames = O.seq_frames_local(case.lay.cu_seqlens, case.lay.cu_frames, case.lay.frame_meta, s)
+        _, _, text = O.split_tokens(L, frames)
+        visual = np.ones(L, bool)
+        visual[text] = False
+        Sref = O.integrate(np.full(L, 0.125), res["phi"][u, a:a + L].astype(np.float64),
+                           res["gate"][u, a:a + L], visual, case.w.alpha)
+        B = int(cb[s + 1] - cb[s])
+        got = kept[u, cb[s]:cb[s + 1]] - a
+        want = O.select_topk(Sref, B)
+        sym = np.setxor1d(got, want)
+        if len(sym):
+            sB = np.sort(Sref.astype(np.float32))[::-1][B - 1]
+            assert (np.abs(Sref[sym] - sB) <= 1e-6 * abs(sB)).all(), f"{name} unit {u} seq {s}"
+

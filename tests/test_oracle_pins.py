@@ -696,3 +696,21 @@ def test_chr_oracle_set_brute_force_and_snapkv_identity():
     snap = O.select_topk(O.base_score(Q[:, None, :], K), B)
     assert O.cache_hit_rate(snap, oracle) == 1.0
 
+
+
+def test_uniform_base_prior_closed_forms():
+    """A constant A: with no CSS and no gate the top-B is the first B tokens
+    (index tie-break); with Phi it ranks visual tokens by Phi, text at the
+    constant, and gated-out visual tokens last (S = 0)."""
+    L, B, c = 12, 5, 0.25
+    A = np.full(L, c)
+    visual = np.zeros(L, bool)
+    visual[2:10] = True
+    assert O.select_topk(O.integrate(A, np.zeros(L), np.ones(L, np.uint8), visual, 1.0), B).tolist() == [0, 1, 2, 3, 4]
+    phi = np.zeros(L)
+    phi[[3, 7, 8]] = [0.5, 0.9, 0.1]
+    gate = np.ones(L, np.uint8)
+    gate[7] = 0
+    S = O.integrate(A, phi, gate, visual, 1.0)
+    # scores: 3 -> 0.75, 8 -> 0.35, the other visual and text tokens -> 0.25, token 7 -> 0
+    assert O.select_topk(S, B).tolist() == [0, 1, 2, 3, 8]
