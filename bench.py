@@ -273,8 +273,9 @@ def chr_harness(prob, q, dk, a_base, out, stream):
     hits_sn = S.kept_overlap(prob, snap, star, stream=stream)
     torch.cuda.synchronize()
     B = np.diff(prob.h["cu_budget"]).astype(np.float64)
-    entry = {"st_lite": round(float((hits_st.cpu().numpy() / B).mean()), 4),
-             "snapkv": round(float((hits_sn.cpu().numpy() / B).mean()), 4),
+    rate = lambda h: float(np.mean(h[:, B > 0] / B[B > 0])) if (B > 0).any() else float("nan")
+    entry = {"st_lite": round(rate(hits_st.cpu().numpy()), 4),
+             "snapkv": round(rate(hits_sn.cpu().numpy()), 4),
              "units": prob.units, "ms_oracle_set_and_overlap": round(e0.elapsed_time(e1), 3)}
     log(f"cache hit rate: ST-Lite {entry['st_lite']:.4f}, SnapKV mode {entry['snapkv']:.4f}")
     return entry

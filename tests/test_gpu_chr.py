@@ -158,3 +158,26 @@ def test_chr_trajectory_sampled(torch_cuda):
     B = case.prob.total_budget
     H.log(f"chr trajectory mean over all units: ST-Lite {r['hits_st'].mean() / B:.4f}, "
           f"SnapKV {r['hits_sn'].mean() / B:.4f}")
+
+
+@pytest.mark.timeout(900)
+def test_chr_ragged_batch_sampled(torch_cuda):
+    """The ragged batch of 8 trajectories (two of its layers): hits of every
+    unit and sequence exact, CHR of sampled sequences against the oracle."""
+    O, S, H, _ = _mods()
+    w = W.config(4)
+    H.log(f"chr ragged batch: generate L={w.total_tokens} x 2 layers")
+    case = H.Case(w, layers=[0, 27])
+    r = run_chr(case)
+    cb = case.cu_budget
+    for u in range(case.prob.units):
+        for s in range(case.lay.n_seqs):
+            a = int(case.lay.cu_seqlens[s])
+            kept = r["res"]["kept"][u, cb[s]:cb[s + 1]]
+            star = r["star"][u, cb[s]:cb[s + 1]]
+            assert r["hits_st"][u, s] == len(np.intersect1d(kept, star)), (u, s)
+            assert r["hits_sn"][u, s] == len(np.intersect1d(r["snap"][u, cb[s]:cb[s + 1]], star)), (u, s)
+            assert (star >= a).all() and (star < case.lay.cu_seqlens[s + 1]).all()
+    for unit in ((0, 0, 0), (0, 3, 4), (1, 1, 7), (1, 2, 2)):
+        H.log(f"chr ragged batch unit {unit}: {check_chr_unit(case, r, *unit)}")
+

@@ -105,3 +105,24 @@ def test_css_nbhd_trajectory_sampled(torch_cuda):
         for layer, kv, frames in ((0, 0, (0, 47)), (0, 3, (20,)), (1, 1, (46,)), (1, 2, (5,))):
             r = check_phi(case, phi, nbhd, layer, kv, 0, frames_only=frames)
             H.log(f"css nbhd trajectory k={nbhd} layer {layer} kv {kv}: worst rel err {r:.3g}")
+
+
+@pytest.mark.timeout(900)
+def test_css_nbhd_ragged_batch_sampled(torch_cuda):
+    """The ragged batch of 8 trajectories (two of its layers): sampled frames of
+    sampled sequences at k = 7, text exactly 0 everywhere."""
+    O, S, H, _ = _mods()
+    w = W.config(4)
+    H.log(f"css nbhd ragged batch: generate L={w.total_tokens} x 2 layers")
+    case = H.Case(w, layers=[0, 27])
+    phi = _phi(case, 7)
+    lay = case.lay
+    for s in range(lay.n_seqs):
+        a, b = int(lay.cu_seqlens[s]), int(lay.cu_seqlens[s + 1])
+        frames = O.seq_frames_local(lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s)
+        _, _, text = O.split_tokens(b - a, frames)
+        assert (phi[:, a:b][:, text] == 0).all(), s
+    for layer, kv, s, fr in ((0, 0, 0, (0, 5)), (0, 3, 4, (2,)), (1, 1, 7, (1,)), (1, 2, 6, (3,))):
+        r = check_phi(case, phi, 7, layer, kv, s, frames_only=fr)
+        H.log(f"css nbhd ragged batch unit ({layer},{kv},{s}): worst rel err {r:.3g}")
+

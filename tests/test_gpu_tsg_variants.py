@@ -258,3 +258,32 @@ def test_uniform_base_prior(torch_cuda, name):
             sB = np.sort(Sref.astype(np.float32))[::-1][B - 1]
             assert (np.abs(Sref[sym] - sB) <= 1e-6 * abs(sB)).all(), f"{name} unit {u} seq {s}"
 
+
+@pytest.mark.timeout(900)
+def test_variants_ragged_batch_sampled(torch_cuda):
+    """The ragged batch of 8 trajectories (two of its layers): dot and -L2 rho on
+    sampled rows of sampled sequences, and the fixed gate on every unit."""
+    import torch
+    O, S, H, SMALL = _mods()
+    w = W.config(4)
+    H.log(f"tsg variants ragged batch: generate L={w.total_tokens} x 2 layers")
+    case = H.Case(w, layers=[0, 27])
+    rng = np.random.default_rng(4)
+    for sim in ("dot", "neg_l2"):
+        rho = _similarity(case, sim).cpu().numpy()
+        for layer, kv, s in ((0, 0, 0), (0, 2, 3), (1, 1, 5), (1, 3, 7)):
+            a, b = int(case.lay.cu_seqlens[s]), int(case.lay.cu_seqlens[s + 1])
+            frames = O.seq_frames_local(case.lay.cu_seqlens, case.lay.cu_frames, case.lay.frame_meta, s)
+            hist, _, _ = O.split_tokens(b - a, frames)
+            rows = np.sort(rng.choice(len(hist), size=min(512, len(hist)), replace=False))
+            rr = check_similarity(case, rho, sim, layer, kv, s, rows=rows)
+            H.log(f"tsg variants ragged batch {sim} unit ({layer},{kv},{s}): worst err/tol {rr:.3g}")
+    S.stlite_tsg_rho(case.prob, case.dk, case.out.rho, case.out.ws_tsg)
+    gate = torch.empty((case.prob.units, case.prob.total_tokens), dtype=torch.uint8, device="cuda")
+    S.stlite_tsg_fixed_gate(case.prob, case.out.rho, 0.85, gate)
+    torch.cuda.synchronize()
+    rho, g = case.out.rho.cpu().numpy(), gate.cpu().numpy()
+    for u, layer, kv, s, a, L, hist, cur in _units(case):
+        want = O.tsg_fixed_gate(rho[u, a:a + L][hist].astype(np.float64), hist, L, 0.85)
+        assert np.array_equal(g[u, a:a + L], want), (u, s)
+
