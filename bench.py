@@ -250,6 +250,52 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
     return entry
 
 
+def measured_peaks(stream):
+    """Second denominators measured on this GPU (the published peaks stay the
+    roofline's `peak`): the matrix cores in the two MFMA shapes the compression
+    kernels use, driven by stlite_probe_mfma with random operands that rotate
+    per instruction; a large hipBLASLt bf16 GEMM (torch.matmul); and a device
+    copy (torch copy_, bytes read + written)."""
+    import torch
+    from paper_2603_00188_amd import stlite as S
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    out = {}
+    n_groups = 2048  # 8 waves per SIMD on all 256 CUs
+    gen = torch.Generator().manual_seed(0)
+    ops = (torch.randn(n_groups * 256 * 128, generator=gen) * 0.25).to(torch.bfloat16).cuda().view(torch.int16)
+    sink = torch.empty(n_groups * 256, dtype=torch.float32, device="cuda")
+    for name, shape, iters in (("mfma_16x16x32_bf16", S.PROBE_MFMA_16X16X32, 200),
+                               ("mfma_32x32x16_bf16", S.PROBE_MFMA_32X32X16, 100)):
+        t = timed(lambda: S.stlite_probe_mfma(shape, ops, sink, n_groups, iters, stream), 5)
+        flops = 8.0 * iters * n_groups * 4 * S.PROBE_FLOPS[shape]
+        out[name + "_tflops"] = round(flops / t / 1e12, 1)
+    n = 8192
+    a = torch.randn((n, n), generator=gen).to(torch.bfloat16).cuda()
+    b = torch.randn((n, n), generator=gen).to(torch.bfloat16).cuda()
+    with torch.cuda.stream(stream):
+        t = timed(lambda: torch.matmul(a, b), 10)
+    out["hipblaslt_gemm_8192_bf16_tflops"] = round(2.0 * n ** 3 / t / 1e12, 1)
+    src = torch.ones(1 << 31, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    with torch.cuda.stream(stream):
+        t = timed(lambda: dst.copy_(src), 10)
+    out["device_copy_2gib_gbs"] = round(2.0 * src.numel() / t / 1e9, 1)
+    del a, b, src, dst, ops, sink
+    log("measured peaks: " + ", ".join(f"{k} {v}" for k, v in out.items()))
+    return out
+
+
 def chr_harness(prob, q, dk, a_base, out, stream):
     """Cache hit rate (Eq. chr) of the pass's kept sets and of SnapKV mode (the
     same window score, flat top-B, no CSS or gate) against I*, the top-B of the
@@ -422,6 +468,11 @@ def main():
         "roofline": roof,
         "stages": stages,
     }
+    peaks = measured_peaks(stream)
+    result["measured_peaks"] = peaks
+    mp = peaks["mfma_16x16x32_bf16_tflops"] if roof["bound"] == "mfma" else peaks["device_copy_2gib_gbs"]
+    roof["measured_peak"] = mp
+    roof["frac_of_measured_peak"] = round(roof["achieved"] / mp, 4)
     result["decode"] = decode_timing(prob, w, q, dk, dv, out, stream)
     result["variants"] = variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream)
     step()  # the pass's kept sets again (the variants overwrote phi and gate)

@@ -1,0 +1,47 @@
+/*
+ * stlite_probe.h -- throughput probes of the MI355X matrix cores, used by the
+ * benchmark as a measured second denominator beside the published bf16 peak.
+ * Not part of the compression method.
+ *
+ * Each probe keeps every SIMD busy with independent MFMA chains whose
+ * operands come from caller-supplied data and rotate among eight A and
+ * eight B fragments per lane, so that the matrix cores switch data as they
+ * do in the compression kernels (a loop on constant operands draws less
+ * power and would overstate the sustained rate).
+ */
+#ifndef STLITE_PROBE_H
+#define STLITE_PROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "stlite.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* MFMA shape of a probe. */
+typedef enum stlite_probe_shape {
+  STLITE_PROBE_MFMA_16X16X32_BF16 = 0, /* v_mfma_f32_16x16x32_bf16: 16384 flops per instruction */
+  STLITE_PROBE_MFMA_32X32X16_BF16 = 1  /* v_mfma_f32_32x32x16_bf16: 32768 flops per instruction */
+} stlite_probe_shape;
+
+/*
+ * Runs n_groups work-groups of 256 threads, each lane issuing 8 MFMAs per
+ * iteration for `iters` iterations: 8 * iters * 4 * n_groups waves' worth of
+ * instructions, i.e. flops = 8 * iters * (4 * n_groups) * flops_per_instruction.
+ *   operands  device, bf16 bits, >= n_groups * 256 * 128 elements (read once)
+ *   sink      device, fp32, >= n_groups * 256 elements (written: keeps the
+ *             results live)
+ * n_groups >= 1, iters >= 1; an unknown shape or a non-positive count is
+ * STLITE_ERR_INVALID_ARG.  Enqueues on `stream` only.
+ */
+stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint16_t* operands, float* sink,
+                                int32_t n_groups, int32_t iters, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STLITE_PROBE_H */

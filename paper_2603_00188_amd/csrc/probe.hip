@@ -1,0 +1,64 @@
+// Matrix-core throughput probes (measurement only; see stlite_probe.h).
+#include "stlite_probe.h"
+#include "stlite_internal.h"
+
+namespace stlite {
+namespace {
+
+constexpr int kProbeThreads = 256;
+constexpr int kProbeElems = 128;  // bf16 operand elements per lane: 8 A + 8 B fragments of 8
+
+template <int SHAPE>
+__global__ __launch_bounds__(kProbeThreads, 2) void probe_mfma_kernel(const uint16_t* ops, float* sink,
+                                                                      int32_t iters) {
+  const size_t lane_id = size_t(blockIdx.x) * kProbeThreads + threadIdx.x;
+  const uint16_t* src = ops + lane_id * kProbeElems;
+  bf16x8_t a[8], b[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(src + 8 * i));
+    b[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(src + 64 + 8 * i));
+  }
+  float s = 0.0f;
+  if constexpr (SHAPE == 0) {
+    f32x4_t acc[4] = {};
+    for (int32_t it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[j & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b[7 - j], acc[j & 3], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s += acc[j][i];
+  } else {
+    f32x16_t acc[2] = {};
+    for (int32_t it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[j & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j], b[7 - j], acc[j & 1], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s += acc[j][i];
+  }
+  sink[lane_id] = s;
+}
+
+}  // namespace
+}  // namespace stlite
+
+extern "C" stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint16_t* operands, float* sink,
+                                           int32_t n_groups, int32_t iters, void* stream) {
+  using namespace stlite;
+  if ((shape != STLITE_PROBE_MFMA_16X16X32_BF16 && shape != STLITE_PROBE_MFMA_32X32X16_BF16) || !operands ||
+      !sink || n_groups < 1 || iters < 1)
+    return STLITE_ERR_INVALID_ARG;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (shape == STLITE_PROBE_MFMA_16X16X32_BF16)
+    hipLaunchKernelGGL(probe_mfma_kernel<0>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
+  else
+    hipLaunchKernelGGL(probe_mfma_kernel<1>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
+  return hipGetLastError() == hipSuccess ? STLITE_OK : STLITE_ERR_HIP;
+}

@@ -26,7 +26,7 @@ EXPORTS = (
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
-    "stlite_css_saliency_nbhd", "stlite_kept_overlap",
+    "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma",
 )
 
 
@@ -83,6 +83,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_tsg_fixed_gate": (st, [P, vp, f32, vp, vp]),
         "stlite_css_saliency_nbhd": (st, [P, ctypes.c_int32, vp, vp, vp]),
         "stlite_kept_overlap": (st, [P, vp, vp, vp, vp]),
+        "stlite_probe_mfma": (st, [st, vp, vp, ctypes.c_int32, ctypes.c_int32, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -277,6 +278,15 @@ class Buffers:
         self.ws_tsg = torch.empty(max(ws_tsg, 256), dtype=torch.uint8, device=device)
         # side streams at the default priority
         self.side = (torch.cuda.Stream(device=device), torch.cuda.Stream(device=device))
+
+
+PROBE_MFMA_16X16X32, PROBE_MFMA_32X32X16 = 0, 1
+PROBE_FLOPS = {PROBE_MFMA_16X16X32: 16 * 16 * 32 * 2, PROBE_MFMA_32X32X16: 32 * 32 * 16 * 2}
+
+
+def stlite_probe_mfma(shape: int, operands, sink, n_groups: int, iters: int, stream=None) -> None:
+    _check(load().stlite_probe_mfma(int(shape), _ptr(operands), _ptr(sink), int(n_groups), int(iters),
+                                    _stream(stream)), "stlite_probe_mfma")
 
 
 def decode_problem(p: Problem) -> Problem:

@@ -12,6 +12,8 @@ from paper_2603_00188_amd import stlite as S
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "stlite.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 
 pytestmark = pytest.mark.skipif(not os.path.exists(S.LIB_PATH), reason="libstlite.so not built")
 
@@ -19,9 +21,12 @@ FAKE_DEV = 0x100000  # never dereferenced: validation reads only the host mirror
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(stlite_[a-z_]+)\s*\(", src)))
+    """Every function any include/*.h declares."""
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(stlite_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_exports_match_header():
@@ -224,3 +229,13 @@ def test_kept_overlap_rejections():
     bad = good()
     bad.c.n_seqs = 0
     assert lib.stlite_kept_overlap(ctypes.byref(bad.c), FAKE_DEV, FAKE_DEV, FAKE_DEV, None) != S.OK
+
+
+def test_probe_rejections():
+    lib = S.load()
+    assert lib.stlite_probe_mfma(2, FAKE_DEV, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_mfma(0, None, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_mfma(1, FAKE_DEV, None, 1, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_mfma(0, FAKE_DEV, FAKE_DEV, 0, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_mfma(1, FAKE_DEV, FAKE_DEV, 4, 0, None) == S.ERR_INVALID_ARG
+
