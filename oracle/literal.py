@@ -218,3 +218,25 @@ def hit_rate(kept, oracle):
         if t in kept:
             hits += 1
     return hits / len(oracle)
+
+
+def compress_concat(Qs, Ks, frames, B, alpha=1.0):
+    """The procedure over a layer's concatenated key space.  Qs: per kv head
+    [G][delta][d]; Ks: per kv head [L][d].  A is the mean of the heads' window
+    sums; h_t is token t's keys of every head, one after the other."""
+    H, L = len(Ks), len(Ks[0])
+    A_h = [base_score(Qs[h], Ks[h]) for h in range(H)]
+    A = [sum(A_h[h][i] for h in range(H)) / H for i in range(L)]
+    K = []
+    for i in range(L):
+        row = []
+        for h in range(H):
+            row.extend(Ks[h][i])
+        K.append(row)
+    hist, cur, visual = partition(L, frames)
+    phi = css(K, frames)
+    r = rho(K, hist, cur)
+    g = gate(r, hist, L, B)
+    S = scores(A, phi, g, visual, alpha)
+    return dict(A=A, phi=phi, rho=r, gate=g, S=S, kept=top_b(S, B))
+

@@ -26,6 +26,8 @@ takes them:
                    phase that consumes K', V')
   cache_hit_rate   |I_keep cap I*| / |I*|, I* = Top_B of the first decode
                    query's attention over the full cache      (Eq. chr)
+  compress_layer_concat  the procedure over the layer's concatenated
+                   key space, one kept set per layer          (problem setup; R3b)
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -44,6 +46,9 @@ Readings where the paper is silent (each is also listed in the design notes):
   R-chr the attention of the first decode query that defines the oracle set
       is averaged over the kv head's query heads (as R2 does for A_base), so
       that I* and I_keep are sets of the same (layer, kv head) unit;
+  R3b the concatenated-head alternative to R3: h_t is token t's keys of all
+      kv heads concatenated (D = H_kv * d), A the mean over all the layer's
+      query heads, and one kept set per layer serves every kv head;
   R8b under the negative-L2 similarity, a squared distance <= 1e-5 ||k_i||^2
       is snapped to 0 (the same duplicate class);
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
@@ -426,3 +431,40 @@ def compress_sequence(q_bits, k_bits, v_bits, cu_seqlens, cu_frames, frame_meta,
     out["kept_abs"] = out["kept"] + a
     out["offset"] = a
     return out
+
+
+# ---------------------------------------------------------------------------
+# Concatenated-head key space (reading R3b): one kept set per layer
+# ---------------------------------------------------------------------------
+
+def compress_layer_concat(q_bits: np.ndarray, k_bits: np.ndarray, v_bits: np.ndarray,
+                          frames: Sequence[Tuple[int, int, int]], beta: Tuple[int, int],
+                          alpha: float = 1.0) -> Dict:
+    """The procedure with the layer's key space D = H_kv * d (problem setup:
+    K^(l) in R^{L x D} per layer) instead of one kv head's d; local indices.
+
+    q_bits [H_q, delta, d], k_bits / v_bits [H_kv, L, d] (bf16 bits) of one layer
+    and sequence.  h_t is the concatenation of token t's keys over the kv heads
+    (CSS and TSG cosines over D), A is the mean over all H_q query heads of the
+    single-head window sum (R2 over the whole layer), and the one kept set is
+    applied to every kv head's K and V.
+    """
+    H_kv, L, d = k_bits.shape
+    G = q_bits.shape[0] // H_kv
+    Q = bf16_to_f64(q_bits)
+    Kh = bf16_to_f64(k_bits)
+    K = np.concatenate([Kh[h] for h in range(H_kv)], axis=1)      # [L, H_kv * d]
+    B = budget(L, *beta)
+    A = np.mean([base_score(Q[h * G:(h + 1) * G], Kh[h]) for h in range(H_kv)], axis=0)
+    hist, cur, text = split_tokens(L, frames)
+    visual = np.zeros(L, dtype=bool)
+    visual[hist] = True
+    visual[cur] = True
+    phi = css_saliency(K, frames)
+    rho = tsg_rho(K, hist, cur)
+    gate, tau = tsg_gate(rho, hist, L, B)
+    S = integrate(A, phi, gate, visual, alpha)
+    kept = select_topk(S, B)
+    return dict(B=B, A=A, phi=phi, hist=hist, cur=cur, rho=rho, gate=gate, tau=tau, S=S, kept=kept,
+                k_out=k_bits[:, kept].copy(), v_out=v_bits[:, kept].copy(), visual=visual)
+

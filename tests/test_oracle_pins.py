@@ -714,3 +714,59 @@ def test_uniform_base_prior_closed_forms():
     S = O.integrate(A, phi, gate, visual, 1.0)
     # scores: 3 -> 0.75, 8 -> 0.35, the other visual and text tokens -> 0.25, token 7 -> 0
     assert O.select_topk(S, B).tolist() == [0, 1, 2, 3, 8]
+
+
+# ----------------------------------------------- concatenated-head key space ----
+
+def _concat_case(seed, H=2, G=2, delta=3, d=128):
+    rng = np.random.default_rng(200 + seed)
+    frames = [(0, 2, 3), (10, 2, 3), (20, 3, 2)]
+    L = 30
+    Kb = np.round(rng.standard_normal((H, L, d)) / math.sqrt(d) * 64) / 64.0   # exact in bf16
+    Kb[:, 2] = Kb[:, 21]           # a token equal to a current-frame token in every head (snap class)
+    Q = np.round(rng.standard_normal((H * G, delta, d)) * 8) / 64.0
+    to_bits = lambda x: (np.asarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return frames, L, to_bits(Q), to_bits(Kb), to_bits(rng.standard_normal((H, L, d)))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_concat_literal_twin(seed):
+    frames, L, qb, kb, vb = _concat_case(seed, H=[2, 4][seed], G=[2, 1][seed])
+    out = O.compress_layer_concat(qb, kb, vb, frames, (1, 4), 1.0)
+    Q, K = O.bf16_to_f64(qb), O.bf16_to_f64(kb)
+    H = K.shape[0]
+    G = Q.shape[0] // H
+    lit = O1.compress_concat([Q[h * G:(h + 1) * G].tolist() for h in range(H)], [K[h].tolist() for h in range(H)],
+                             frames, out["B"], 1.0)
+    np.testing.assert_allclose(out["A"], lit["A"], rtol=1e-12, atol=0)
+    np.testing.assert_allclose(out["phi"], lit["phi"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(out["rho"], [lit["rho"][int(i)] for i in out["hist"]], atol=1e-13)
+    assert out["gate"].tolist() == lit["gate"]
+    assert out["kept"].tolist() == lit["kept"]
+    assert out["rho"][list(out["hist"]).index(2)] == 1.0
+    assert (out["k_out"] == kb[:, out["kept"]]).all() and out["k_out"].shape == (H, out["B"], 128)
+
+
+def test_concat_one_head_is_the_per_head_procedure():
+    frames, L, qb, kb, vb = _concat_case(2, H=1, G=3)
+    cat = O.compress_layer_concat(qb, kb, vb, frames, (1, 4), 0.5)
+    one = O.compress_unit(qb, kb[0], vb[0], frames, (1, 4), 0.5)
+    for k in ("A", "phi", "rho", "S"):
+        np.testing.assert_array_equal(cat[k], one[k])
+    assert cat["kept"].tolist() == one["kept"].tolist() and cat["gate"].tolist() == one["gate"].tolist()
+
+
+def test_concat_identical_heads_match_one_head():
+    """Every kv head with the same keys and the same queries: the concatenated
+    cosines equal one head's, the mean A equals one head's A, and so the kept set
+    is the per-head one."""
+    frames, L, qb, kb, vb = _concat_case(3, H=1, G=2)
+    kb4 = np.repeat(kb, 4, axis=0)
+    qb4 = np.tile(qb, (4, 1, 1))
+    cat = O.compress_layer_concat(qb4, kb4, np.repeat(vb, 4, axis=0), frames, (1, 3), 1.0)
+    one = O.compress_unit(qb, kb[0], vb[0], frames, (1, 3), 1.0)
+    np.testing.assert_allclose(cat["A"], one["A"], rtol=1e-14)
+    np.testing.assert_allclose(cat["phi"], one["phi"], atol=1e-14)
+    np.testing.assert_allclose(cat["rho"], one["rho"], atol=1e-14)
+    assert cat["kept"].tolist() == one["kept"].tolist()
+
