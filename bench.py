@@ -246,6 +246,18 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
         e = roofline_entry({"bound": "hbm", "bytes": model["css_saliency"]["bytes"]}, ms)
         e["mfma_tflops"] = round(units * 2.0 * ((k * k - 1) // 2 + 1) * n_vis * w.head_dim / (ms * 1e-3) / 1e12, 2)
         entry[f"css_saliency_{k}x{k}"] = e
+    # the concatenated key space (one kept set per layer, D = 512)
+    if prob.n_kv_heads in (2, 4):
+        n_l = prob.n_layers
+        rho_l = torch.empty((n_l, prob.total_tokens), dtype=torch.float32, device="cuda")
+        phi_l = torch.empty_like(rho_l)
+        ws_c = torch.empty(max(prob.workspace_size(S.CALL_TSG_RHO_CONCAT), 256), dtype=torch.uint8, device="cuda")
+        ms = timed(lambda: S.stlite_tsg_rho_concat(prob, dk, rho_l, ws_c, stream))
+        entry["tsg_rho_concat"] = roofline_entry(model["tsg_rho"], ms)
+        ms = timed(lambda: S.stlite_css_saliency_concat(prob, dk, phi_l, stream))
+        entry["css_saliency_concat"] = roofline_entry(
+            {"bound": "hbm", "bytes": units * 2.0 * n_vis * w.head_dim + 4.0 * n_l * lay.total_tokens}, ms)
+        del rho_l, phi_l, ws_c
     log("variants: " + ", ".join(f"{n} {e['ms']:.3f} ms ({e['frac']:.2f})" for n, e in entry.items()))
     return entry
 

@@ -24,6 +24,8 @@
  *   stlite_tsg_similarity    rho under the dot product or -L2 (similarity ablation)
  *   stlite_tsg_fixed_gate    gate = 1[rho <= tau] for a fixed tau (necessity controls)
  *   stlite_css_saliency_nbhd CSS over 5x5, 7x7, 9x9 windows (neighbourhood ablation)
+ *   stlite_layer_mean, stlite_tsg_rho_concat, stlite_css_saliency_concat,
+ *   stlite_compact_kv_layer  the concatenated (per-layer) key space
  *
  * and, for the cache hit rate evaluation,
  *
@@ -99,7 +101,8 @@ typedef enum stlite_call {
   STLITE_CALL_TSG_THRESHOLD = 5,
   STLITE_CALL_TSG_RHO = 6,
   STLITE_CALL_DECODE_FULL = 7,    /* stlite_decode_attention on STLITE_CACHE_FULL */
-  STLITE_CALL_DECODE_COMPACT = 8  /* stlite_decode_attention on STLITE_CACHE_COMPACT */
+  STLITE_CALL_DECODE_COMPACT = 8, /* stlite_decode_attention on STLITE_CACHE_COMPACT */
+  STLITE_CALL_TSG_RHO_CONCAT = 9  /* stlite_tsg_rho_concat */
 } stlite_call;
 
 /* Which cache a decode call reads. */
@@ -309,6 +312,40 @@ stlite_status stlite_decode_attention(const stlite_problem* p, stlite_cache cach
                                       const uint16_t* q_dec, const uint16_t* k,
                                       const uint16_t* v, float* out, void* workspace,
                                       size_t workspace_bytes, void* stream);
+
+/*
+ * The concatenated key space (problem setup: the cache of a layer is
+ * K^(l) in R^{L x D}; here D = n_kv_heads * 128): token t's keys of every kv
+ * head, one after the other, form h_t; the cosines of CSS and TSG run over D;
+ * A is the mean over all of the layer's query heads; one kept set per layer
+ * serves every kv head.  Outputs are per layer, [n_layers][total_tokens] (fp32)
+ * or [n_layers][total_budget] (kept).  The threshold, gate and top-B steps are
+ * stlite_tsg_threshold and stlite_select_topk on a layer-level problem: the same
+ * layout and budgets with n_kv_heads = n_q_heads = 1.  Implemented for
+ * n_kv_heads = 2 or 4 (else STLITE_ERR_UNSUPPORTED).
+ */
+
+/* a_layer[l][t] = (1/n_kv_heads) sum_h a_base[l * n_kv_heads + h][t]: the mean over
+ * the layer's query heads, since each a_base row is its kv head's group mean. */
+stlite_status stlite_layer_mean(const stlite_problem* p, const float* a_base, float* a_layer,
+                                void* stream);
+
+/* rho over the concatenated keys (Sec. TSG with h in R^D): rho_layer [n_layers][L]
+ * gets the clamped, snapped maximum cosine on historical tokens and 0 elsewhere.
+ * Needs the workspace of STLITE_CALL_TSG_RHO_CONCAT. */
+stlite_status stlite_tsg_rho_concat(const stlite_problem* p, const uint16_t* k, float* rho_layer,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Phi over the concatenated keys (Eq. css_calc with h in R^D, 3 x 3 window):
+ * phi_layer [n_layers][L], 0 on text.  No workspace. */
+stlite_status stlite_css_saliency_concat(const stlite_problem* p, const uint16_t* k, float* phi_layer,
+                                         void* stream);
+
+/* Compaction with one kept set per layer: k_out[l * n_kv_heads + h][j] =
+ * k[l * n_kv_heads + h][kept_layer[l][j]], likewise v; exact row copies. */
+stlite_status stlite_compact_kv_layer(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                      const int32_t* kept_layer, uint16_t* k_out, uint16_t* v_out,
+                                      void* stream);
 
 /*
  * Cache hit rate numerator (Sec. cache hit rate evaluation, Eq. chr):

@@ -19,6 +19,7 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   const int sub = threadIdx.x >> 4, part = threadIdx.x & 15;
   const size_t ubase = size_t(unit) * lay.total_tokens;
   const size_t obase = size_t(unit) * lay.total_budget;
+  const size_t kbase = size_t(a.kept_per_layer ? unit / lay.n_kv_heads : unit) * lay.total_budget;
   // All of a thread's loads are issued before its stores, so that each lane
   // keeps 2 * kPer 16-byte reads in flight.
   int32_t tok[kPer];
@@ -27,7 +28,7 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   for (int r = 0; r < kPer; ++r) {
     const int64_t j = j0 + r * 16 + sub;
     row_ok[r] = j < lay.total_budget;
-    tok[r] = row_ok[r] ? a.kept[obase + j] : -1;
+    tok[r] = row_ok[r] ? a.kept[kbase + j] : -1;
   }
   // Loads are unconditional (an out-of-range index reads row 0 and is stored
   // as zeros), so that no branch forces a wait between them.

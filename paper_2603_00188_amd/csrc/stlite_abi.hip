@@ -315,6 +315,10 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
       // current-frame norms, plan
       *bytes = align_up(per_token * sizeof(float)) + plan_bytes(p, f);
       break;
+    case STLITE_CALL_TSG_RHO_CONCAT:
+      // current-frame norms per layer, plan
+      *bytes = align_up(size_t(p->n_layers) * p->total_tokens * sizeof(float)) + plan_bytes(p, f);
+      break;
     case STLITE_CALL_TSG_THRESHOLD:
       *bytes = plan_bytes(p, f) + seg_bytes(p, f, f.gate_chunks);
       break;
@@ -494,8 +498,77 @@ stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base, c
   return hip_status(launch_select(a, static_cast<hipStream_t>(stream)), "select_topk launch");
 }
 
+static stlite_status compact_common(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                    const int32_t* kept, int32_t per_layer, uint16_t* k_out, uint16_t* v_out,
+                                    void* stream);
+
 stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
                                 const int32_t* kept, uint16_t* k_out, uint16_t* v_out, void* stream) {
+  return compact_common(p, k, v, kept, 0, k_out, v_out, stream);
+}
+
+stlite_status stlite_compact_kv_layer(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                      const int32_t* kept_layer, uint16_t* k_out, uint16_t* v_out, void* stream) {
+  return compact_common(p, k, v, kept_layer, 1, k_out, v_out, stream);
+}
+
+stlite_status stlite_layer_mean(const stlite_problem* p, const float* a_base, float* a_layer, void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (!a_base || !a_layer) return fail(STLITE_ERR_INVALID_ARG, "a_base and a_layer must be non-NULL");
+  return hip_status(launch_layer_mean(a_base, a_layer, make_layout(p), static_cast<hipStream_t>(stream)),
+                    "layer_mean launch");
+}
+
+stlite_status stlite_tsg_rho_concat(const stlite_problem* p, const uint16_t* k, float* rho_layer, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  stlite_status st = check_ws(p, STLITE_CALL_TSG_RHO_CONCAT, ws, ws_bytes);
+  if (st != STLITE_OK) return st;
+  if (p->n_kv_heads != 2 && p->n_kv_heads != 4)
+    return fail(STLITE_ERR_UNSUPPORTED, "the concatenated key space is implemented for 2 or 4 kv heads (got %d)",
+                p->n_kv_heads);
+  if (!k || !rho_layer) return fail(STLITE_ERR_INVALID_ARG, "k and rho_layer must be non-NULL");
+  if (!aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "k must be 16-byte aligned");
+  const Facts f = derive(p);
+  char* w = static_cast<char*>(ws);
+  GateArgs g{};
+  g.lay = make_layout(p);
+  g.lay.n_units = p->n_layers;  // per-layer output: rho_layer is zero-filled over [n_layers][L]
+  g.lay.n_kv_heads = 1;
+  g.rho = rho_layer;
+  g.rho_zero_fill = rho_layer;
+  g.gate = nullptr;
+  const size_t slab = align_up(size_t(p->n_layers) * p->total_tokens * sizeof(float));
+  gate_carve(p, f, w + slab, false, g);
+  RhoArgs r = rho_args(p, f, k, rho_layer, reinterpret_cast<float*>(w), g);
+  r.lay = make_layout(p);
+  return hip_status(launch_tsg_rho_concat(r, g, static_cast<hipStream_t>(stream)), "tsg_rho_concat launch");
+}
+
+stlite_status stlite_css_saliency_concat(const stlite_problem* p, const uint16_t* k, float* phi_layer, void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (p->n_kv_heads != 2 && p->n_kv_heads != 4)
+    return fail(STLITE_ERR_UNSUPPORTED, "the concatenated key space is implemented for 2 or 4 kv heads (got %d)",
+                p->n_kv_heads);
+  if (!k || !phi_layer) return fail(STLITE_ERR_INVALID_ARG, "k and phi_layer must be non-NULL");
+  if (!aligned16(k)) return fail(STLITE_ERR_INVALID_ARG, "k must be 16-byte aligned");
+  CssArgs a;
+  a.lay = make_layout(p);
+  a.k = k;
+  a.phi = phi_layer;
+  int32_t strips = 1;
+  const int32_t rows = p->n_kv_heads >= 4 ? 1 : 2;  // output rows per wave tile (css_cat_kernel)
+  for (int32_t fi = 0; fi < p->n_frames; ++fi)      // wave tiles of the largest frame
+    strips = std::max<int32_t>(strips, ((p->h_frame_meta[3 * fi + 1] + rows - 1) / rows) *
+                                           ((p->h_frame_meta[3 * fi + 2] + 15) / 16));
+  a.strips = strips;
+  return hip_status(launch_css_concat(a, static_cast<hipStream_t>(stream)), "css_saliency_concat launch");
+}
+
+static stlite_status compact_common(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
+                                    const int32_t* kept, int32_t per_layer, uint16_t* k_out, uint16_t* v_out,
+                                    void* stream) {
   stlite_status st = stlite_validate(p);
   if (st != STLITE_OK) return st;
   if (p->total_budget == 0) return ok();
@@ -508,6 +581,7 @@ stlite_status stlite_compact_kv(const stlite_problem* p, const uint16_t* k, cons
   a.k = k;
   a.v = v;
   a.kept = kept;
+  a.kept_per_layer = per_layer;
   a.k_out = k_out;
   a.v_out = v_out;
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)), "compact_kv launch");

@@ -154,7 +154,8 @@ struct CompactArgs {
   Layout lay;
   const uint16_t* k;
   const uint16_t* v;
-  const int32_t* kept;
+  const int32_t* kept;   // [units][total_budget], or [n_layers][total_budget] with kept_per_layer
+  int32_t kept_per_layer;
   uint16_t* k_out;
   uint16_t* v_out;
 };
@@ -183,6 +184,13 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 // gate = 1[float32(rho) <= tau] on historical tokens, 1 elsewhere (g.gate, g.rho, g.lay).
 hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream);
+// TSG plan tables (historical-token table, rho blocks, gate segments) and the
+// fill of g.gate with 1 / g.rho_zero_fill with 0 over g.lay.n_units units.
+hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream);
+// Concatenated key space (D = n_kv_heads * 128; outputs [n_layers][total_tokens]).
+hipError_t launch_layer_mean(const float* a_base, float* a_layer, const Layout& lay, hipStream_t stream);
+hipError_t launch_tsg_rho_concat(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
+hipError_t launch_css_concat(const CssArgs& a, hipStream_t stream);
 // hits[u][s] = |kept_a cap kept_b| of sequence s in unit u.
 hipError_t launch_kept_overlap(const OverlapArgs& a, hipStream_t stream);
 hipError_t launch_css(const CssArgs& a, hipStream_t stream);

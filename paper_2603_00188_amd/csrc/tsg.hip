@@ -407,6 +407,8 @@ __global__ __launch_bounds__(256) void fixed_gate_kernel(GateArgs a, float tau) 
   for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.gate[base + off + j] = a.rho[base + off + j] <= tau ? 1 : 0;
 }
 
+}  // namespace
+
 hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
   hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs + g.lay.n_frames), dim3(256), 0, stream, g);
   hipError_t e = hipGetLastError();
@@ -416,6 +418,8 @@ hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
   hipLaunchKernelGGL(gate_fill_kernel, dim3(blocks), dim3(256), 0, stream, g, n);
   return hipGetLastError();
 }
+
+namespace {
 
 hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
   const SegSel& s = g.sel;

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstlite.s
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 (CALL_SCORE_WINDOW, CALL_TSG_GATE, CALL_CSS_SALIENCY, CALL_SELECT_TOPK, CALL_COMPACT_KV, CALL_TSG_THRESHOLD,
- CALL_TSG_RHO, CALL_DECODE_FULL, CALL_DECODE_COMPACT) = range(9)
+ CALL_TSG_RHO, CALL_DECODE_FULL, CALL_DECODE_COMPACT, CALL_TSG_RHO_CONCAT) = range(10)
 CACHE_FULL, CACHE_COMPACT = 0, 1
 SIM_COSINE, SIM_DOT, SIM_NEG_L2 = 0, 1, 2
 
@@ -27,6 +27,7 @@ EXPORTS = (
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
     "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma",
+    "stlite_layer_mean", "stlite_tsg_rho_concat", "stlite_css_saliency_concat", "stlite_compact_kv_layer",
 )
 
 
@@ -84,6 +85,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_css_saliency_nbhd": (st, [P, ctypes.c_int32, vp, vp, vp]),
         "stlite_kept_overlap": (st, [P, vp, vp, vp, vp]),
         "stlite_probe_mfma": (st, [st, vp, vp, ctypes.c_int32, ctypes.c_int32, vp]),
+        "stlite_layer_mean": (st, [P, vp, vp, vp]),
+        "stlite_tsg_rho_concat": (st, [P, vp, vp, vp, sz, vp]),
+        "stlite_css_saliency_concat": (st, [P, vp, vp, vp]),
+        "stlite_compact_kv_layer": (st, [P, vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -287,6 +292,62 @@ PROBE_FLOPS = {PROBE_MFMA_16X16X32: 16 * 16 * 32 * 2, PROBE_MFMA_32X32X16: 32 * 
 def stlite_probe_mfma(shape: int, operands, sink, n_groups: int, iters: int, stream=None) -> None:
     _check(load().stlite_probe_mfma(int(shape), _ptr(operands), _ptr(sink), int(n_groups), int(iters),
                                     _stream(stream)), "stlite_probe_mfma")
+
+
+def stlite_layer_mean(p: Problem, a_base, a_layer, stream=None) -> None:
+    _check(load().stlite_layer_mean(p.ref, _ptr(a_base), _ptr(a_layer), _stream(stream)), "stlite_layer_mean")
+
+
+def stlite_tsg_rho_concat(p: Problem, k, rho_layer, workspace, stream=None) -> None:
+    _check(load().stlite_tsg_rho_concat(p.ref, _ptr(k), _ptr(rho_layer), _ptr(workspace), _nbytes(workspace),
+                                        _stream(stream)), "stlite_tsg_rho_concat")
+
+
+def stlite_css_saliency_concat(p: Problem, k, phi_layer, stream=None) -> None:
+    _check(load().stlite_css_saliency_concat(p.ref, _ptr(k), _ptr(phi_layer), _stream(stream)),
+           "stlite_css_saliency_concat")
+
+
+def stlite_compact_kv_layer(p: Problem, k, v, kept_layer, k_out, v_out, stream=None) -> None:
+    _check(load().stlite_compact_kv_layer(p.ref, _ptr(k), _ptr(v), _ptr(kept_layer), _ptr(k_out), _ptr(v_out),
+                                          _stream(stream)), "stlite_compact_kv_layer")
+
+
+def layer_problem(p: Problem) -> Problem:
+    """The layer-level view of p for the concatenated key space: the same layout
+    and budgets, one unit per layer (n_kv_heads = n_q_heads = 1)."""
+    h = p.h
+    return Problem(p.n_layers, 1, 1, 1, h["cu_seqlens"], h["cu_frames"], h["frame_meta"], h["cu_budget"],
+                   device=p.d["cu_seqlens"].device)
+
+
+def compress_concat(p: Problem, pl: Problem, q_win, k, v, alpha: float = 1.0, stream=None) -> dict:
+    """The procedure over the concatenated key space, one kept set per layer
+    (pl = layer_problem(p)): window score per kv head, its layer mean, rho and
+    Phi over the concatenated keys, the rank gate and the top-B on the layer
+    view, and the compaction of every head with its layer's kept set.  Returns
+    the device tensors of every stage."""
+    import torch
+    dev = k.device
+    U, Lyr, L, Bt = p.units, p.n_layers, p.total_tokens, p.total_budget
+    f32 = dict(dtype=torch.float32, device=dev)
+    r = {"a_base": torch.empty((U, L), **f32), "a_layer": torch.empty((Lyr, L), **f32),
+         "rho": torch.empty((Lyr, L), **f32), "phi": torch.empty((Lyr, L), **f32),
+         "tau": torch.empty((Lyr, p.n_seqs), **f32), "gate": torch.empty((Lyr, L), dtype=torch.uint8, device=dev),
+         "kept": torch.empty((Lyr, max(Bt, 1)), dtype=torch.int32, device=dev),
+         "k_out": torch.empty((U, max(Bt, 1), 128), dtype=k.dtype, device=dev),
+         "v_out": torch.empty((U, max(Bt, 1), 128), dtype=v.dtype, device=dev)}
+    n = max(p.workspace_size(CALL_SCORE_WINDOW), p.workspace_size(CALL_TSG_RHO_CONCAT),
+            pl.workspace_size(CALL_TSG_THRESHOLD), pl.workspace_size(CALL_SELECT_TOPK), 256)
+    ws = torch.empty(n, dtype=torch.uint8, device=dev)
+    stlite_score_window(p, q_win, k, r["a_base"], ws, stream)
+    stlite_layer_mean(p, r["a_base"], r["a_layer"], stream)
+    stlite_tsg_rho_concat(p, k, r["rho"], ws, stream)
+    stlite_tsg_threshold(pl, r["rho"], r["tau"], r["gate"], ws, stream)
+    stlite_css_saliency_concat(p, k, r["phi"], stream)
+    stlite_select_topk(pl, r["a_layer"], r["phi"], r["gate"], alpha, r["kept"], None, ws, stream)
+    stlite_compact_kv_layer(p, k, v, r["kept"], r["k_out"], r["v_out"], stream)
+    return r
 
 
 def decode_problem(p: Problem) -> Problem:

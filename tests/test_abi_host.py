@@ -239,3 +239,21 @@ def test_probe_rejections():
     assert lib.stlite_probe_mfma(0, FAKE_DEV, FAKE_DEV, 0, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(1, FAKE_DEV, FAKE_DEV, 4, 0, None) == S.ERR_INVALID_ARG
 
+
+
+def test_concat_rejections_and_workspace():
+    lib = S.load()
+    p = good()   # 4 kv heads
+    ref = ctypes.byref(p.c)
+    n = ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(ref, S.CALL_TSG_RHO_CONCAT, ctypes.byref(n)) == S.OK and n.value > 0
+    assert lib.stlite_tsg_rho_concat(ref, FAKE_DEV, FAKE_DEV, FAKE_DEV, n.value - 1, None) == S.ERR_WORKSPACE
+    assert lib.stlite_tsg_rho_concat(ref, None, FAKE_DEV, FAKE_DEV, n.value, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_css_saliency_concat(ref, FAKE_DEV, None, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_layer_mean(ref, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    three = HostProblem([0, 72, 102], [[(0, 4, 5), (30, 4, 5)], []], [14, 6], n_q_heads=27, n_kv_heads=3)
+    r3 = ctypes.byref(three.c)
+    n3 = ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(r3, S.CALL_TSG_RHO_CONCAT, ctypes.byref(n3)) == S.OK
+    assert lib.stlite_tsg_rho_concat(r3, FAKE_DEV, FAKE_DEV, FAKE_DEV, n3.value, None) == S.ERR_UNSUPPORTED
+    assert lib.stlite_css_saliency_concat(r3, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
