@@ -323,6 +323,9 @@ __global__ __launch_bounds__(256) void css_cat_kernel(CssArgs a) {
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) ss[nb] += sumsq8(v[nb][kk]);
+      // The sums are formed here, not after the last head: otherwise every
+      // head's loaded keys stay live until then.
+      asm volatile("" : "+v"(ss[0]), "+v"(ss[1]));
 #pragma unroll
       for (int o = 0; o < kCssRows; ++o) {
         const int32_t ro = r0 + o;
