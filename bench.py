@@ -444,8 +444,8 @@ def main():
     stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
     dom = max(names, key=lambda n: per_call[n])
     kernel_of = {"score_window": "score_pass_kernel<1> + score_pass_kernel<2>",
-                 "tsg_rho": "rho_kernel", "tsg_threshold": "gate_keys/segsel/gate_emit kernels",
-                 "css_saliency": "css_kernel", "select_topk": "select_keys/segsel/select_emit kernels",
+                 "tsg_rho": "rho_kernel", "tsg_threshold": "gate_kernel",
+                 "css_saliency": "css_kernel", "select_topk": "select_kernel",
                  "compact_kv": "compact_kernel"}
     roof = dict(stages[dom])
     roof.pop("ms")

@@ -3,7 +3,7 @@
 //   S = A on text tokens, S = M * (A + alpha * Phi) on visual tokens,
 //   I_keep = the B tokens first in (S descending, index ascending) order,
 //   written in ascending token order.
-// The selection is the segmented radix select of segsel.h on the keys
+// The selection is the per-segment radix select of segsel.h on the keys
 // ~order_key(S) (ascending key = descending S).
 #include "segsel.h"
 #include "stlite_internal.h"
@@ -11,133 +11,110 @@
 namespace stlite {
 namespace {
 
-constexpr int kMaxChunkFrames = 64;
+template <bool LDS>
+struct SelectProd {
+  __amdgpu_buffer_rsrc_t a_base;  // the segment's A, Phi and gate (out-of-range lanes read 0)
+  __amdgpu_buffer_rsrc_t phi;
+  __amdgpu_buffer_rsrc_t gate;
+  bool has_phi, has_gate;
+  float* score;          // nullable: the segment's S
+  int32_t* kept;         // the segment's kept list
+  float alpha;
+  SeqFrames<LDS> fr;
+  bool classify;  // Phi or the gate is given: visual tokens must be told from text
 
-// Sequence table of the selection: n = L_s, k = B_s.
-__global__ __launch_bounds__(64) void select_plan_kernel(SelectArgs a) {
-  if (threadIdx.x != 0) return;
-  SeqInfo* info = a.info;
-  const Layout& lay = a.lay;
-  int32_t cb = 0;
-  for (int32_t q = 0; q < lay.n_seqs; ++q) {
-    const int32_t n = lay.cu_seqlens[q + 1] - lay.cu_seqlens[q];
-    info[q] = SeqInfo{n, lay.cu_budget[q + 1] - lay.cu_budget[q], cb, 0};
-    cb += (n + kSegChunk - 1) / kSegChunk;
-  }
-  info[lay.n_seqs] = SeqInfo{0, 0, cb, 0};
-}
+  __device__ int32_t cursor(const SelCtx& c, int32_t i) const { return classify ? fr.find(c.s0 + i) : -1; }
 
-// Does token `tok` (absolute) lie in one of the sequence's frames f0 .. f1-1?
-__device__ inline bool is_visual_search(const Layout& lay, int32_t f0, int32_t f1, int32_t tok) {
-  int32_t lo = f0, hi = f1 - 1, hit = -1;
-  while (lo <= hi) {  // last frame with offset <= tok
-    const int32_t mid = (lo + hi) >> 1;
-    if (lay.frame_meta[3 * mid] <= tok) { hit = mid; lo = mid + 1; } else { hi = mid - 1; }
-  }
-  return hit >= 0 && tok < lay.frame_meta[3 * hit] + lay.frame_meta[3 * hit + 1] * lay.frame_meta[3 * hit + 2];
-}
-
-// Scores, order keys and the level-0 histogram of one 4096-token chunk.
-__global__ __launch_bounds__(kSegThreads) void select_keys_kernel(SelectArgs a) {
-  const SegSel& s = a.sel;
-  __shared__ uint32_t lh[kSegBins];
-  __shared__ int32_t fr_lo[kMaxChunkFrames], fr_hi[kMaxChunkFrames];
-  __shared__ int32_t nfr;
-  const Layout& lay = a.lay;
-  const int unit = blockIdx.y;
-  const ChunkRef cr = seg_chunk(s, blockIdx.x);
-  const int32_t seq_start = lay.cu_seqlens[cr.seq];
-  const int32_t t_begin = seq_start + cr.begin, t_end = seq_start + cr.end;
-  const int32_t f0 = lay.cu_frames[cr.seq], f1 = lay.cu_frames[cr.seq + 1];
-  seg_hist_zero(lh);
-  if (threadIdx.x == 0) {
-    // frames overlapping [t_begin, t_end), in order; -1 if there are too many
-    int32_t lo = f0, hi = f1 - 1, first = f1;
-    while (lo <= hi) {  // first frame that ends after t_begin
-      const int32_t mid = (lo + hi) >> 1;
-      const int32_t end = lay.frame_meta[3 * mid] + lay.frame_meta[3 * mid + 1] * lay.frame_meta[3 * mid + 2];
-      if (end > t_begin) { first = mid; hi = mid - 1; } else { lo = mid + 1; }
-    }
-    int32_t n = 0;
-    for (int32_t f = first; f < f1 && lay.frame_meta[3 * f] < t_end; ++f) {
-      if (n == kMaxChunkFrames) { n = -1; break; }
-      fr_lo[n] = lay.frame_meta[3 * f];
-      fr_hi[n] = lay.frame_meta[3 * f] + lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
-      ++n;
-    }
-    nfr = n;
-  }
-  __syncthreads();
-  const int32_t n_fr = nfr;
-  const size_t ubase = size_t(unit) * lay.total_tokens;
-  uint32_t* keys = seg_keys(s, unit, cr.seq);
-#pragma unroll 4
-  for (int j = 0; j < kSegPer; ++j) {
-    const int32_t i = cr.begin + j * kSegThreads + threadIdx.x;
-    const bool in = i < cr.end;
-    uint32_t key = 0;
-    if (in) {
-      const int32_t tok = seq_start + i;
-      bool visual = false;
-      if (n_fr >= 0) {
-        for (int32_t f = 0; f < n_fr; ++f) visual |= (tok >= fr_lo[f]) & (tok < fr_hi[f]);
-      } else {
-        visual = is_visual_search(lay, f0, f1, tok);
-      }
-      const float A = a.a_base[ubase + tok];
-      float S = A;
-      if (visual) {
-        const float x = a.phi ? fmaf(a.alpha, a.phi[ubase + tok], A) : A;
-        S = (a.gate && a.gate[ubase + tok] == 0) ? 0.0f : x;
-      }
-      if (a.score) a.score[ubase + tok] = S;
-      key = ~order_key(S);
-      keys[i] = key;
-    }
-    seg_hist_add(lh, in, key >> 21);
-  }
-  __syncthreads();
-  seg_hist_flush(lh, seg_hist(s, unit, cr.seq, 0));
-}
-
-// Kept token indices, ascending, at cu_budget[seq] + rank.
-__global__ __launch_bounds__(kSegThreads) void select_emit_kernel(SelectArgs a) {
-  const SegSel& s = a.sel;
-  __shared__ int32_t scratch[kSegThreads / 64];
-  const Layout& lay = a.lay;
-  const int unit = blockIdx.y;
-  const ChunkRef cr = seg_chunk(s, blockIdx.x);
-  TakeChunk tc;
-  take_chunk(s, unit, cr, scratch, tc);
-  const int32_t seq_start = lay.cu_seqlens[cr.seq];
-  const int32_t kb = lay.cu_budget[cr.seq], B = lay.cu_budget[cr.seq + 1] - kb;
-  int32_t* kept = a.kept + size_t(unit) * lay.total_budget + kb;
-  const int32_t i0 = cr.begin + threadIdx.x * kSegPer;
+  __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
+                          uint32_t (&key)[kSelJ]) const {
+    bool vis[kSelJ];
 #pragma unroll
-  for (int i = 0; i < kSegPer; ++i)
-    if (tc.take[i] && tc.pos[i] < B) kept[tc.pos[i]] = seq_start + i0 + i;
+    for (int j = 0; j < kSelJ; ++j) vis[j] = false;
+    if (classify) {
+      const StepFrames st = step_frames(fr, cur, c.s0 + base, 64 * kSelJ);
+      const int u = st.n >= 0 ? st.uniform(c.s0 + base, 64 * kSelJ) : -1;
+      if (u >= 0) {
+#pragma unroll
+        for (int j = 0; j < kSelJ; ++j) vis[j] = u != kText;
+      } else if (st.n >= 0) {
+#pragma unroll
+        for (int j = 0; j < kSelJ; ++j) vis[j] = st.cls(c.s0 + base + 64 * j + lane) != kText;
+      } else {
+#pragma unroll
+        for (int j = 0; j < kSelJ; ++j) vis[j] = tok_class_search(fr, c.s0 + base + 64 * j + lane) != kText;
+      }
+    }
+    float A[kSelJ], ph[kSelJ];
+    uint32_t g[kSelJ];
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j) {
+      const int32_t i = base + 64 * j + lane;
+      A[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
+      ph[j] = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
+      g[j] = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j) {
+      const int32_t i = base + 64 * j + lane;
+      float S = A[j];
+      if (vis[j]) {
+        const float x = has_phi ? fmaf(alpha, ph[j], A[j]) : A[j];
+        S = g[j] == 0 ? 0.0f : x;
+      }
+      if (score && i < hi) score[i] = S;
+      key[j] = i < hi ? min(~order_key(S), kSelNever - 1u) : kSelNever;
+    }
+  }
+
+  __device__ void emit(const SelCtx& c, int32_t i, uint32_t, bool take, int32_t pos) const {
+    if (take && pos < c.k) kept[pos] = c.s0 + i;
+  }
+};
+
+template <bool LDS>
+__device__ inline SelectProd<LDS> select_prod(const SelectArgs& a, const SelCtx& c) {
+  SelectProd<LDS> p{};
+  const size_t seg0 = c.ubase + size_t(c.s0);
+  const int32_t n = c.n;
+  p.a_base = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.a_base) + seg0, 0, n * 4, kBufferFlags);
+  p.has_phi = a.phi != nullptr;
+  p.has_gate = a.gate != nullptr;
+  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0, n * 4, kBufferFlags);
+  p.gate = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.has_gate ? a.gate + seg0 : nullptr), 0,
+                                             p.has_gate ? n : 0, kBufferFlags);
+  p.score = a.score ? a.score + seg0 : nullptr;
+  p.kept = a.kept + size_t(blockIdx.z) * a.lay.total_budget + a.lay.cu_budget[c.seq];
+  p.alpha = a.alpha;
+  return p;
+}
+
+// Work-group (part, seq, unit): scores and keys of one part of a segment.
+// LDS: every sequence has at most kSelFrames frames (their ranges go to LDS).
+template <bool LDS>
+__global__ __launch_bounds__(kSelThreads) void select_produce_kernel(SelectArgs a) {
+  __shared__ SelShared sh;
+  SelCtx c = sel_ctx(a.lay);
+  c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  SelectProd<LDS> p = select_prod<LDS>(a, c);
+  p.classify = a.phi != nullptr || a.gate != nullptr;
+  p.fr = load_frames<LDS>(sh, a.lay, c.seq);
+  __syncthreads();
+  sel_produce(p, sh, a.sel, a.lay, c);
+}
+
+// Work-group (part, seq, unit): kept indices of one part of a segment.
+__global__ __launch_bounds__(kSelThreads) void select_emit_kernel(SelectArgs a) {
+  __shared__ SelShared sh;
+  SelCtx c = sel_ctx(a.lay);
+  const SelectProd<false> p = select_prod<false>(a, c);  // the emit pass reads keys only
+  sel_emit(p, sh, a.sel, a.lay, c);
 }
 
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
-  const SegSel& s = a.sel;
-  const int32_t U = a.lay.n_units;
-  hipLaunchKernelGGL(select_plan_kernel, dim3(1), dim3(64), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  e = launch_segsel_zero(s, U, stream);
-  if (e != hipSuccess) return e;
-  const dim3 chunk_grid(s.chunks_per_unit, U);
-  if (s.chunks_per_unit > 0) {
-    hipLaunchKernelGGL(select_keys_kernel, chunk_grid, dim3(kSegThreads), 0, stream, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  e = launch_segsel_middle(s, U, stream);
-  if (e != hipSuccess || s.chunks_per_unit == 0) return e;
-  hipLaunchKernelGGL(select_emit_kernel, chunk_grid, dim3(kSegThreads), 0, stream, a);
-  return hipGetLastError();
+  return launch_sel_passes(a.sel.lds_frames ? select_produce_kernel<true> : select_produce_kernel<false>,
+                           select_emit_kernel, a, a.sel, a.lay, stream);
 }
 
 }  // namespace stlite

@@ -41,8 +41,8 @@ struct Facts {
   int64_t max_cur;
   int32_t rows, rows_pad, blocks, waves, row_blocks, chunk;
   int64_t total_chunks;
-  int64_t sel_chunks;   // selection chunks per unit over all tokens (top-B)
-  int64_t gate_chunks;  // selection chunks per unit over historical tokens (gate)
+  int32_t sel_parts;    // parts per segment of the gate and top-B selections
+  int32_t max_seq_frames;
 };
 
 Facts derive(const stlite_problem* p) {
@@ -68,6 +68,7 @@ Facts derive(const stlite_problem* p) {
     f.max_seq = std::max(f.max_seq, L);
     f.total_chunks += ceil_div(L, f.chunk);
     const int32_t f0 = p->h_cu_frames[s], f1 = p->h_cu_frames[s + 1];
+    f.max_seq_frames = std::max(f.max_seq_frames, f1 - f0);
     int64_t hist = 0;
     for (int32_t fi = f0; fi < f1; ++fi) {
       const int64_t n = int64_t(p->h_frame_meta[3 * fi + 1]) * p->h_frame_meta[3 * fi + 2];
@@ -77,60 +78,59 @@ Facts derive(const stlite_problem* p) {
         f.max_cur = std::max(f.max_cur, n);
     }
     f.total_hist_blocks += ceil_div(hist, kRhoRows);
-    f.sel_chunks += ceil_div(L, kSegChunk);
-    f.gate_chunks += ceil_div(hist, kSegChunk);
   }
+  // Selection parts: aim for >= 512 work-groups over all segments, with
+  // parts of at least ~4096 tokens, at most 16.
+  const int64_t segs = std::max<int64_t>(f.units * p->n_seqs, 1);
+  int64_t parts = std::min(ceil_div(512, segs), std::max<int64_t>(ceil_div(f.max_seq, 4096), 1));
+  f.sel_parts = int32_t(std::min<int64_t>(std::max<int64_t>(parts, 1), 16));
   return f;
 }
 
-// Workspace of one segmented selection: keys, histograms, per-segment state,
-// per-chunk counts and offsets.
-size_t seg_bytes(const stlite_problem* p, const Facts& f, int64_t chunks) {
-  return align_up(size_t(f.units) * p->total_tokens * sizeof(uint32_t)) +
-         align_up(size_t(f.units) * p->n_seqs * 3 * 2048 * sizeof(uint32_t)) +
-         align_up(size_t(f.units) * p->n_seqs * sizeof(SegState)) +
-         align_up(size_t(f.units) * chunks * sizeof(SegCount)) +
-         align_up(size_t(f.units) * chunks * sizeof(SegOffset));
+// Workspace of one selection (gate or top-B): a row of 32-bit keys per unit
+// (every sequence's keys starting 16-byte aligned), the part histograms of the
+// three radix levels, the parts' counts below the level-1 prefix and the
+// per-segment state.
+size_t seg_bytes(const stlite_problem* p, const Facts& f) {
+  const size_t segparts = size_t(f.units) * p->n_seqs * f.sel_parts;
+  return align_up(size_t(f.units) * size_t(sel_key_stride(p->total_tokens, p->n_seqs)) * sizeof(uint32_t)) +
+         2 * align_up(segparts * (2048 + 64) * sizeof(uint32_t)) + align_up(segparts * (1024 + 32) * sizeof(uint32_t)) +
+         align_up(segparts * sizeof(int32_t)) + align_up(size_t(f.units) * p->n_seqs * 8 * sizeof(int32_t));
 }
 
-SegSel seg_carve(const stlite_problem* p, const Facts& f, int64_t chunks, const SeqInfo* info, char* w) {
-  SegSel s;
-  s.info = info;
-  s.cu_seqlens = p->cu_seqlens;
-  s.n_seqs = p->n_seqs;
-  s.chunks_per_unit = int32_t(chunks);
-  s.total_tokens = p->total_tokens;
+SelPlan sel_carve(const stlite_problem* p, const Facts& f, char* w) {
+  const size_t segparts = size_t(f.units) * p->n_seqs * f.sel_parts;
+  SelPlan s;
+  s.parts = f.sel_parts;
+  s.lds_frames = f.max_seq_frames <= kSelFrames ? 1 : 0;
   s.keys = reinterpret_cast<uint32_t*>(w);
-  w += align_up(size_t(f.units) * p->total_tokens * sizeof(uint32_t));
-  s.hist = reinterpret_cast<uint32_t*>(w);
-  w += align_up(size_t(f.units) * p->n_seqs * 3 * 2048 * sizeof(uint32_t));
-  s.state = reinterpret_cast<SegState*>(w);
-  w += align_up(size_t(f.units) * p->n_seqs * sizeof(SegState));
-  s.counts = reinterpret_cast<SegCount*>(w);
-  w += align_up(size_t(f.units) * chunks * sizeof(SegCount));
-  s.offsets = reinterpret_cast<SegOffset*>(w);
-  s.pivot_value = nullptr;
+  w += align_up(size_t(f.units) * size_t(sel_key_stride(p->total_tokens, p->n_seqs)) * sizeof(uint32_t));
+  s.hist0 = reinterpret_cast<uint32_t*>(w);
+  w += align_up(segparts * (2048 + 64) * sizeof(uint32_t));
+  s.hist1 = reinterpret_cast<uint32_t*>(w);
+  w += align_up(segparts * (2048 + 64) * sizeof(uint32_t));
+  s.hist2 = reinterpret_cast<uint32_t*>(w);
+  w += align_up(segparts * (1024 + 32) * sizeof(uint32_t));
+  s.below = reinterpret_cast<int32_t*>(w);
+  w += align_up(segparts * sizeof(int32_t));
+  s.state = reinterpret_cast<int32_t*>(w);
   return s;
 }
 
-size_t info_bytes(const stlite_problem* p) { return align_up(size_t(p->n_seqs + 1) * sizeof(SeqInfo)); }
-
-// TSG plan: historical-token table, rho block table, gate segment table.
+// TSG plan: historical-token table and rho block table.
 size_t plan_bytes(const stlite_problem* p, const Facts& f) {
   return align_up(size_t(p->total_tokens) * sizeof(int32_t)) +
-         align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock)) + info_bytes(p);
+         align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock));
 }
 
-// Carves the plan at w and, when `select` is set, the gate's selection after it.
+// Carves the plan at w and, when `select` is set, the gate's selection keys after it.
 void gate_carve(const stlite_problem* p, const Facts& f, char* w, bool select, GateArgs& g) {
   g.hist_tok = reinterpret_cast<int32_t*>(w);
   w += align_up(size_t(p->total_tokens) * sizeof(int32_t));
   g.blocks = reinterpret_cast<HistBlock*>(w);
   w += align_up(size_t(std::max<int64_t>(f.total_hist_blocks, 1)) * sizeof(HistBlock));
-  g.info = reinterpret_cast<SeqInfo*>(w);
-  w += info_bytes(p);
-  g.sel = seg_carve(p, f, f.gate_chunks, g.info, w);
-  if (!select) g.sel.keys = nullptr;
+  g.sel = select ? sel_carve(p, f, w) : SelPlan{};
+  g.tau = nullptr;
 }
 
 RhoArgs rho_args(const stlite_problem* p, const Facts& f, const uint16_t* k, float* rho, float* rn_cur,
@@ -258,6 +258,8 @@ stlite_status stlite_validate(const stlite_problem* p) {
   if (p->h_cu_budget[0] != 0) return fail(STLITE_ERR_INVALID_ARG, "cu_budget[0] must be 0");
   for (int s = 0; s < p->n_seqs; ++s) {
     const int64_t a = p->h_cu_seqlens[s], b = p->h_cu_seqlens[s + 1];
+    if (b - a > (int64_t(1) << 28))
+      return fail(STLITE_ERR_UNSUPPORTED, "sequence %d has %lld tokens; at most 2^28 are supported", s, (long long)(b - a));
     if (b - a < p->window)
       return fail(STLITE_ERR_INVALID_ARG, "sequence %d has %lld tokens, fewer than the window %d", s,
                   (long long)(b - a), p->window);
@@ -309,7 +311,7 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
       break;
     case STLITE_CALL_TSG_GATE:
       // rho scratch, current-frame norms, plan, selection
-      *bytes = 2 * align_up(per_token * sizeof(float)) + plan_bytes(p, f) + seg_bytes(p, f, f.gate_chunks);
+      *bytes = 2 * align_up(per_token * sizeof(float)) + plan_bytes(p, f) + seg_bytes(p, f);
       break;
     case STLITE_CALL_TSG_RHO:
       // current-frame norms, plan
@@ -320,10 +322,10 @@ stlite_status stlite_workspace_size(const stlite_problem* p, stlite_call call, s
       *bytes = align_up(size_t(p->n_layers) * p->total_tokens * sizeof(float)) + plan_bytes(p, f);
       break;
     case STLITE_CALL_TSG_THRESHOLD:
-      *bytes = plan_bytes(p, f) + seg_bytes(p, f, f.gate_chunks);
+      *bytes = plan_bytes(p, f) + seg_bytes(p, f);
       break;
     case STLITE_CALL_SELECT_TOPK:
-      *bytes = info_bytes(p) + seg_bytes(p, f, f.sel_chunks);
+      *bytes = seg_bytes(p, f);
       break;
     case STLITE_CALL_CSS_SALIENCY:
     case STLITE_CALL_COMPACT_KV:
@@ -413,7 +415,7 @@ stlite_status stlite_tsg_gate(const stlite_problem* p, const uint16_t* k, float*
   g.rho_zero_fill = rho;
   g.gate = gate;
   gate_carve(p, f, w + 2 * slab, true, g);
-  g.sel.pivot_value = tau;
+  g.tau = tau;
   const RhoArgs r = rho_args(p, f, k, const_cast<float*>(g.rho), reinterpret_cast<float*>(w + slab), g);
   return hip_status(launch_tsg_gate(r, g, static_cast<hipStream_t>(stream)), "tsg_gate launch");
 }
@@ -471,7 +473,7 @@ stlite_status stlite_tsg_threshold(const stlite_problem* p, const float* rho, fl
   g.rho_zero_fill = nullptr;
   g.gate = gate;
   gate_carve(p, f, static_cast<char*>(ws), true, g);
-  g.sel.pivot_value = tau;
+  g.tau = tau;
   return hip_status(launch_tsg_threshold(g, static_cast<hipStream_t>(stream)), "tsg_threshold launch");
 }
 
@@ -492,9 +494,7 @@ stlite_status stlite_select_topk(const stlite_problem* p, const float* a_base, c
   a.alpha = alpha;
   a.kept = kept;
   a.score = score;
-  const Facts f = derive(p);
-  a.info = static_cast<SeqInfo*>(ws);
-  a.sel = seg_carve(p, f, f.sel_chunks, a.info, static_cast<char*>(ws) + info_bytes(p));
+  a.sel = sel_carve(p, derive(p), static_cast<char*>(ws));
   return hip_status(launch_select(a, static_cast<hipStream_t>(stream)), "select_topk launch");
 }
 

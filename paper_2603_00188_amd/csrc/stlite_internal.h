@@ -47,46 +47,6 @@ struct ScoreArgs {
   int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
 };
 
-// Segmented k-smallest selection (segsel.h).  A segment is one (unit,
-// sequence) pair; its keys are cut into chunks of kSegChunk.
-constexpr int kSegChunk = 4096;
-
-struct SeqInfo {
-  int32_t n;            // keys in the segment (same for every unit)
-  int32_t k;            // keys to select
-  int32_t chunk_begin;  // first chunk of this sequence (chunks of all sequences of a unit are numbered together)
-  int32_t aux;          // producer-specific (first historical row of the sequence for the gate)
-};
-
-struct SegState {
-  uint32_t prefix, mask;
-  int32_t k_rem;        // rank still to find inside the current prefix; after level 2: keys == T to take
-  int32_t k;            // total selected
-};
-
-struct SegCount {
-  int32_t less, eq;
-};
-
-struct SegOffset {
-  int32_t out;          // selected keys in earlier chunks of the segment
-  int32_t eq_before;    // keys == T in earlier chunks of the segment
-};
-
-struct SegSel {
-  const SeqInfo* info;     // [n_seqs + 1]: entry n_seqs holds chunk_begin = chunks per unit
-  const int32_t* cu_seqlens;
-  int32_t n_seqs;
-  int32_t chunks_per_unit;
-  int64_t total_tokens;
-  uint32_t* keys;          // [units][total_tokens]
-  uint32_t* hist;          // [units][n_seqs][3][kSegBins]
-  SegState* state;         // [units][n_seqs]
-  SegCount* counts;        // [units][chunks_per_unit]
-  SegOffset* offsets;      // [units][chunks_per_unit]
-  float* pivot_value;      // nullable [units][n_seqs]: value of the k-th key, NaN when k = 0
-};
-
 // Historical rows per work-group of the rho contraction.
 constexpr int kRhoRows = 256;
 
@@ -112,6 +72,31 @@ struct RhoArgs {
   int32_t max_cur;       // largest current frame (tokens)
 };
 
+// Frames of one sequence that the selection kernels keep in LDS.
+constexpr int kSelFrames = 1024;
+
+// Workspace of one exact k-selection over (unit, sequence) segments, each cut
+// into `parts` parts (segsel.h).
+struct SelPlan {
+  uint32_t* keys;        // [units][sel_key_stride]: one key per token
+  uint32_t* hist0;       // [units][seqs][parts][2048 + 64]: level-0 part histograms (bins, 32-bin sums)
+  uint32_t* hist1;       // [units][seqs][parts][2048 + 64]: level 1
+  uint32_t* hist2;       // [units][seqs][parts][1024 + 32]: level 2
+  int32_t* below;        // [units][seqs][parts]: keys below the level-1 prefix
+  int32_t* state;        // [units][seqs][8]: k, then prefix and rank after levels 0 and 1
+  int32_t parts;         // 1 .. 16
+  int32_t lds_frames;    // 1: no sequence has more than kSelFrames frames
+};
+
+// Key rows of a selection: a row of sel_key_stride keys per unit; the keys of
+// sequence seq (first token s0) start at sel_key_base, a multiple of 4, and the
+// 16-byte group holding a sequence's last key stays inside the row and clear of
+// the next sequence.
+__host__ __device__ inline int64_t sel_key_stride(int64_t total_tokens, int32_t n_seqs) {
+  return ((total_tokens + 3) / 4) * 4 + 4 * int64_t(n_seqs);
+}
+__host__ __device__ inline int64_t sel_key_base(int32_t s0, int32_t seq) { return int64_t(s0 / 4) * 4 + 4 * int64_t(seq); }
+
 struct GateArgs {
   Layout lay;
   const float* rho;      // [units][L] (historical entries read)
@@ -119,8 +104,8 @@ struct GateArgs {
   uint8_t* gate;         // nullable for the rho-only call; [units][L]
   int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
   HistBlock* blocks;     // workspace [total_hist_blocks]
-  SeqInfo* info;         // workspace [n_seqs + 1]: segment table (n = N_hist, k = min(B, N_hist))
-  SegSel sel;            // keys in compact historical order; pivot_value = tau
+  SelPlan sel;           // workspace of the rank gate's selection
+  float* tau;            // nullable [units][seqs]: rho of the last admitted token, NaN when none is
 };
 
 struct CssArgs {
@@ -146,8 +131,7 @@ struct SelectArgs {
   float alpha;
   int32_t* kept;         // [units][total_budget]
   float* score;          // nullable [units][L]
-  SeqInfo* info;         // workspace [n_seqs + 1]: segment table (n = L_s, k = B_s)
-  SegSel sel;
+  SelPlan sel;           // workspace of the top-B selection
 };
 
 struct CompactArgs {

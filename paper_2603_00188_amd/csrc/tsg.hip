@@ -45,29 +45,22 @@ __device__ inline int32_t hist_count(const Layout& lay, int32_t s) {
 }
 
 // Plan of the TSG pass.  Work-groups 0 .. n_seqs-1: per sequence, the 256-row
-// block descriptors of the rho GEMM and the gate's selection segment
-// (n = N_hist, k = min(B, N_hist)).  Work-groups n_seqs + f: the historical
+// block descriptors of the rho GEMM.  Work-groups n_seqs + f: the historical
 // token table entries of frame f (frames in order, row-major inside a frame),
 // unless f is its sequence's current frame.
 __global__ __launch_bounds__(256) void tsg_plan_kernel(GateArgs a) {
   const Layout& lay = a.lay;
   if (int32_t(blockIdx.x) < lay.n_seqs) {
     const int s = blockIdx.x;
-    int32_t hist_base = 0, blk_base = 0, chunk_base = 0;
+    int32_t hist_base = 0, blk_base = 0;
     for (int32_t t = 0; t < s; ++t) {
       const int32_t n = hist_count(lay, t);
       hist_base += n;
       blk_base += (n + kRhoRows - 1) / kRhoRows;
-      chunk_base += (n + kSegChunk - 1) / kSegChunk;
     }
     const int32_t n_hist = hist_count(lay, s);
     const int32_t nb = (n_hist + kRhoRows - 1) / kRhoRows;
     for (int32_t b = threadIdx.x; b < nb; b += blockDim.x) a.blocks[blk_base + b] = HistBlock{s, b, n_hist, hist_base};
-    if (threadIdx.x == 0) {
-      const int32_t B = lay.cu_budget[s + 1] - lay.cu_budget[s];
-      a.info[s] = SeqInfo{n_hist, min(B, n_hist), chunk_base, hist_base};
-      if (s == lay.n_seqs - 1) a.info[s + 1] = SeqInfo{0, 0, chunk_base + (n_hist + kSegChunk - 1) / kSegChunk, 0};
-    }
     return;
   }
   const int32_t f = int32_t(blockIdx.x) - lay.n_seqs;
@@ -348,47 +341,89 @@ __global__ __launch_bounds__(256, 2) void rho_kernel(RhoArgs a) {
     }
 }
 
-// Gate keys (rho ascending) of one 4096-row chunk of a sequence's historical
-// tokens, in compact order, and the level-0 histogram.
-__global__ __launch_bounds__(kSegThreads) void gate_keys_kernel(GateArgs a) {
-  __shared__ uint32_t lh[kSegBins];
-  const SegSel& s = a.sel;
-  const int unit = blockIdx.y;
-  const ChunkRef cr = seg_chunk(s, blockIdx.x);
-  const int32_t* htok = a.hist_tok + s.info[cr.seq].aux;
-  const float* rho = a.rho + size_t(unit) * a.lay.total_tokens;
-  uint32_t* keys = seg_keys(s, unit, cr.seq);
-  seg_hist_zero(lh);
-  __syncthreads();
-#pragma unroll 4
-  for (int j = 0; j < kSegPer; ++j) {
-    const int32_t i = cr.begin + j * kSegThreads + threadIdx.x;
-    const bool in = i < cr.end;
-    uint32_t key = 0;
-    if (in) {
-      key = order_key(rho[htok[i]]);
-      keys[i] = key;
+// Rank gate of one (sequence, unit) segment: the keys are order_key(rho) on
+// historical tokens (a NaN rho is kept below the never-selected key) and
+// kSelNever elsewhere; k = m = min(B, N_hist).  Every gate byte of the
+// sequence is written: 1 on text and the current frame, 1 on the m admitted
+// historical tokens and 0 on the others.
+template <bool LDS>
+struct GateProd {
+  __amdgpu_buffer_rsrc_t rho;   // the segment's rho (out-of-range lanes read 0)
+  __amdgpu_buffer_rsrc_t gate;  // the segment's gate bytes
+  SeqFrames<LDS> fr;
+
+  __device__ int32_t cursor(const SelCtx& c, int32_t i) const { return fr.find(c.s0 + i); }
+
+  __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
+                          uint32_t (&key)[kSelJ]) const {
+    bool hist[kSelJ];
+    const StepFrames st = step_frames(fr, cur, c.s0 + base, 64 * kSelJ);
+    const int u = st.n >= 0 ? st.uniform(c.s0 + base, 64 * kSelJ) : -1;
+    if (u >= 0) {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = u == kHist;
+    } else if (st.n >= 0) {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = st.cls(c.s0 + base + 64 * j + lane) == kHist;
+    } else {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = tok_class_search(fr, c.s0 + base + 64 * j + lane) == kHist;
     }
-    seg_hist_add(lh, in, key >> 21);
+    float r[kSelJ];
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j)
+      r[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, (base + 64 * j + lane) * 4, 0, 0));
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j) {
+      const bool h = hist[j] && base + 64 * j + lane < hi;
+      key[j] = h ? min(order_key(r[j]), kSelNever - 1u) : kSelNever;
+    }
   }
-  __syncthreads();
-  seg_hist_flush(lh, seg_hist(s, unit, cr.seq, 0));
+
+  __device__ void emit(const SelCtx&, int32_t i, uint32_t key, bool take, int32_t) const {
+    __builtin_amdgcn_raw_buffer_store_b8(uint8_t((key == kSelNever || take) ? 1 : 0), gate, i, 0, 0);
+  }
+};
+
+__device__ inline void gate_buffers(const GateArgs& a, const SelCtx& c, __amdgpu_buffer_rsrc_t& rho,
+                                    __amdgpu_buffer_rsrc_t& gate) {
+  const size_t seg0 = c.ubase + size_t(c.s0);
+  rho = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.rho) + seg0, 0, c.n * 4, kBufferFlags);
+  gate = __builtin_amdgcn_make_buffer_rsrc(a.gate + seg0, 0, c.n, kBufferFlags);
 }
 
-// gate = 1 for the selected historical tokens, 0 for the others.
-__global__ __launch_bounds__(kSegThreads) void gate_emit_kernel(GateArgs a) {
-  __shared__ int32_t scratch[kSegThreads / 64];
-  const SegSel& s = a.sel;
-  const int unit = blockIdx.y;
-  const ChunkRef cr = seg_chunk(s, blockIdx.x);
-  TakeChunk tc;
-  take_chunk(s, unit, cr, scratch, tc);
-  const int32_t* htok = a.hist_tok + s.info[cr.seq].aux;
-  uint8_t* gate = a.gate + size_t(unit) * a.lay.total_tokens;
-  const int32_t i0 = cr.begin + threadIdx.x * kSegPer;
-#pragma unroll
-  for (int i = 0; i < kSegPer; ++i)
-    if (i0 + i < cr.end) gate[htok[i0 + i]] = tc.take[i] ? 1 : 0;
+// Work-group (part, seq, unit): keys of one part of a segment; k = min(B, N_hist).
+// LDS: every sequence has at most kSelFrames frames (their ranges go to LDS).
+template <bool LDS>
+__global__ __launch_bounds__(kSelThreads) void gate_produce_kernel(GateArgs a) {
+  __shared__ SelShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c = sel_ctx(lay);
+  GateProd<LDS> p{};
+  gate_buffers(a, c, p.rho, p.gate);
+  p.fr = load_frames<LDS>(sh, lay, c.seq);
+  int32_t nh = 0;  // N_hist: every frame of the sequence but the last
+  for (int32_t f = threadIdx.x; f + 1 < p.fr.nf; f += kSelThreads) nh += frame_size(lay, p.fr.f0 + f);
+  nh = wave_sum(nh);
+  if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = nh;
+  __syncthreads();
+  int32_t n_hist = 0;
+  for (int w = 0; w < kSelWaves; ++w) n_hist += sh.red[w];
+  c.k = min(lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq], n_hist);
+  sel_produce(p, sh, a.sel, lay, c);
+}
+
+// Work-group (part, seq, unit): gate bytes of one part of a segment; part 0
+// writes tau.
+__global__ __launch_bounds__(kSelThreads) void gate_emit_kernel(GateArgs a) {
+  __shared__ SelShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c = sel_ctx(lay);
+  GateProd<false> p{};  // the emit pass reads keys only
+  gate_buffers(a, c, p.rho, p.gate);
+  const uint32_t T = sel_emit(p, sh, a.sel, lay, c);
+  if (a.tau && c.part == 0 && threadIdx.x == 0)
+    a.tau[size_t(blockIdx.z) * lay.n_seqs + c.seq] = c.k > 0 ? order_key_value(T) : __builtin_nanf("");
 }
 
 // Fixed-threshold gate of frame blockIdx.x in unit blockIdx.y: every token of a
@@ -422,29 +457,13 @@ hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
 namespace {
 
 hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
-  const SegSel& s = g.sel;
-  const int32_t U = g.lay.n_units;
-  hipError_t e = launch_segsel_zero(s, U, stream);
-  if (e != hipSuccess) return e;
-  const dim3 chunk_grid(s.chunks_per_unit, U);
-  if (s.chunks_per_unit > 0) {
-    hipLaunchKernelGGL(gate_keys_kernel, chunk_grid, dim3(kSegThreads), 0, stream, g);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  e = launch_segsel_middle(s, U, stream);
-  if (e != hipSuccess || s.chunks_per_unit == 0) return e;
-  hipLaunchKernelGGL(gate_emit_kernel, chunk_grid, dim3(kSegThreads), 0, stream, g);
-  return hipGetLastError();
+  return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
+                           gate_emit_kernel, g, g.sel, g.lay, stream);
 }
 
 }  // namespace
 
-hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) {
-  hipError_t e = launch_gate_prologue(g, stream);
-  if (e != hipSuccess) return e;
-  return launch_gate_select(g, stream);
-}
+hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream) { return launch_gate_select(g, stream); }
 
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
   hipError_t e = launch_gate_prologue(g, stream);
@@ -480,7 +499,9 @@ hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t strea
 }
 
 hipError_t launch_tsg_gate(const RhoArgs& r, const GateArgs& g, hipStream_t stream) {
-  hipError_t e = launch_tsg_rho(r, g, stream);
+  GateArgs pro = g;
+  pro.gate = nullptr;  // the gate kernel writes every gate byte itself
+  hipError_t e = launch_tsg_rho(r, pro, stream);
   if (e != hipSuccess) return e;
   return launch_gate_select(g, stream);
 }
