@@ -173,6 +173,59 @@ def test_stage_threshold_and_select_exact(torch_cuda):
         assert (kept[u, cb[s]:cb[s + 1]] == want).all(), (u, s)
 
 
+def test_stage_exact_many_parts_and_ties(torch_cuda):
+    """Stage-isolated on sequences long enough that the gate's and the top-B's
+    selections are cut into several parts per segment, with inputs drawn from
+    a few values so that long runs of equal keys straddle part and wave
+    boundaries: gate, tau and kept lists must equal the oracle's exactly."""
+    import torch
+    from oracle import stlite_oracle as O
+    from paper_2603_00188_amd import stlite as S
+    # two sequences: 13 frames of 40 x 50 patches + 100 text, and 5 frames of 30 x 37 + 77 text
+    seqs, metas, cu = [], [], [0]
+    for nf, (r, c), nt in ((13, (40, 50), 100), (5, (30, 37), 77)):
+        off = cu[-1]
+        fm = []
+        for _ in range(nf):
+            fm.append((off, r, c))
+            off += r * c + nt
+        metas.append(fm)
+        cu.append(off)
+    cu_seqlens = np.array(cu, np.int32)
+    cu_frames = np.array([0, len(metas[0]), len(metas[0]) + len(metas[1])], np.int32)
+    frame_meta = np.array(metas[0] + metas[1], np.int32)
+    n_layers, hkv = 1, 2
+    for beta in ((1, 5), (1, 2)):
+        cu_budget = S.budgets(cu_seqlens, *beta)
+        prob = S.Problem(n_layers, hkv, hkv, 8, cu_seqlens, cu_frames, frame_meta, cu_budget)
+        U, L = prob.units, prob.total_tokens
+        rng = np.random.default_rng(5)
+        rho = rng.choice(np.float32([0.1, 0.25, 0.5, 0.75, 1.0]), size=(U, L)).astype(np.float32)
+        A = rng.choice(np.float32([1e-4, 2e-4, 5e-4]), size=(U, L)).astype(np.float32)
+        phi = rng.choice(np.float32([0.9, 1.0, 1.1]), size=(U, L)).astype(np.float32)
+        out = S.Buffers(prob)
+        dev = lambda x: torch.from_numpy(x).cuda()
+        S.stlite_tsg_threshold(prob, dev(rho), out.tau, out.gate, out.ws_tsg)
+        S.stlite_select_topk(prob, dev(A), dev(phi), out.gate, 1.0, out.kept, out.score, out.ws)
+        torch.cuda.synchronize()
+        gate, tau, kept = out.gate.cpu().numpy(), out.tau.cpu().numpy(), out.kept.cpu().numpy()
+        for u in range(U):
+            for s in range(2):
+                a, b = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
+                fm = metas[s]
+                vis = np.zeros(b - a, bool)
+                for off, r, c in fm:
+                    vis[off - a:off - a + r * c] = True
+                hist = np.concatenate([np.arange(off - a, off - a + r * c) for off, r, c in fm[:-1]])
+                B = int(cu_budget[s + 1] - cu_budget[s])
+                g_ref, tau_ref = O.tsg_gate(rho[u, a:b][hist].astype(np.float64), hist, b - a, B)
+                assert (gate[u, a:b] == g_ref).all(), (beta, u, s)
+                assert np.float32(tau[u, s]) == np.float32(tau_ref), (beta, u, s)
+                s32 = np.where(vis, np.where(g_ref > 0, A[u, a:b] + phi[u, a:b], np.float32(0)), A[u, a:b])
+                want = O.select_topk(s32.astype(np.float64), B) + a
+                assert (kept[u, cu_budget[s]:cu_budget[s + 1]] == want).all(), (beta, u, s)
+
+
 def test_split_tsg_matches_fused(torch_cuda):
     """stlite_tsg_rho followed by stlite_tsg_threshold reproduces stlite_tsg_gate
     bit for bit (rho, gate and tau)."""
