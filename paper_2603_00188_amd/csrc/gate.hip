@@ -1,0 +1,108 @@
+// Rank form of the TSG gate (Eqs. budget_threshold and temporal_mask of the
+// paper): per (sequence, unit), m = min(B, N_hist) historical tokens are
+// admitted, those first in (rho ascending, index ascending) order; tau_red is
+// the rho of the last one admitted.  The selection is the exact k-selection of
+// segsel.h over the keys order_key(rho).
+#include "segsel.h"
+#include "stlite_internal.h"
+
+namespace stlite {
+namespace {
+
+__device__ inline int32_t frame_size(const Layout& lay, int32_t f) {
+  return lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
+}
+
+// Rank gate of one (sequence, unit) segment: the keys are order_key(rho) on
+// historical tokens (a NaN rho is kept below the never-selected key) and
+// kSelNever elsewhere; k = m = min(B, N_hist).  Every gate byte of the
+// sequence is written: 1 on text and the current frame, 1 on the m admitted
+// historical tokens and 0 on the others.
+template <bool LDS>
+struct GateProd {
+  __amdgpu_buffer_rsrc_t rho;   // the segment's rho (out-of-range lanes read 0)
+  __amdgpu_buffer_rsrc_t gate;  // the segment's gate bytes
+  SeqFrames<LDS> fr;
+
+  __device__ int32_t cursor(const SelCtx& c, int32_t i) const { return __builtin_amdgcn_readfirstlane(fr.find(c.s0 + i)); }
+
+  __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
+                          uint32_t (&key)[kSelJ]) const {
+    bool hist[kSelJ];
+    const StepFrames st = step_frames(fr, cur, c.s0 + base, 64 * kSelJ);
+    const int u = st.n >= 0 ? st.uniform(c.s0 + base, 64 * kSelJ) : -1;
+    if (u >= 0) {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = u == kHist;
+    } else if (st.n >= 0) {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = st.cls(c.s0 + base + 64 * j + lane) == kHist;
+    } else {
+#pragma unroll
+      for (int j = 0; j < kSelJ; ++j) hist[j] = tok_class_search(fr, c.s0 + base + 64 * j + lane) == kHist;
+    }
+    float r[kSelJ];
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j)
+      r[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, (base + 64 * j + lane) * 4, 0, 0));
+#pragma unroll
+    for (int j = 0; j < kSelJ; ++j) {
+      const bool h = hist[j] && base + 64 * j + lane < hi;
+      key[j] = h ? min(order_key(r[j]), kSelNever - 1u) : kSelNever;
+    }
+  }
+
+  __device__ void emit(const SelCtx&, int32_t i, uint32_t key, bool take, int32_t) const {
+    __builtin_amdgcn_raw_buffer_store_b8(uint8_t((key == kSelNever || take) ? 1 : 0), gate, i, 0, 0);
+  }
+};
+
+__device__ inline void gate_buffers(const GateArgs& a, const SelCtx& c, __amdgpu_buffer_rsrc_t& rho,
+                                    __amdgpu_buffer_rsrc_t& gate) {
+  const size_t seg0 = c.ubase + size_t(c.s0);
+  rho = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.rho) + seg0, 0, c.n * 4, kBufferFlags);
+  gate = __builtin_amdgcn_make_buffer_rsrc(a.gate + seg0, 0, c.n, kBufferFlags);
+}
+
+// Work-group (part, seq, unit): keys of one part of a segment; k = min(B, N_hist).
+// LDS: every sequence has at most kSelFrames frames (their ranges go to LDS).
+template <bool LDS>
+__global__ __launch_bounds__(kSelThreads) void gate_produce_kernel(GateArgs a) {
+  __shared__ SelShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c = sel_ctx(lay);
+  GateProd<LDS> p{};
+  gate_buffers(a, c, p.rho, p.gate);
+  p.fr = load_frames<LDS>(sh, lay, c.seq);
+  int32_t nh = 0;  // N_hist: every frame of the sequence but the last
+  for (int32_t f = threadIdx.x; f + 1 < p.fr.nf; f += kSelThreads) nh += frame_size(lay, p.fr.f0 + f);
+  nh = wave_sum(nh);
+  if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = nh;
+  __syncthreads();
+  int32_t n_hist = 0;
+  for (int w = 0; w < kSelWaves; ++w) n_hist += sh.red[w];
+  c.k = min(lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq], n_hist);
+  sel_produce(p, sh, a.sel, lay, c);
+}
+
+// Work-group (part, seq, unit): gate bytes of one part of a segment; part 0
+// writes tau.
+__global__ __launch_bounds__(kSelThreads) void gate_emit_kernel(GateArgs a) {
+  __shared__ SelShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c = sel_ctx(lay);
+  GateProd<false> p{};  // the emit pass reads keys only
+  gate_buffers(a, c, p.rho, p.gate);
+  const uint32_t T = sel_emit(p, sh, a.sel, lay, c);
+  if (a.tau && c.part == 0 && threadIdx.x == 0)
+    a.tau[size_t(blockIdx.z) * lay.n_seqs + c.seq] = c.k > 0 ? order_key_value(T) : __builtin_nanf("");
+}
+
+}  // namespace
+
+hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
+  return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
+                           gate_emit_kernel, g, g.sel, g.lay, stream);
+}
+
+}  // namespace stlite

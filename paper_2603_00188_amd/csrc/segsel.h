@@ -56,8 +56,10 @@ __device__ inline SelPart sel_part(int32_t n, int32_t parts, int32_t p) {
   r.pa = min(p * plen, n);
   r.pb = min(r.pa + plen, n);
   const int32_t wlen = ((r.pb - r.pa + kSelWaves * 256 - 1) / (kSelWaves * 256)) * 256;
-  r.lo = min(r.pa + int32_t(threadIdx.x >> 6) * wlen, r.pb);
-  r.hi = min(r.lo + wlen, r.pb);
+  // the wave's range is wave-uniform: keep it in scalar registers so that the
+  // loops over it branch on scalars
+  r.lo = __builtin_amdgcn_readfirstlane(min(r.pa + int32_t(threadIdx.x >> 6) * wlen, r.pb));
+  r.hi = __builtin_amdgcn_readfirstlane(min(r.lo + wlen, r.pb));
   return r;
 }
 
@@ -138,19 +140,26 @@ struct StepFrames {
   }
 };
 
+// Every value here is wave-uniform (readfirstlane keeps it in scalar
+// registers, so the loops branch on scalars).
 template <bool LDS>
 __device__ __forceinline__ StepFrames step_frames(const SeqFrames<LDS>& fr, int32_t& cur, int32_t base, int32_t span) {
-  while (cur + 1 < fr.nf && fr.start(cur + 1) <= base) ++cur;
+  auto uni = [](int32_t x) { return __builtin_amdgcn_readfirstlane(x); };
+  base = uni(base);
+  cur = uni(cur);
+  while (cur + 1 < fr.nf && uni(fr.start(cur + 1)) <= base) ++cur;
   StepFrames st;
   st.n = 0;
-  int32_t f = (cur >= 0 && fr.end(cur) > base) ? cur : cur + 1;
-  for (; f < fr.nf && fr.start(f) < base + span; ++f) {
+  int32_t f = (cur >= 0 && uni(fr.end(cur)) > base) ? cur : cur + 1;
+  for (; f < fr.nf; ++f) {
+    const int32_t s = uni(fr.start(f));
+    if (s >= base + span) break;
     if (st.n == kStepFrames) {
       st.n = -1;
       break;
     }
-    st.s[st.n] = fr.start(f);
-    st.e[st.n] = fr.end(f);
+    st.s[st.n] = s;
+    st.e[st.n] = uni(fr.end(f));
     st.last[st.n] = f == fr.nf - 1;
     ++st.n;
   }

@@ -23,7 +23,9 @@ struct SelectProd {
   SeqFrames<LDS> fr;
   bool classify;  // Phi or the gate is given: visual tokens must be told from text
 
-  __device__ int32_t cursor(const SelCtx& c, int32_t i) const { return classify ? fr.find(c.s0 + i) : -1; }
+  __device__ int32_t cursor(const SelCtx& c, int32_t i) const {
+    return classify ? __builtin_amdgcn_readfirstlane(fr.find(c.s0 + i)) : -1;
+  }
 
   __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
                           uint32_t (&key)[kSelJ]) const {

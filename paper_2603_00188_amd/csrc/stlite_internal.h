@@ -168,7 +168,9 @@ hipError_t launch_tsg_threshold(const GateArgs& g, hipStream_t stream);
 hipError_t launch_tsg_rho(const RhoArgs& r, const GateArgs& g, hipStream_t stream);
 // gate = 1[float32(rho) <= tau] on historical tokens, 1 elsewhere (g.gate, g.rho, g.lay).
 hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t stream);
-// TSG plan tables (historical-token table, rho blocks, gate segments) and the
+// Rank gate and tau_red from g.rho (the exact selection of segsel.h).
+hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream);
+// TSG plan tables (historical-token table, rho blocks) and the
 // fill of g.gate with 1 / g.rho_zero_fill with 0 over g.lay.n_units units.
 hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream);
 // Concatenated key space (D = n_kv_heads * 128; outputs [n_layers][total_tokens]).
