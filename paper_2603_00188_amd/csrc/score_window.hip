@@ -18,6 +18,8 @@
 // shared by all waves.  Every exponential and sum of one key block is issued
 // between the MFMAs of the other, in an order fixed in the source: the long
 // 32x32 MFMAs hide that vector work, which the short 16x16 forms cannot.
+#include <algorithm>
+
 #include "stlite_internal.h"
 #include "tile_lds.h"
 
@@ -397,9 +399,13 @@ __global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_rowstats_exa
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems];
   __shared__ int32_t lim_s[NW * RB * 32];
   const int unit = blockIdx.y;
-  if (a.redo[size_t(unit) * a.total_chunks + blockIdx.x] == 0) return;
-  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
-  if (cp.seq < 0) return;
+  // A few work-groups per unit walk the unit's chunks: most launches find no
+  // flagged chunk, and the flag reads then cost little.
+  for (int32_t x = blockIdx.x; x < a.total_chunks; x += gridDim.x) {
+  if (a.redo[size_t(unit) * a.total_chunks + x] == 0) continue;
+  const ChunkPos cp = locate_chunk(a.lay, a.chunk, x);
+  if (cp.seq < 0) continue;
+  __syncthreads();  // the previous chunk's readers of lim_s are done
   const int lane = threadIdx.x & 63;
   fill_row_limits(a, cp, lim_s);
   bf16x8_t qa[RB][8];
@@ -457,13 +463,18 @@ __global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_rowstats_exa
         a.partial[(size_t(unit) * a.total_chunks + cp.gchunk) * a.rows_pad + r] = make_float2(mm, ss);
       }
     }
+  }
 }
 
 // Per (sequence, row): lse = log2 of the softmax denominator over the
 // sequence's chunks.  Each chunk's (offset, sum) is first turned into its
-// log2 total, so that the merge cannot overflow however large a chunk's sum.
-__global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
-  const int s = blockIdx.x, unit = blockIdx.y;
+// log2 total t_c, and the totals are merged in one pass as a running maximum M
+// with Z = sum 2^(t_c - M), so that the merge cannot overflow however large a
+// chunk's sum.  One row per thread; work-group (row block of 64, sequence, unit).
+__global__ __launch_bounds__(64) void score_combine_kernel(ScoreArgs a) {
+  const int s = blockIdx.y, unit = blockIdx.z;
+  const int r = blockIdx.x * 64 + threadIdx.x;
+  if (r >= a.rows_pad) return;
   int32_t first = 0;
   for (int32_t t = 0; t < s; ++t) {
     const int32_t L = a.lay.cu_seqlens[t + 1] - a.lay.cu_seqlens[t];
@@ -471,24 +482,24 @@ __global__ __launch_bounds__(256) void score_combine_kernel(ScoreArgs a) {
   }
   const int32_t L = a.lay.cu_seqlens[s + 1] - a.lay.cu_seqlens[s];
   const int32_t nch = (L + a.chunk - 1) / a.chunk;
-  for (int r = threadIdx.x; r < a.rows_pad; r += blockDim.x) {
-    float out = INFINITY;  // padding rows contribute exp2(-inf) = 0 in pass 2
-    if (r < a.rows) {
-      const float2* pr = a.partial + (size_t(unit) * a.total_chunks + first) * a.rows_pad + r;
-      float M = -INFINITY;
-      for (int32_t c = 0; c < nch; ++c) {
-        const float2 v = pr[size_t(c) * a.rows_pad];
-        M = fmaxf(M, v.x + __log2f(v.y));
+  float out = INFINITY;  // padding rows contribute exp2(-inf) = 0 in pass 2
+  if (r < a.rows) {
+    const float2* pr = a.partial + (size_t(unit) * a.total_chunks + first) * a.rows_pad + r;
+    float M = -INFINITY, Z = 0.0f;
+#pragma unroll 8
+    for (int32_t c = 0; c < nch; ++c) {
+      const float2 v = pr[size_t(c) * a.rows_pad];
+      const float t = v.x + __log2f(v.y);  // -inf for an empty sum
+      if (t > M) {
+        Z = Z * __builtin_amdgcn_exp2f(M - t) + 1.0f;
+        M = t;
+      } else if (t > -INFINITY) {
+        Z += __builtin_amdgcn_exp2f(t - M);
       }
-      float Z = 0.0f;
-      for (int32_t c = 0; c < nch; ++c) {
-        const float2 v = pr[size_t(c) * a.rows_pad];
-        Z += v.y * __builtin_amdgcn_exp2f(v.x - M);
-      }
-      out = M + __log2f(Z);
     }
-    a.lse2[(size_t(unit) * a.lay.n_seqs + s) * a.rows_pad + r] = out;
+    out = M + __log2f(Z);
   }
+  a.lse2[(size_t(unit) * a.lay.n_seqs + s) * a.rows_pad + r] = out;
 }
 
 template <int RB, int NW>
@@ -498,10 +509,12 @@ hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((score_pass_kernel<1, RB, NW>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((score_rowstats_exact_kernel<RB, NW>), grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_rowstats_exact_kernel<RB, NW>), dim3(std::min(a.total_chunks, 4), a.lay.n_units), block, 0,
+                     stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(score_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(score_combine_kernel, dim3((a.rows_pad + 63) / 64, a.lay.n_seqs, a.lay.n_units), dim3(64), 0,
+                     stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((score_pass_kernel<2, RB, NW>), grid, block, 0, stream, a);

@@ -243,6 +243,7 @@ stlite_status stlite_validate(const stlite_problem* p) {
   if (p->head_dim != kHeadDim)
     return fail(STLITE_ERR_UNSUPPORTED, "head_dim %d: only %d is implemented", p->head_dim, kHeadDim);
   if (p->n_seqs < 1) return fail(STLITE_ERR_INVALID_ARG, "n_seqs must be >= 1");
+  if (p->n_seqs > 65535) return fail(STLITE_ERR_UNSUPPORTED, "n_seqs %d: at most 65535 sequences", p->n_seqs);
   if (p->n_frames < 0) return fail(STLITE_ERR_INVALID_ARG, "n_frames must be >= 0");
   if (p->window < 1) return fail(STLITE_ERR_INVALID_ARG, "window must be >= 1");
   const int64_t G = p->n_q_heads / p->n_kv_heads;
