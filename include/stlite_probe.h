@@ -24,7 +24,12 @@ extern "C" {
 /* MFMA shape of a probe. */
 typedef enum stlite_probe_shape {
   STLITE_PROBE_MFMA_16X16X32_BF16 = 0, /* v_mfma_f32_16x16x32_bf16: 16384 flops per instruction */
-  STLITE_PROBE_MFMA_32X32X16_BF16 = 1  /* v_mfma_f32_32x32x16_bf16: 32768 flops per instruction */
+  STLITE_PROBE_MFMA_32X32X16_BF16 = 1, /* v_mfma_f32_32x32x16_bf16: 32768 flops per instruction */
+  /* v_mfma_f32_32x32x16_bf16 with the window score's vector work: after every
+   * MFMA, fma + exp2 + add on two finished fp32 results of the other of two
+   * accumulators (one exponential per logit, the mix of the score passes);
+   * 32768 flops per instruction */
+  STLITE_PROBE_MFMA_32X32X16_BF16_EXP2 = 2
 } stlite_probe_shape;
 
 /*

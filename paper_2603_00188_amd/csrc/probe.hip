@@ -1,4 +1,6 @@
 // Matrix-core throughput probes (measurement only; see stlite_probe.h).
+#include <type_traits>
+
 #include "stlite_probe.h"
 #include "stlite_internal.h"
 
@@ -31,6 +33,32 @@ __global__ __launch_bounds__(kProbeThreads, 2) void probe_mfma_kernel(const uint
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) s += acc[j][i];
+  } else if constexpr (SHAPE == 2) {
+    // The window score's instruction mix: two 32-key blocks in turn, each
+    // MFMA followed by fma + exp2 + add on two finished logits of the other
+    // block, in a fixed order (as in the score passes).
+    f32x16_t acc[2] = {};
+    float sum[16] = {};
+    auto body = [&](auto kb_c) {
+      constexpr int kb = decltype(kb_c)::value;
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], b[(kk + 4 * kb) & 7], kk == 0 ? f32x16_t{} : acc[kb],
+                                                          0, 0, 0);
+        float sc = 0.125f;
+        asm volatile("" : "+s"(sc));
+        sum[2 * kk] += __builtin_amdgcn_exp2f(fmaf(acc[kb ^ 1][2 * kk], sc, -1.0f));
+        sum[2 * kk + 1] += __builtin_amdgcn_exp2f(fmaf(acc[kb ^ 1][2 * kk + 1], sc, -1.0f));
+        asm volatile("" ::"v"(sum[2 * kk]), "v"(sum[2 * kk + 1]));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    for (int32_t it = 0; it < iters; it += 2) {
+      body(std::integral_constant<int, 0>{});
+      if (it + 1 < iters) body(std::integral_constant<int, 1>{});
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += sum[i] + acc[0][i] + acc[1][i];
   } else {
     f32x16_t acc[2] = {};
     for (int32_t it = 0; it < iters; ++it) {
@@ -52,13 +80,16 @@ __global__ __launch_bounds__(kProbeThreads, 2) void probe_mfma_kernel(const uint
 extern "C" stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint16_t* operands, float* sink,
                                            int32_t n_groups, int32_t iters, void* stream) {
   using namespace stlite;
-  if ((shape != STLITE_PROBE_MFMA_16X16X32_BF16 && shape != STLITE_PROBE_MFMA_32X32X16_BF16) || !operands ||
-      !sink || n_groups < 1 || iters < 1)
+  if ((shape != STLITE_PROBE_MFMA_16X16X32_BF16 && shape != STLITE_PROBE_MFMA_32X32X16_BF16 &&
+       shape != STLITE_PROBE_MFMA_32X32X16_BF16_EXP2) ||
+      !operands || !sink || n_groups < 1 || iters < 1)
     return STLITE_ERR_INVALID_ARG;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (shape == STLITE_PROBE_MFMA_16X16X32_BF16)
     hipLaunchKernelGGL(probe_mfma_kernel<0>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
-  else
+  else if (shape == STLITE_PROBE_MFMA_32X32X16_BF16)
     hipLaunchKernelGGL(probe_mfma_kernel<1>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
+  else
+    hipLaunchKernelGGL(probe_mfma_kernel<2>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
   return hipGetLastError() == hipSuccess ? STLITE_OK : STLITE_ERR_HIP;
 }
