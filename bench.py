@@ -290,9 +290,10 @@ def measured_peaks(stream):
     sink = torch.empty(n_groups * 256, dtype=torch.float32, device="cuda")
     for name, shape, iters in (("mfma_16x16x32_bf16", S.PROBE_MFMA_16X16X32, 200),
                                ("mfma_32x32x16_bf16", S.PROBE_MFMA_32X32X16, 100),
-                               ("mfma_32x32x16_bf16_exp2_mix", S.PROBE_MFMA_32X32X16_EXP2, 100)):
+                               ("mfma_32x32x16_bf16_exp2_mix", S.PROBE_MFMA_32X32X16_EXP2, 100),
+                               ("mfma_16x16x32_bf16_exp2_mix", S.PROBE_MFMA_16X16X32_EXP2, 100)):
         t = timed(lambda: S.stlite_probe_mfma(shape, ops, sink, n_groups, iters, stream), 5)
-        flops = 8.0 * iters * n_groups * 4 * S.PROBE_FLOPS[shape]
+        flops = float(S.PROBE_MFMAS_PER_ITER[shape]) * iters * n_groups * 4 * S.PROBE_FLOPS[shape]
         out[name + "_tflops"] = round(flops / t / 1e12, 1)
     n = 8192
     a = torch.randn((n, n), generator=gen).to(torch.bfloat16).cuda()

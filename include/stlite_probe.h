@@ -29,13 +29,18 @@ typedef enum stlite_probe_shape {
    * MFMA, fma + exp2 + add on two finished fp32 results of the other of two
    * accumulators (one exponential per logit, the mix of the score passes);
    * 32768 flops per instruction */
-  STLITE_PROBE_MFMA_32X32X16_BF16_EXP2 = 2
+  STLITE_PROBE_MFMA_32X32X16_BF16_EXP2 = 2,
+  /* v_mfma_f32_16x16x32_bf16 with the same vector work per matrix-core cycle
+   * (fma + exp2 + add on two results per two MFMAs); 16384 flops per
+   * instruction */
+  STLITE_PROBE_MFMA_16X16X32_BF16_EXP2 = 3
 } stlite_probe_shape;
 
 /*
  * Runs n_groups work-groups of 256 threads, each lane issuing 8 MFMAs per
- * iteration for `iters` iterations: 8 * iters * 4 * n_groups waves' worth of
- * instructions, i.e. flops = 8 * iters * (4 * n_groups) * flops_per_instruction.
+ * iteration (16 for STLITE_PROBE_MFMA_16X16X32_BF16_EXP2) for `iters` iterations: 8 * iters * 4 * n_groups waves' worth of
+ * instructions, i.e. flops = 8 * iters * (4 * n_groups) * flops_per_instruction
+ * (16 * ... for the 16x16x32 exp2 probe).
  *   operands  device, bf16 bits, >= n_groups * 256 * 128 elements (read once)
  *   sink      device, fp32, >= n_groups * 256 elements (written: keeps the
  *             results live)

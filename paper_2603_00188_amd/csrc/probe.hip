@@ -59,6 +59,43 @@ __global__ __launch_bounds__(kProbeThreads, 2) void probe_mfma_kernel(const uint
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) s += sum[i] + acc[0][i] + acc[1][i];
+  } else if constexpr (SHAPE == 3) {
+    // The same vector work per matrix-core cycle on 16x16x32 MFMAs: two
+    // accumulator sets of four 16x16 blocks, each MFMA pair followed by
+    // fma + exp2 + add on two finished results of the other set.
+    f32x4_t acc[2][4] = {};
+    float sum[8] = {};
+    auto body = [&](auto h_c) {
+      constexpr int h = decltype(h_c)::value;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const int blk = 2 * p + t;
+            acc[h][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[(2 * kk + p) & 7], b[(kk + 2 * t + 4 * h) & 7],
+                                                                  kk == 0 ? f32x4_t{} : acc[h][blk], 0, 0, 0);
+          }
+          float sc = 0.125f;
+          asm volatile("" : "+s"(sc));
+          const int e = 2 * kk + p;  // 0 .. 7: two results of block e / 2 of the other set
+          sum[e] += __builtin_amdgcn_exp2f(fmaf(acc[h ^ 1][e >> 1][2 * (e & 1)], sc, -1.0f)) +
+                    __builtin_amdgcn_exp2f(fmaf(acc[h ^ 1][e >> 1][2 * (e & 1) + 1], sc, -1.0f));
+          asm volatile("" ::"v"(sum[e]));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    for (int32_t it = 0; it < iters; it += 2) {
+      body(std::integral_constant<int, 0>{});
+      if (it + 1 < iters) body(std::integral_constant<int, 1>{});
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += sum[i];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s += acc[0][j][i] + acc[1][j][i];
   } else {
     f32x16_t acc[2] = {};
     for (int32_t it = 0; it < iters; ++it) {
@@ -81,7 +118,7 @@ extern "C" stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint1
                                            int32_t n_groups, int32_t iters, void* stream) {
   using namespace stlite;
   if ((shape != STLITE_PROBE_MFMA_16X16X32_BF16 && shape != STLITE_PROBE_MFMA_32X32X16_BF16 &&
-       shape != STLITE_PROBE_MFMA_32X32X16_BF16_EXP2) ||
+       shape != STLITE_PROBE_MFMA_32X32X16_BF16_EXP2 && shape != STLITE_PROBE_MFMA_16X16X32_BF16_EXP2) ||
       !operands || !sink || n_groups < 1 || iters < 1)
     return STLITE_ERR_INVALID_ARG;
   const hipStream_t st = static_cast<hipStream_t>(stream);
@@ -89,7 +126,9 @@ extern "C" stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint1
     hipLaunchKernelGGL(probe_mfma_kernel<0>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
   else if (shape == STLITE_PROBE_MFMA_32X32X16_BF16)
     hipLaunchKernelGGL(probe_mfma_kernel<1>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
-  else
+  else if (shape == STLITE_PROBE_MFMA_32X32X16_BF16_EXP2)
     hipLaunchKernelGGL(probe_mfma_kernel<2>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
+  else
+    hipLaunchKernelGGL(probe_mfma_kernel<3>, dim3(n_groups), dim3(kProbeThreads), 0, st, operands, sink, iters);
   return hipGetLastError() == hipSuccess ? STLITE_OK : STLITE_ERR_HIP;
 }

@@ -285,9 +285,11 @@ class Buffers:
         self.side = (torch.cuda.Stream(device=device), torch.cuda.Stream(device=device))
 
 
-PROBE_MFMA_16X16X32, PROBE_MFMA_32X32X16, PROBE_MFMA_32X32X16_EXP2 = 0, 1, 2
+PROBE_MFMA_16X16X32, PROBE_MFMA_32X32X16, PROBE_MFMA_32X32X16_EXP2, PROBE_MFMA_16X16X32_EXP2 = 0, 1, 2, 3
 PROBE_FLOPS = {PROBE_MFMA_16X16X32: 16 * 16 * 32 * 2, PROBE_MFMA_32X32X16: 32 * 32 * 16 * 2,
-               PROBE_MFMA_32X32X16_EXP2: 32 * 32 * 16 * 2}
+               PROBE_MFMA_32X32X16_EXP2: 32 * 32 * 16 * 2, PROBE_MFMA_16X16X32_EXP2: 16 * 16 * 32 * 2}
+PROBE_MFMAS_PER_ITER = {PROBE_MFMA_16X16X32: 8, PROBE_MFMA_32X32X16: 8, PROBE_MFMA_32X32X16_EXP2: 8,
+                        PROBE_MFMA_16X16X32_EXP2: 16}
 
 
 def stlite_probe_mfma(shape: int, operands, sink, n_groups: int, iters: int, stream=None) -> None:

@@ -233,7 +233,7 @@ def test_kept_overlap_rejections():
 
 def test_probe_rejections():
     lib = S.load()
-    assert lib.stlite_probe_mfma(3, FAKE_DEV, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_mfma(4, FAKE_DEV, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(-1, FAKE_DEV, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(0, None, FAKE_DEV, 1, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(1, FAKE_DEV, None, 1, 1, None) == S.ERR_INVALID_ARG
