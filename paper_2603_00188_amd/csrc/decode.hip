@@ -182,29 +182,33 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_chunk_kernel(DecodeArgs
   }
 }
 
-// Per (unit, sequence): merge the chunks, out = O / L (0 for a sequence
-// without rows).
-__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
+// Per (unit, sequence, query head): merge the chunks, out = O / L (0 for a
+// sequence without rows).  One output dimension per thread; the chunks are
+// merged in one pass with a running maximum M, rescaling L and O whenever it
+// rises, so the loads of successive chunks do not wait on each other.
+__global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(DecodeArgs a) {
   const int32_t s = blockIdx.x;
-  const int unit = blockIdx.y;
+  const int unit = blockIdx.y, h = blockIdx.z;
+  const int dim = threadIdx.x;
   const int layer = unit / a.lay.n_kv_heads, kv = unit % a.lay.n_kv_heads;
   int32_t first = 0;
   for (int32_t t = 0; t < s; ++t) first += (a.cu_rows[t + 1] - a.cu_rows[t] + a.chunk - 1) / a.chunk;
   const int32_t nch = (a.cu_rows[s + 1] - a.cu_rows[s] + a.chunk - 1) / a.chunk;
   const size_t c0 = size_t(unit) * a.total_chunks + first;
-  for (int e = threadIdx.x; e < a.group * kHeadDim; e += blockDim.x) {
-    const int h = e / kHeadDim, dim = e % kHeadDim;
-    float M = -INFINITY;
-    for (int32_t c = 0; c < nch; ++c) M = fmaxf(M, a.pm[(c0 + c) * kDecHeads + h]);
-    float L = 0.0f, O = 0.0f;
-    for (int32_t c = 0; c < nch; ++c) {
-      const float wt = __builtin_amdgcn_exp2f(a.pm[(c0 + c) * kDecHeads + h] - M);
-      L += wt * a.pl[(c0 + c) * kDecHeads + h];
-      O += wt * a.po[((c0 + c) * kDecHeads + h) * kHeadDim + dim];
-    }
-    a.out[((size_t(layer) * a.lay.n_seqs + s) * a.n_q_heads + size_t(kv) * a.group + h) * kHeadDim + dim] =
-        L > 0.0f ? O / L : 0.0f;
+  float M = -INFINITY, L = 0.0f, O = 0.0f;
+#pragma unroll 4
+  for (int32_t c = 0; c < nch; ++c) {
+    const size_t ch = (c0 + c) * kDecHeads + h;
+    const float m = a.pm[ch], l = a.pl[ch], o = a.po[ch * kHeadDim + dim];
+    if (m == -INFINITY) continue;  // a chunk that saw no row of the sequence
+    const float mx = fmaxf(M, m);
+    const float sa = __builtin_amdgcn_exp2f(M - mx), sb = __builtin_amdgcn_exp2f(m - mx);
+    L = L * sa + l * sb;
+    O = O * sa + o * sb;
+    M = mx;
   }
+  a.out[((size_t(layer) * a.lay.n_seqs + s) * a.n_q_heads + size_t(kv) * a.group + h) * kHeadDim + dim] =
+      L > 0.0f ? O / L : 0.0f;
 }
 
 }  // namespace
@@ -215,7 +219,7 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(decode_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(decode_combine_kernel, dim3(a.lay.n_seqs, a.lay.n_units, a.group), dim3(kHeadDim), 0, stream, a);
   return hipGetLastError();
 }
 
