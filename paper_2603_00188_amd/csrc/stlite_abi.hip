@@ -79,10 +79,12 @@ Facts derive(const stlite_problem* p) {
     }
     f.total_hist_blocks += ceil_div(hist, kRhoRows);
   }
-  // Selection parts: aim for >= 512 work-groups over all segments, with
-  // parts of at least ~4096 tokens, at most 16.
+  // Selection parts: aim for >= 512 work-groups over all segments and for
+  // parts of at most ~32768 tokens (the longest segment's part bounds the
+  // pass), with parts of at least ~4096 tokens, at most 16.
   const int64_t segs = std::max<int64_t>(f.units * p->n_seqs, 1);
-  int64_t parts = std::min(ceil_div(512, segs), std::max<int64_t>(ceil_div(f.max_seq, 4096), 1));
+  int64_t parts = std::max(ceil_div(512, segs), ceil_div(f.max_seq, 32768));
+  parts = std::min(parts, std::max<int64_t>(ceil_div(f.max_seq, 4096), 1));
   f.sel_parts = int32_t(std::min<int64_t>(std::max<int64_t>(parts, 1), 16));
   return f;
 }
