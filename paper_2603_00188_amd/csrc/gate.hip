@@ -26,29 +26,35 @@ struct GateProd {
 
   __device__ int32_t cursor(const SelCtx& c, int32_t i) const { return __builtin_amdgcn_readfirstlane(fr.find(c.s0 + i)); }
 
-  __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
-                          uint32_t (&key)[kSelJ]) const {
-    bool hist[kSelJ];
+  struct Raw {
+    uint32_t hist;  // bit j: token j of the step is historical
+    float r[kSelJ];
+  };
+
+  __device__ void fetch(const SelCtx& c, int32_t base, int32_t lane, int32_t& cur, Raw& w) const {
     const StepFrames st = step_frames(fr, cur, c.s0 + base, 64 * kSelJ);
     const int u = st.n >= 0 ? st.uniform(c.s0 + base, 64 * kSelJ) : -1;
+    w.hist = 0u;
     if (u >= 0) {
-#pragma unroll
-      for (int j = 0; j < kSelJ; ++j) hist[j] = u == kHist;
+      w.hist = u == kHist ? (1u << kSelJ) - 1u : 0u;
     } else if (st.n >= 0) {
 #pragma unroll
-      for (int j = 0; j < kSelJ; ++j) hist[j] = st.cls(c.s0 + base + 64 * j + lane) == kHist;
+      for (int j = 0; j < kSelJ; ++j) w.hist |= (st.cls(c.s0 + base + 64 * j + lane) == kHist ? 1u : 0u) << j;
     } else {
 #pragma unroll
-      for (int j = 0; j < kSelJ; ++j) hist[j] = tok_class_search(fr, c.s0 + base + 64 * j + lane) == kHist;
+      for (int j = 0; j < kSelJ; ++j) w.hist |= (tok_class_search(fr, c.s0 + base + 64 * j + lane) == kHist ? 1u : 0u) << j;
     }
-    float r[kSelJ];
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j)
-      r[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, (base + 64 * j + lane) * 4, 0, 0));
+      w.r[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, (base + 64 * j + lane) * 4, 0, 0));
+  }
+
+  __device__ void finish(const SelCtx&, int32_t base, int32_t lane, int32_t hi, const Raw& w,
+                         uint32_t (&key)[kSelJ]) const {
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) {
-      const bool h = hist[j] && base + 64 * j + lane < hi;
-      key[j] = h ? min(order_key(r[j]), kSelNever - 1u) : kSelNever;
+      const bool h = ((w.hist >> j) & 1u) && base + 64 * j + lane < hi;
+      key[j] = h ? min(order_key(w.r[j]), kSelNever - 1u) : kSelNever;
     }
   }
 

@@ -151,18 +151,25 @@ __device__ __forceinline__ StepFrames step_frames(const SeqFrames<LDS>& fr, int3
   StepFrames st;
   st.n = 0;
   int32_t f = (cur >= 0 && uni(fr.end(cur)) > base) ? cur : cur + 1;
-  for (; f < fr.nf; ++f) {
-    const int32_t s = uni(fr.start(f));
-    if (s >= base + span) break;
-    if (st.n == kStepFrames) {
-      st.n = -1;
-      break;
+  // static slots (no runtime index into the arrays, which would put them in
+  // private memory)
+#pragma unroll
+  for (int q = 0; q < kStepFrames; ++q) {
+    st.s[q] = 0;
+    st.e[q] = 0;
+    st.last[q] = false;
+    if (f < fr.nf) {
+      const int32_t s = uni(fr.start(f));
+      if (s < base + span) {
+        st.s[q] = s;
+        st.e[q] = uni(fr.end(f));
+        st.last[q] = f == fr.nf - 1;
+        st.n = q + 1;
+        ++f;
+      }
     }
-    st.s[st.n] = s;
-    st.e[st.n] = uni(fr.end(f));
-    st.last[st.n] = f == fr.nf - 1;
-    ++st.n;
   }
+  if (f < fr.nf && uni(fr.start(f)) < base + span) st.n = -1;  // more frames overlap the step
   return st;
 }
 
@@ -365,9 +372,14 @@ __device__ inline __amdgpu_buffer_rsrc_t sel_keys(const SelPlan& s, const Layout
 
 // Produce pass: keys of this part and its level-0 histogram.  Prod provides
 //   int32_t cursor(const SelCtx&, int32_t i): wave-uniform frame cursor for segment token i;
-//   void produce(const SelCtx&, int32_t base, int32_t lane, int32_t hi, int32_t& cur, uint32_t (&key)[kSelJ]):
-//        keys of segment tokens base + 64 j + lane, kSelNever where that is >= hi.
-// c.k is written to the segment state by part 0.
+//   Raw: the loaded inputs of one step;
+//   void fetch(const SelCtx&, int32_t base, int32_t lane, int32_t& cur, Raw&): issue the
+//        loads of segment tokens base + 64 j + lane (and classify them);
+//   void finish(const SelCtx&, int32_t base, int32_t lane, int32_t hi, const Raw&, uint32_t (&key)[kSelJ]):
+//        their keys, kSelNever where base + 64 j + lane >= hi.
+// The loads of step s + 1 are issued before step s is finished, so a wave
+// keeps one step's loads in flight while it computes.  c.k is written to the
+// segment state by part 0.
 template <class Prod>
 __device__ void sel_produce(const Prod& p, SelShared& sh, const SelPlan& s, const Layout& lay, const SelCtx& c) {
   const int lane = threadIdx.x & 63;
@@ -377,9 +389,15 @@ __device__ void sel_produce(const Prod& p, SelShared& sh, const SelPlan& s, cons
   sel_hist_zero(sh, 2048);
   __syncthreads();
   int32_t cur = p.cursor(c, pt.lo);
+  // (a fetch past the part reads inside the sequence or gets 0 from the
+  // buffer, and its result is never finished)
+  typename Prod::Raw raw;
+  p.fetch(c, pt.lo, lane, cur, raw);
   for (int32_t base = pt.lo; base < pt.hi; base += 64 * kSelJ) {
+    typename Prod::Raw next;
+    p.fetch(c, base + 64 * kSelJ, lane, cur, next);
     uint32_t key[kSelJ];
-    p.produce(c, base, lane, pt.hi, cur, key);
+    p.finish(c, base, lane, pt.hi, raw, key);
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) {
       const int32_t i = base + 64 * j + lane;
@@ -387,6 +405,7 @@ __device__ void sel_produce(const Prod& p, SelShared& sh, const SelPlan& s, cons
     }
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) sel_hist_add<1>(sh.hist, base + 64 * j + lane < pt.hi, key[j] >> 21);
+    raw = next;
   }
   __syncthreads();
   const size_t seg = sel_seg(lay);

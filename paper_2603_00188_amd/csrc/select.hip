@@ -27,41 +27,45 @@ struct SelectProd {
     return classify ? __builtin_amdgcn_readfirstlane(fr.find(c.s0 + i)) : -1;
   }
 
-  __device__ void produce(const SelCtx& c, int32_t base, int32_t lane, int32_t hi, int32_t& cur,
-                          uint32_t (&key)[kSelJ]) const {
-    bool vis[kSelJ];
-#pragma unroll
-    for (int j = 0; j < kSelJ; ++j) vis[j] = false;
+  struct Raw {
+    uint32_t vis;  // bit j: token j of the step is visual
+    float A[kSelJ], ph[kSelJ];
+    uint32_t g[kSelJ];
+  };
+
+  __device__ void fetch(const SelCtx& c, int32_t base, int32_t lane, int32_t& cur, Raw& r) const {
+    r.vis = 0u;
     if (classify) {
       const StepFrames st = step_frames(fr, cur, c.s0 + base, 64 * kSelJ);
       const int u = st.n >= 0 ? st.uniform(c.s0 + base, 64 * kSelJ) : -1;
       if (u >= 0) {
-#pragma unroll
-        for (int j = 0; j < kSelJ; ++j) vis[j] = u != kText;
+        r.vis = u != kText ? (1u << kSelJ) - 1u : 0u;
       } else if (st.n >= 0) {
 #pragma unroll
-        for (int j = 0; j < kSelJ; ++j) vis[j] = st.cls(c.s0 + base + 64 * j + lane) != kText;
+        for (int j = 0; j < kSelJ; ++j) r.vis |= (st.cls(c.s0 + base + 64 * j + lane) != kText ? 1u : 0u) << j;
       } else {
 #pragma unroll
-        for (int j = 0; j < kSelJ; ++j) vis[j] = tok_class_search(fr, c.s0 + base + 64 * j + lane) != kText;
+        for (int j = 0; j < kSelJ; ++j) r.vis |= (tok_class_search(fr, c.s0 + base + 64 * j + lane) != kText ? 1u : 0u) << j;
       }
     }
-    float A[kSelJ], ph[kSelJ];
-    uint32_t g[kSelJ];
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) {
       const int32_t i = base + 64 * j + lane;
-      A[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
-      ph[j] = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
-      g[j] = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+      r.A[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
+      r.ph[j] = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
+      r.g[j] = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
     }
+  }
+
+  __device__ void finish(const SelCtx&, int32_t base, int32_t lane, int32_t hi, const Raw& r,
+                         uint32_t (&key)[kSelJ]) const {
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) {
       const int32_t i = base + 64 * j + lane;
-      float S = A[j];
-      if (vis[j]) {
-        const float x = has_phi ? fmaf(alpha, ph[j], A[j]) : A[j];
-        S = g[j] == 0 ? 0.0f : x;
+      float S = r.A[j];
+      if ((r.vis >> j) & 1u) {
+        const float x = has_phi ? fmaf(alpha, r.ph[j], r.A[j]) : r.A[j];
+        S = r.g[j] == 0 ? 0.0f : x;
       }
       if (score && i < hi) score[i] = S;
       key[j] = i < hi ? min(~order_key(S), kSelNever - 1u) : kSelNever;
