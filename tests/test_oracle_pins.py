@@ -770,3 +770,71 @@ def test_concat_identical_heads_match_one_head():
     np.testing.assert_allclose(cat["rho"], one["rho"], atol=1e-14)
     assert cat["kept"].tolist() == one["kept"].tolist()
 
+
+
+# ------------------------------------------- packed varlen batch entry point --
+
+def _bits(x):
+    """bf16 bit patterns of float values that bf16 holds exactly."""
+    f = np.asarray(x, dtype=np.float32)
+    b = f.view(np.uint32)
+    assert ((b & 0xFFFF) == 0).all(), "value not exact in bf16"
+    return (b >> 16).astype(np.uint16)
+
+
+def test_compress_sequence_packed_batch_matches_hand_slices():
+    """compress_sequence on a packed batch of three sequences (ragged lengths,
+    one text-only) equals compress_unit and the literal twin run on arrays
+    sliced by hand: the contiguous GQA group of query heads kv*G .. kv*G+G-1,
+    the sequence's own token range and frames with local offsets.  The local
+    frames and the per-head queries are built first and packed afterwards, so
+    an interleaved head slice, a wrong sequence offset or frames left absolute
+    give different inputs to the two sides."""
+    rng = np.random.default_rng(2024)
+    d, G, Hkv, n_layers, delta = 128, 2, 2, 2, 3
+    beta, alpha = (1, 3), 1.0
+    # local layouts: (frames as (local offset, rows, cols), length)
+    seqs = [([(2, 2, 3), (10, 2, 3), (19, 3, 2)], 29),   # text, frames, text between, trailing text
+            ([], 11),                                        # text only
+            ([(0, 3, 3), (12, 3, 3)], 25)]                  # frame first, current frame then text
+    lens = [L for _, L in seqs]
+    cu_seqlens = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    cu_frames = np.concatenate([[0], np.cumsum([len(f) for f, _ in seqs])]).astype(np.int32)
+    frame_meta = np.array([(int(cu_seqlens[s]) + o, r, c) for s, (fr, _) in enumerate(seqs) for o, r, c in fr],
+                          np.int32).reshape(-1, 3)
+    Lt = int(cu_seqlens[-1])
+    coarse = lambda *shape: np.round(rng.standard_normal(shape) * 8) / 64.0   # exact in bf16
+    # distinct queries per (layer, sequence, query head), keys/values per (layer, kv head)
+    Qf = coarse(n_layers, len(seqs), G * Hkv, delta, d)
+    Kf = coarse(n_layers, Hkv, Lt, d)
+    Vf = coarse(n_layers, Hkv, Lt, d)
+    # one current-frame key copied into the history of sequence 0 (the snap class)
+    a0 = int(cu_seqlens[0])
+    Kf[:, :, a0 + 2] = Kf[:, :, a0 + 19 + 1]
+    q_bits, k_bits, v_bits = _bits(Qf), _bits(Kf), _bits(Vf)
+    for s, (frames_local, L) in enumerate(seqs):
+        a = int(cu_seqlens[s])
+        assert O.seq_frames_local(cu_seqlens, cu_frames, frame_meta, s) == frames_local
+        for layer in range(n_layers):
+            for kv in range(Hkv):
+                got = O.compress_sequence(q_bits, k_bits, v_bits, cu_seqlens, cu_frames, frame_meta, s,
+                                          layer, kv, G, beta, alpha)
+                Qg = np.stack([Qf[layer, s, kv * G + g] for g in range(G)])     # [G, delta, d]
+                Ks, Vs = Kf[layer, kv, a:a + L], Vf[layer, kv, a:a + L]
+                ref = O.compress_unit(_bits(Qg), _bits(Ks), _bits(Vs), frames_local, beta, alpha)
+                lit = O1.compress([[list(map(float, r)) for r in g] for g in Qg],
+                                  [list(map(float, r)) for r in Ks], frames_local, O.budget(L, *beta), alpha)
+                where = (s, layer, kv)
+                assert got["B"] == ref["B"] == O.budget(L, *beta), where
+                np.testing.assert_array_equal(got["A"], ref["A"])
+                np.testing.assert_allclose(got["A"], lit["A"], rtol=1e-12, atol=0)
+                np.testing.assert_allclose(got["phi"], lit["phi"], rtol=1e-12, atol=1e-13)
+                assert got["gate"].tolist() == lit["gate"], where
+                assert got["kept"].tolist() == lit["kept"], where
+                assert (got["kept_abs"] == got["kept"] + a).all() and got["offset"] == a
+                np.testing.assert_array_equal(got["k_out"], _bits(Ks[lit["kept"]]))
+                np.testing.assert_array_equal(got["v_out"], _bits(Vs[lit["kept"]]))
+    # an interleaved head grouping (query head kv + Hkv * g) picks other queries
+    Qi = np.stack([Qf[0, 0, kv_g] for kv_g in (1, 1 + Hkv)])
+    Qc = np.stack([Qf[0, 0, 1 * G + g] for g in range(G)])
+    assert not np.array_equal(Qi, Qc)
