@@ -241,6 +241,8 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
     S.stlite_tsg_rho(prob, dk, rho, out.ws_tsg, stream)
     ms = timed(lambda: S.stlite_tsg_fixed_gate(prob, rho, 0.85, out.gate, stream))
     entry["tsg_fixed_gate"] = roofline_entry(model["tsg_threshold"], ms)
+    ms = timed(lambda: S.stlite_css_saliency(prob, dk, out.phi, None, stream))
+    entry["css_saliency_ungated"] = roofline_entry(model["css_saliency"], ms)
     for k in (5, 7, 9):
         ms = timed(lambda: S.stlite_css_saliency_nbhd(prob, k, dk, out.phi, stream))
         e = roofline_entry({"bound": "hbm", "bytes": model["css_saliency"]["bytes"]}, ms)
@@ -385,23 +387,22 @@ def main():
     log(f"inputs resident: K+V {2 * dk.numel() * 2 / 1e9:.2f} GB")
 
     stream = torch.cuda.current_stream()
-    s_tsg, s_css = out.side
+    s_tsg = out.side[0]
     names = ["score_window", "tsg_rho", "tsg_threshold", "css_saliency", "select_topk", "compact_kv"]
     # Concurrent streams gain about 1% here (the two MFMA passes share the
     # matrix cores) and blur the per-kernel times, so the timed step is serial.
     overlap = args.overlap
 
     def step(ev=None):
-        # With --overlap the three independent steps run concurrently (score on
-        # the main stream, TSG and CSS on side streams).  The TSG step runs as
+        # With --overlap the window score runs on the main stream while TSG
+        # and then the gated CSS run on a side stream.  The TSG step runs as
         # its two calls (rho, then threshold and gate), so that the rho GEMM
         # is timed on its own.  Per-call events sit on the stream of their call.
-        st = (stream, s_tsg, s_css) if overlap else (stream, stream, stream)
+        st = (stream, s_tsg) if overlap else (stream, stream)
         if overlap:
             start = torch.cuda.Event()
             start.record(stream)
             s_tsg.wait_event(start)
-            s_css.wait_event(start)
         if ev: ev["score_window"][0].record(st[0])
         S.stlite_score_window(prob, dq, dk, out.a_base, out.ws, st[0])
         if ev: ev["score_window"][1].record(st[0])
@@ -411,14 +412,13 @@ def main():
         if ev: ev["tsg_threshold"][0].record(st[1])
         S.stlite_tsg_threshold(prob, rho, None, out.gate, out.ws_tsg, st[1])
         if ev: ev["tsg_threshold"][1].record(st[1])
-        if ev: ev["css_saliency"][0].record(st[2])
-        S.stlite_css_saliency(prob, dk, out.phi, st[2])
-        if ev: ev["css_saliency"][1].record(st[2])
+        if ev: ev["css_saliency"][0].record(st[1])
+        S.stlite_css_saliency(prob, dk, out.phi, out.gate, st[1])
+        if ev: ev["css_saliency"][1].record(st[1])
         if overlap:
-            for s in (s_tsg, s_css):
-                done = torch.cuda.Event()
-                done.record(s)
-                stream.wait_event(done)
+            done = torch.cuda.Event()
+            done.record(s_tsg)
+            stream.wait_event(done)
         if ev: ev["select_topk"][0].record(stream)
         S.stlite_select_topk(prob, out.a_base, out.phi, out.gate, w.alpha, out.kept, None, out.ws, stream)
         if ev: ev["select_topk"][1].record(stream)
@@ -447,8 +447,10 @@ def main():
     stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
     dom = max(names, key=lambda n: per_call[n])
     kernel_of = {"score_window": "score_pass_kernel<1> + score_pass_kernel<2>",
-                 "tsg_rho": "rho_kernel", "tsg_threshold": "gate_kernel",
-                 "css_saliency": "css_kernel", "select_topk": "select_kernel",
+                 "tsg_rho": "rho_kernel",
+                 "tsg_threshold": "gate_produce_kernel + sel_level1_kernel + sel_level2_kernel + gate_emit_kernel",
+                 "css_saliency": "css_kernel<true>",
+                 "select_topk": "select_produce_kernel + sel_level1_kernel + sel_level2_kernel + select_emit_kernel",
                  "compact_kv": "compact_kernel"}
     roof = dict(stages[dom])
     roof.pop("ms")
@@ -478,7 +480,7 @@ def main():
             "tokens": lay.total_tokens, "layers": w.n_layers, "kv_heads": w.n_kv_heads,
             "q_heads": w.n_q_heads, "window": w.window, "beta": f"{w.beta[0]}/{w.beta[1]}",
             "budget_per_unit": int(cu_budget[-1]),
-            "streams": "score | tsg_rho+tsg_threshold | css, then select, compact" if overlap else "one stream",
+            "streams": "score | tsg_rho+tsg_threshold+css, then select, compact" if overlap else "one stream",
         },
         "roofline": roof,
         "stages": stages,

@@ -81,7 +81,7 @@
 extern "C" {
 #endif
 
-#define STLITE_ABI_VERSION 1
+#define STLITE_ABI_VERSION 2
 
 typedef enum stlite_status {
   STLITE_OK = 0,
@@ -192,9 +192,14 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
  * H = mean over its in-grid Moore neighbours (8, 5 or 3 of them) of the key
  * cosine, and phi = 1 - H; phi = 0 for a 1x1 frame and for text tokens.  A
  * cosine with a zero key is 0.  Writes phi [units][total_tokens].
+ * gate (nullable) is the TSG gate [units][total_tokens] that stlite_tsg_gate
+ * or stlite_tsg_threshold wrote: where gate == 0 the token's phi is written
+ * as exactly 0 without being computed (Eq. modal_scoring multiplies it by
+ * M = 0), and cosines that no admitted token needs are skipped; where
+ * gate != 0, phi is bit for bit the value of the ungated call.
  */
-stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, float* phi,
-                                  void* stream);
+stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, const uint8_t* gate,
+                                  float* phi, void* stream);
 
 /*
  * CSS under a wider neighbourhood, for the paper's neighbourhood-size ablation

@@ -17,6 +17,13 @@
 // strip.  The strips of one frame are given to work-groups that land on the
 // same XCD, where the halo columns hit the shared L2.
 //
+// With the TSG gate given (GATED), a token whose gate is 0 gets Phi = 0 (its
+// saliency is multiplied away by M = 0 in Eq. modal_scoring), and a strip row
+// whose cosines no admitted cell of that row or the next needs skips them
+// (the row is still loaded: its keys are the neighbours of the rows around
+// it).  Each lane's gate byte is loaded three rows ahead, right after the
+// row's DMA, so the loads complete in the same order as the ring rows.
+//
 // The neighbourhood-size ablation widens the window to k x k, k = 2 KR + 1 in
 // {5, 7, 9} (css_wide_kernel): H = mean over the in-grid cells of the square
 // other than the centre.  There the cosines form a small dense contraction,
@@ -111,6 +118,7 @@ __device__ inline float inv_norm(float ss) {
   return r;
 }
 
+template <bool GATED>
 __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ring0[kRowElems], ring1[kRowElems], ring2[kRowElems],
       ring3[kRowElems];
@@ -139,15 +147,30 @@ __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   const __amdgpu_buffer_rsrc_t phi_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(a.phi + size_t(unit) * lay.total_tokens + off, 0, frame_bytes, kBufferFlags);
   const int ge = min(g + 1, kStripCells - 1), gw = max(g - 1, 0);
+  // The gate bytes of the frame (GATED): lanes without an output read an
+  // offset past the end, which returns 0.
+  const __amdgpu_buffer_rsrc_t gate_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(GATED ? a.gate + size_t(unit) * lay.total_tokens + off : nullptr), 0,
+      GATED ? uint32_t(R) * uint32_t(C) : 0u, kBufferFlags);
+  const uint32_t gate_none = uint32_t(R) * uint32_t(C);
+  auto gate_load = [&](int32_t row) -> uint32_t {
+    return __builtin_amdgcn_raw_buffer_load_b8(gate_rsrc, out_lane ? uint32_t(row * C + col) : gate_none, 0, 0);
+  };
+  // vector-memory operations per ring row: its DMA and, gated, the gate bytes
+  constexpr int kPerRow = kRowLoads + (GATED ? 1 : 0);
 
   // Every step issues one row (rows past the end repeat row R-1 and hit L2),
   // so the number of loads in flight is the same on every path: 2 rows.
+  uint32_t g0 = 1, g1 = 1, g2 = 1, g3 = 1;  // gates of rows r .. r+3 (GATED)
   row_dma(kframe, 0, c0, C, ring0);
+  if (GATED) g0 = gate_load(0);
   row_dma(kframe, min(1, R - 1), c0, C, ring1);
+  if (GATED) g1 = gate_load(min(1, R - 1));
   row_dma(kframe, min(2, R - 1), c0, C, ring2);
+  if (GATED) g2 = gate_load(min(2, R - 1));
 
   // Row 0: own slice and inverse norm.
-  wait_vmcnt<2 * kRowLoads>();
+  wait_vmcnt<2 * kPerRow>();
   Slice own = read_slice(ring0, g, s);
   float rn_own = inv_norm(quad_sum(dot_slice(own, own)));
   float carry = 0.0f;  // sum of row r-1's cosines with (r, col)
@@ -155,39 +178,52 @@ __global__ __launch_bounds__(64) void css_kernel(CssArgs a) {
   auto step = [&](int32_t r, uint16_t* cur, uint16_t* nxt, uint16_t* issue_dst) {
     const bool has_s = r + 1 < R;
     row_dma(kframe, min(r + 3, R - 1), c0, C, issue_dst);
-    wait_vmcnt<2 * kRowLoads>();  // row r+1 has landed
-    // East neighbour in this row; norms of the east cell come by shuffle.
-    const Slice e = read_slice(cur, ge, s);
-    const float dE = quad_sum(dot_slice(own, e));
-    const float rnE = __shfl(rn_own, (ge << 2) | s);
-    const float cE = has_e ? dE * rn_own * rnE : 0.0f;
+    if (GATED) g3 = gate_load(min(r + 3, R - 1));
+    wait_vmcnt<2 * kPerRow>();  // row r+1 (and its gate bytes) have landed
     // Row r+1 (on the last row the slot holds a repeat of row R-1; masked).
     const Slice down = read_slice(nxt, g, s);
-    const Slice se = read_slice(nxt, ge, s);
-    const Slice sw = read_slice(nxt, gw, s);
     const float rn_down = inv_norm(quad_sum(dot_slice(down, down)));
-    const float dS = quad_sum(dot_slice(own, down));
-    const float dSE = quad_sum(dot_slice(own, se));
-    const float dSW = quad_sum(dot_slice(own, sw));
-    const float rnSE = __shfl(rn_down, (ge << 2) | s);
-    const float rnSW = __shfl(rn_down, (gw << 2) | s);
-    const float cS = has_s ? dS * rn_own * rn_down : 0.0f;
-    const float cSE = has_s && has_e ? dSE * rn_own * rnSE : 0.0f;
-    const float cSW = has_s && has_w ? dSW * rn_own * rnSW : 0.0f;
-    // Cosines owned by the west / east neighbours of this cell.
-    const float cE_w = __shfl(cE, (gw << 2) | s);
-    const float cSE_w = __shfl(cSE, (gw << 2) | s);
-    const float cSW_e = __shfl(cSW, (ge << 2) | s);
-    const float H = carry + cE + cS + cSE + cSW + (has_w ? cE_w : 0.0f);
+    // The cosines of this step serve rows r and r+1: skip them when no cell
+    // of either needs its Phi (wave-uniform).
+    const bool need = r < R && (!GATED || __ballot(out_lane && (g0 | g1) != 0u) != 0);
+    float H = 0.0f;
+    if (need) {
+      // East neighbour in this row; norms of the east cell come by shuffle.
+      const Slice e = read_slice(cur, ge, s);
+      const float dE = quad_sum(dot_slice(own, e));
+      const float rnE = __shfl(rn_own, (ge << 2) | s);
+      const float cE = has_e ? dE * rn_own * rnE : 0.0f;
+      const Slice se = read_slice(nxt, ge, s);
+      const Slice sw = read_slice(nxt, gw, s);
+      const float dS = quad_sum(dot_slice(own, down));
+      const float dSE = quad_sum(dot_slice(own, se));
+      const float dSW = quad_sum(dot_slice(own, sw));
+      const float rnSE = __shfl(rn_down, (ge << 2) | s);
+      const float rnSW = __shfl(rn_down, (gw << 2) | s);
+      const float cS = has_s ? dS * rn_own * rn_down : 0.0f;
+      const float cSE = has_s && has_e ? dSE * rn_own * rnSE : 0.0f;
+      const float cSW = has_s && has_w ? dSW * rn_own * rnSW : 0.0f;
+      // Cosines owned by the west / east neighbours of this cell.
+      const float cE_w = __shfl(cE, (gw << 2) | s);
+      const float cSE_w = __shfl(cSE, (gw << 2) | s);
+      const float cSW_e = __shfl(cSW, (ge << 2) | s);
+      H = carry + cE + cS + cSE + cSW + (has_w ? cE_w : 0.0f);
+      carry = cS + (has_w ? cSE_w : 0.0f) + (has_e ? cSW_e : 0.0f);
+    } else {
+      carry = 0.0f;  // row r+1 has no admitted cell either
+    }
     const int32_t nrows = 1 + (r > 0 ? 1 : 0) + (has_s ? 1 : 0);
     const int32_t nn = nrows * ncols - 1;
     const bool store = r < R && out_lane && s == 0;
     const uint32_t byte_off = store ? uint32_t(r * C + col) * 4u : frame_bytes;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(nn > 0 ? 1.0f - H * __builtin_amdgcn_rcpf(float(nn)) : 0.0f), phi_rsrc, byte_off,
-                                          0, 0);
-    carry = cS + (has_w ? cSE_w : 0.0f) + (has_e ? cSW_e : 0.0f);
+    const bool zero = nn <= 0 || (GATED && g0 == 0u);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(zero ? 0.0f : 1.0f - H * __builtin_amdgcn_rcpf(float(nn))),
+                                          phi_rsrc, byte_off, 0, 0);
     own = down;
     rn_own = rn_down;
+    g0 = g1;
+    g1 = g2;
+    g2 = g3;
   };
 
   // Row r lives in slot r % 4; unrolled by four so each slot is a distinct
@@ -400,7 +436,10 @@ hipError_t launch_css(const CssArgs& a, hipStream_t stream) {
   if (e != hipSuccess || a.lay.n_frames == 0) return e;
   const int64_t logical = int64_t(a.lay.n_frames) * a.strips;  // a.strips: max over frames of ceil(C / 14)
   const int64_t grid_x = (logical + 7) / 8 * 8;
-  hipLaunchKernelGGL(css_kernel, dim3(unsigned(grid_x), a.lay.n_units), dim3(64), 0, stream, a);
+  if (a.gate)
+    hipLaunchKernelGGL(css_kernel<true>, dim3(unsigned(grid_x), a.lay.n_units), dim3(64), 0, stream, a);
+  else
+    hipLaunchKernelGGL(css_kernel<false>, dim3(unsigned(grid_x), a.lay.n_units), dim3(64), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -376,12 +376,21 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
   return hip_status(launch_score_window(a, static_cast<hipStream_t>(stream)), "score_window launch");
 }
 
-stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, float* phi, void* stream) {
-  return stlite_css_saliency_nbhd(p, 3, k, phi, stream);
+static stlite_status css_common(const stlite_problem* p, int32_t nbhd, const uint16_t* k, const uint8_t* gate,
+                                float* phi, void* stream);
+
+stlite_status stlite_css_saliency(const stlite_problem* p, const uint16_t* k, const uint8_t* gate, float* phi,
+                                  void* stream) {
+  return css_common(p, 3, k, gate, phi, stream);
 }
 
 stlite_status stlite_css_saliency_nbhd(const stlite_problem* p, int32_t nbhd, const uint16_t* k, float* phi,
                                        void* stream) {
+  return css_common(p, nbhd, k, nullptr, phi, stream);
+}
+
+static stlite_status css_common(const stlite_problem* p, int32_t nbhd, const uint16_t* k, const uint8_t* gate,
+                                float* phi, void* stream) {
   if (nbhd != 3 && nbhd != 5 && nbhd != 7 && nbhd != 9)
     return fail(STLITE_ERR_INVALID_ARG, "nbhd must be 3, 5, 7 or 9 (got %d)", int(nbhd));
   stlite_status st = stlite_validate(p);
@@ -391,6 +400,7 @@ stlite_status stlite_css_saliency_nbhd(const stlite_problem* p, int32_t nbhd, co
   CssArgs a;
   a.lay = make_layout(p);
   a.k = k;
+  a.gate = gate;
   a.phi = phi;
   int32_t strips = 1;
   if (nbhd == 3) {
@@ -561,6 +571,7 @@ stlite_status stlite_css_saliency_concat(const stlite_problem* p, const uint16_t
   CssArgs a;
   a.lay = make_layout(p);
   a.k = k;
+  a.gate = nullptr;
   a.phi = phi_layer;
   int32_t strips = 1;
   const int32_t rows = p->n_kv_heads >= 4 ? 1 : 2;  // output rows per wave tile (css_cat_kernel)

@@ -111,6 +111,7 @@ struct GateArgs {
 struct CssArgs {
   Layout lay;
   const uint16_t* k;
+  const uint8_t* gate;   // nullable (3 x 3 only): Phi = 0 where gate == 0
   float* phi;
   int32_t strips;        // largest number of 14-column strips in a frame (3 x 3), or of 4 x 16 tiles (k x k)
 };

@@ -73,7 +73,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_validate": (st, [P]),
         "stlite_workspace_size": (st, [P, st, ctypes.POINTER(sz)]),
         "stlite_score_window": (st, [P, vp, vp, vp, vp, sz, vp]),
-        "stlite_css_saliency": (st, [P, vp, vp, vp]),
+        "stlite_css_saliency": (st, [P, vp, vp, vp, vp]),
         "stlite_tsg_gate": (st, [P, vp, vp, vp, vp, vp, sz, vp]),
         "stlite_tsg_rho": (st, [P, vp, vp, vp, sz, vp]),
         "stlite_tsg_threshold": (st, [P, vp, vp, vp, vp, sz, vp]),
@@ -185,8 +185,9 @@ def stlite_score_window(p: Problem, q_win, k, a_base, workspace, stream=None) ->
                                       _nbytes(workspace), _stream(stream)), "stlite_score_window")
 
 
-def stlite_css_saliency(p: Problem, k, phi, stream=None) -> None:
-    _check(load().stlite_css_saliency(p.ref, _ptr(k), _ptr(phi), _stream(stream)), "stlite_css_saliency")
+def stlite_css_saliency(p: Problem, k, phi, gate=None, stream=None) -> None:
+    _check(load().stlite_css_saliency(p.ref, _ptr(k), _ptr(gate), _ptr(phi), _stream(stream)),
+           "stlite_css_saliency")
 
 
 def stlite_css_saliency_nbhd(p: Problem, nbhd: int, k, phi, stream=None) -> None:
@@ -393,35 +394,35 @@ def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: boo
              tsg: bool = True, stream=None, overlap: bool = False) -> Buffers:
     """The whole pass: score, gate, saliency, select, compact (five C calls).
 
-    With ``overlap`` the three independent steps run concurrently: the window
-    scoring on ``stream``, TSG and CSS on the two side streams of ``out``;
-    the top-B selection waits for all three.  Otherwise everything runs in
-    order on ``stream``.
+    The TSG gate runs before CSS, which skips the tokens the gate leaves out
+    (their Phi is 0; Eq. modal_scoring multiplies it by M = 0 anyway).  With
+    ``overlap`` the window scoring runs on ``stream`` while TSG and then CSS
+    run on a side stream of ``out``; the top-B selection waits for both.
+    Otherwise everything runs in order on ``stream``.
     """
     import torch
     main = stream if stream is not None else torch.cuda.current_stream()
+    gate = out.gate if tsg else None
     if not overlap:
         stlite_score_window(p, q_win, k, out.a_base, out.ws, main)
         if tsg:
             stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws_tsg, main)
         if css:
-            stlite_css_saliency(p, k, out.phi, main)
+            stlite_css_saliency(p, k, out.phi, gate, main)
     else:
-        s_tsg, s_css = out.side
+        side = out.side[0]
         start = torch.cuda.Event()
         start.record(main)
-        for s in (s_tsg, s_css):
-            s.wait_event(start)
-            k.record_stream(s)
+        side.wait_event(start)
+        k.record_stream(side)
         stlite_score_window(p, q_win, k, out.a_base, out.ws, main)
         if tsg:
-            stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws_tsg, s_tsg)
+            stlite_tsg_gate(p, k, out.rho, out.tau, out.gate, out.ws_tsg, side)
         if css:
-            stlite_css_saliency(p, k, out.phi, s_css)
-        for s in (s_tsg, s_css):
-            done = torch.cuda.Event()
-            done.record(s)
-            main.wait_event(done)
+            stlite_css_saliency(p, k, out.phi, gate, side)
+        done = torch.cuda.Event()
+        done.record(side)
+        main.wait_event(done)
     stlite_select_topk(p, out.a_base, out.phi if css else None, out.gate if tsg else None, alpha,
                        out.kept, out.score, out.ws, main)
     stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, main)

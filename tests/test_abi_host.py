@@ -35,7 +35,7 @@ def test_exports_match_header():
     assert set(names) == set(S.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.stlite_abi_version() == 1
+    assert lib.stlite_abi_version() == 2
 
 
 def test_budget_exact():
@@ -137,7 +137,7 @@ def test_calls_fail_before_launch():
                                   None) == S.ERR_INVALID_ARG
     assert lib.stlite_select_topk(ref, FAKE_DEV, None, None, float("nan"), FAKE_DEV, None, FAKE_DEV,
                                   n.value, None) == S.ERR_INVALID_ARG
-    assert lib.stlite_css_saliency(ref, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_css_saliency(ref, None, None, FAKE_DEV, None) == S.ERR_INVALID_ARG
     assert lib.stlite_compact_kv(ref, FAKE_DEV + 8, FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
                                  None) == S.ERR_INVALID_ARG
     assert lib.stlite_tsg_gate(ref, FAKE_DEV, None, None, None, None, 0, None) == S.ERR_WORKSPACE
@@ -146,7 +146,7 @@ def test_calls_fail_before_launch():
     assert n.value > 0
     assert lib.stlite_tsg_rho(ref, FAKE_DEV, None, FAKE_DEV, n.value, None) == S.ERR_INVALID_ARG
     p.c.head_dim = 96
-    assert lib.stlite_css_saliency(ref, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
+    assert lib.stlite_css_saliency(ref, FAKE_DEV, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
     assert lib.stlite_status_string(S.ERR_HIP) == b"STLITE_ERR_HIP"
 
 
