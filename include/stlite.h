@@ -369,6 +369,27 @@ stlite_status stlite_compact_kv_layer(const stlite_problem* p, const uint16_t* k
 stlite_status stlite_kept_overlap(const stlite_problem* p, const int32_t* kept_a,
                                   const int32_t* kept_b, int32_t* hits, void* stream);
 
+/*
+ * stlite_select_topk without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the selection's workspace is a static
+ * device array of STLITE_NOALLOC_SCRATCH_BYTES inside the library, one per
+ * GPU, held from module load until the process ends.  Same arguments, results
+ * and errors as stlite_select_topk; a problem whose selection needs more than
+ * STLITE_NOALLOC_SCRATCH_BYTES (stlite_workspace_size with
+ * STLITE_CALL_SELECT_TOPK) fails with STLITE_ERR_WORKSPACE, nothing enqueued.
+ * The call allocates nothing: on the first call on a device it looks up that
+ * device's copy of the array (hipGetSymbolAddress on the current device, which
+ * must be the device of `stream`).  Every call on one GPU shares that GPU's
+ * array: calls that may overlap on one GPU (other streams, other threads)
+ * race and must be ordered by the caller.
+ */
+#define STLITE_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+stlite_status stlite_select_topk_noalloc(const stlite_problem* p, const float* a_base,
+                                         const float* phi, const uint8_t* gate, float alpha,
+                                         int32_t* kept, float* score, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

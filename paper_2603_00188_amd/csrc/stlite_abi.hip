@@ -213,6 +213,14 @@ size_t decode_bytes(const stlite_problem* p, const DecodePlan& d) {
 
 }  // namespace
 
+namespace stlite {
+
+// Sets the calling thread's stlite_last_error() message for another source
+// file of the library and returns st.
+stlite_status report_error(stlite_status st, const char* msg) { return fail(st, "%s", msg); }
+
+}  // namespace stlite
+
 extern "C" {
 
 int32_t stlite_abi_version(void) { return STLITE_ABI_VERSION; }

@@ -28,6 +28,7 @@ EXPORTS = (
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
     "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma",
     "stlite_layer_mean", "stlite_tsg_rho_concat", "stlite_css_saliency_concat", "stlite_compact_kv_layer",
+    "stlite_select_topk_noalloc",
 )
 
 
@@ -89,6 +90,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_tsg_rho_concat": (st, [P, vp, vp, vp, sz, vp]),
         "stlite_css_saliency_concat": (st, [P, vp, vp, vp]),
         "stlite_compact_kv_layer": (st, [P, vp, vp, vp, vp, vp, vp]),
+        "stlite_select_topk_noalloc": (st, [P, vp, vp, vp, f32, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -225,6 +227,14 @@ def stlite_select_topk(p: Problem, a_base, phi, gate, alpha: float, kept, score,
     _check(load().stlite_select_topk(p.ref, _ptr(a_base), _ptr(phi), _ptr(gate), float(alpha), _ptr(kept),
                                      _ptr(score), _ptr(workspace), _nbytes(workspace), _stream(stream)),
            "stlite_select_topk")
+
+
+def stlite_select_topk_noalloc(p: Problem, a_base, phi, gate, alpha: float, kept, score, stream=None) -> None:
+    _check(load().stlite_select_topk_noalloc(p.ref, _ptr(a_base), _ptr(phi), _ptr(gate), float(alpha), _ptr(kept),
+                                             _ptr(score), _stream(stream)), "stlite_select_topk_noalloc")
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20   # STLITE_NOALLOC_SCRATCH_BYTES
 
 
 def stlite_compact_kv(p: Problem, k, v, kept, k_out, v_out, stream=None) -> None:

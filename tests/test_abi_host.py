@@ -258,3 +258,21 @@ def test_concat_rejections_and_workspace():
     assert lib.stlite_workspace_size(r3, S.CALL_TSG_RHO_CONCAT, ctypes.byref(n3)) == S.OK
     assert lib.stlite_tsg_rho_concat(r3, FAKE_DEV, FAKE_DEV, FAKE_DEV, n3.value, None) == S.ERR_UNSUPPORTED
     assert lib.stlite_css_saliency_concat(r3, FAKE_DEV, FAKE_DEV, None) == S.ERR_UNSUPPORTED
+
+
+def test_noalloc_select_rejects_oversized_problem():
+    """stlite_select_topk_noalloc refuses a problem whose selection workspace
+    exceeds its static buffer, before anything is enqueued (no GPU touched):
+    28 layers x 4 kv heads over one 150,528-token sequence."""
+    lib = S.load()
+    L = 150528
+    p = HostProblem([0, L], [[]], [L // 5], n_layers=28)
+    n = ctypes.c_size_t(0)
+    assert lib.stlite_workspace_size(ctypes.byref(p.c), S.CALL_SELECT_TOPK, ctypes.byref(n)) == S.OK
+    assert n.value > S.NOALLOC_SCRATCH_BYTES
+    st = lib.stlite_select_topk_noalloc(ctypes.byref(p.c), FAKE_DEV, None, None, 1.0, FAKE_DEV, None, None)
+    assert st == S.ERR_WORKSPACE
+    assert "static buffer" in lib.stlite_last_error().decode()
+    p.c.head_dim = 64   # an invalid problem is reported as such first
+    st = lib.stlite_select_topk_noalloc(ctypes.byref(p.c), FAKE_DEV, None, None, 1.0, FAKE_DEV, None, None)
+    assert st == S.ERR_UNSUPPORTED
