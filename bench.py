@@ -344,6 +344,73 @@ def chr_harness(prob, q, dk, a_base, out, stream):
     return entry
 
 
+def multistep_timing(w, inputs, dk, dv, stream, reps=2):
+    """Recompression at every step of the trajectory (problem setup, Eq.
+    history_context): step t compresses its own context, frames 0..t with the
+    text after each (L_t tokens, B_t = floor(beta L_t)), as one problem per step,
+    the way a serving loop calls the library after each step's prefill.  Each
+    step's cache is a copy of the first L_t rows of the resident trajectory,
+    made before its timing starts.  Per step: the whole pass (five calls, HIP
+    events on the launch stream, mean of `reps` after one warm-up) and the
+    cache hit rates of its kept sets and of SnapKV mode against I*, the top-B_t
+    of the step's decode query (not a window query) over its full cache;
+    Eq. chr averages them over the steps and units."""
+    import dataclasses
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    from paper_2603_00188_amd import workload as W
+    si = W.make_step_inputs(w, base=inputs, pack=False)
+    toks, ms, chr_st, chr_sn = [], [], [], []
+    for i, t in enumerate(si.steps):
+        wt = dataclasses.replace(w, seqs=(W.step_prefix_segments(w, t),))
+        lay = W.make_layout(wt)
+        n = lay.total_tokens
+        cu_b = S.budgets(lay.cu_seqlens, *w.beta)
+        p = S.Problem(w.n_layers, w.n_q_heads, w.n_kv_heads, w.window, lay.cu_seqlens, lay.cu_frames,
+                      lay.frame_meta, cu_b)
+        kt = dk[:, :, :n].contiguous()
+        vt = dv[:, :, :n].contiguous()
+        qt = torch.from_numpy(np.ascontiguousarray(si.q[:, i:i + 1]).view(np.int16)).cuda()
+        qd = torch.from_numpy(np.ascontiguousarray(si.q_dec[:, i:i + 1]).view(np.int16)).cuda()
+        o = S.Buffers(p, keep_stages=False)
+        S.compress(p, qt, kt, vt, o, alpha=w.alpha, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            S.compress(p, qt, kt, vt, o, alpha=w.alpha, stream=stream)
+        e1.record(stream)
+        snap = torch.empty_like(o.kept)
+        S.stlite_select_topk(p, o.a_base, None, None, 0.0, snap, None, o.ws, stream)
+        star, _ = S.oracle_set(S.decode_problem(p), qd, kt, stream=stream)
+        h_st = S.kept_overlap(p, o.kept, star, stream=stream)
+        h_sn = S.kept_overlap(p, snap, star, stream=stream)
+        torch.cuda.synchronize()
+        B = int(cu_b[-1])
+        toks.append(n)
+        ms.append(e0.elapsed_time(e1) / reps)
+        chr_st.append(float(h_st.cpu().numpy().mean()) / B if B else float("nan"))
+        chr_sn.append(float(h_sn.cpu().numpy().mean()) / B if B else float("nan"))
+        del kt, vt, o, snap, star
+    mean = lambda r: float(np.mean([x for x in r if x == x]))
+    entry = {
+        "workload": f"{w.name} recompressed at each of its {len(si.steps)} steps; step t: frames 0..t "
+                    f"and their text, one problem per step, beta {w.beta[0]}/{w.beta[1]}",
+        "steps": len(si.steps), "tokens_total": int(sum(toks)), "ms_total": round(float(sum(ms)), 3),
+        "tokens_per_s": round(sum(toks) / (sum(ms) * 1e-3), 1),
+        "per_step": {"tokens": toks, "ms": [round(x, 4) for x in ms],
+                     "tokens_per_s": [round(n / (m * 1e-3), 1) for n, m in zip(toks, ms)]},
+        "chr_st_lite": round(mean(chr_st), 4), "chr_snapkv": round(mean(chr_sn), 4),
+        "chr_per_step_st_lite": [round(x, 4) for x in chr_st],
+        "chr_per_step_snapkv": [round(x, 4) for x in chr_sn],
+        "decode_query": "sum of the step's element keys and of an earlier frame's changed region, plus noise",
+    }
+    log(f"multi-step: {entry['steps']} steps, {entry['tokens_total']} tokens in {entry['ms_total']:.2f} ms "
+        f"({entry['tokens_per_s'] / 1e6:.2f} M tokens/s); CHR ST-Lite {entry['chr_st_lite']:.4f}, "
+        f"SnapKV mode {entry['chr_snapkv']:.4f}")
+    return entry
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -500,6 +567,9 @@ def main():
     result["variants"] = variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream)
     step()  # the pass's kept sets again (the variants overwrote phi and gate)
     result["chr"] = chr_harness(prob, q, dk, out.a_base, out, stream)
+    if lay.n_seqs == 1 and len(lay.frame_meta) > 1:
+        del out, rho
+        result["multistep"] = multistep_timing(w, inputs, dk, dv, stream)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host (cpu baseline)")
         result["cpu_baseline"] = cpu_baseline(w, inputs)

@@ -28,6 +28,10 @@ takes them:
                    query's attention over the full cache      (Eq. chr)
   compress_layer_concat  the procedure over the layer's concatenated
                    key space, one kept set per layer          (problem setup; R3b)
+  recompress_steps the procedure at every step t of one trajectory, on step
+                   t's own context (frames 0..t and their text), with the
+                   per-step cache hit rates                   (Eq. history_context, Eq. chr)
+  trajectory_cache_hit_rate  (1/T) sum_t of the per-step rates      (Eq. chr)
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -54,6 +58,9 @@ Readings where the paper is silent (each is also listed in the design notes):
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
   R11 no forced keep of the window; R13 gated-out visual tokens score 0;
   R16 I_keep is emitted in ascending token order;
+  R-step recompression along a trajectory: step t compresses its own full
+      prefill cache (frames 0..t and the text after each, B_t = floor(beta L_t)),
+      with no reuse of an earlier step's compacted cache;
   R-dec ranking decisions (gate admission, top-B) are taken on the scores
       rounded to float32, the precision the GPU kernels compute them in; ties
       go to the lowest token index.
@@ -406,6 +413,47 @@ def cache_hit_rate(kept: np.ndarray, oracle: np.ndarray) -> float:
     if len(oracle) == 0:
         return float("nan")
     return len(np.intersect1d(kept, oracle)) / len(oracle)
+
+
+def trajectory_cache_hit_rate(rates: Sequence[float]) -> float:
+    """Eq. chr: the mean over the T evaluation steps of the per-step hit rates
+    |I_keep^(t) cap I*^(t)| / |I*^(t)|.  Steps whose oracle set is empty (B_t = 0,
+    rate NaN) are not evaluation steps and are left out; NaN if none is left."""
+    r = [float(x) for x in rates if not math.isnan(float(x))]
+    if not r:
+        return float("nan")
+    return sum(r) / len(r)
+
+
+def recompress_steps(q_steps, q_dec_steps, k_bits, v_bits, frames: Sequence[Tuple[int, int, int]],
+                     frame_ends: Sequence[int], steps: Sequence[int], beta, alpha=1.0) -> Dict:
+    """The procedure at each listed step of one trajectory, for one unit (reading R-step).
+
+    The trajectory's context at step t (Eq. history_context) is every token
+    before frame t + 1: frames 0..t with the text after each, L_t = frame_ends[t]
+    tokens, and its cache is the first L_t rows of the trajectory's keys and
+    values.  Frame t is that step's current frame.  Each step is compressed on
+    its own (compress_unit) at budget B_t = floor(beta * L_t); its oracle set
+    I*^(t) is the top-B_t of its decode query's attention over those L_t rows.
+
+    q_steps [T, G, delta, d] and q_dec_steps [T, G, d] (bf16 bits) are the
+    window queries and decode queries of the listed steps; k_bits, v_bits
+    [L, d] are the whole trajectory's rows; frames are (offset, rows, cols)
+    local to it.  Returns the per-step outputs and cache hit rates and their
+    Eq. chr mean.
+    """
+    outs, rates = [], []
+    for i, t in enumerate(steps):
+        L_t = int(frame_ends[t])
+        out = compress_unit(q_steps[i], k_bits[:L_t], v_bits[:L_t], list(frames[:t + 1]), beta, alpha)
+        a_dec = decode_attention_scores(bf16_to_f64(q_dec_steps[i]), bf16_to_f64(k_bits[:L_t]))
+        star = chr_oracle_set(a_dec, out["B"])
+        out["a_dec"] = a_dec
+        out["star"] = star
+        out["chr"] = cache_hit_rate(out["kept"], star)
+        outs.append(out)
+        rates.append(out["chr"])
+    return dict(steps=outs, rates=rates, chr=trajectory_cache_hit_rate(rates))
 
 
 def seq_frames_local(cu_seqlens, cu_frames, frame_meta, s: int):

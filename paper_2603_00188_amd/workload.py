@@ -400,3 +400,133 @@ def decode_queries(q: np.ndarray) -> np.ndarray:
     position, i.e. the query the model formed at the end of prefill, which the
     first decode step's query resembles."""
     return np.ascontiguousarray(q[:, :, :, -1, :])
+
+
+# ---------------------------------------------------------------------------
+# Recompression at every step of one trajectory
+# ---------------------------------------------------------------------------
+
+STEP_STREAM = 0x57E95   # spawn key of the per-step draws (elements, anchors, query noise)
+
+
+@dataclasses.dataclass
+class StepInputs:
+    """The caches of the steps of one trajectory, packed one sequence per step.
+
+    Step t's context is the trajectory's prefix up to and including the text
+    that follows frame t (problem setup, Eq. history_context: the earlier
+    screenshots and actions, then the current screenshot); frame t is that
+    step's current frame.  Keys and values of a prefix are the trajectory's own
+    rows (causal attention leaves a prefix's cache unchanged), so sequence t of
+    the packed batch is a copy of rows 0 .. L_t - 1.
+
+    Window queries of step t aim at an element rectangle of frame t.  The
+    decode query of step t (first action token) is not one of the window
+    queries: it sums the keys of the same element and of an anchor rectangle of
+    an earlier frame whose content has since changed (a distant token the
+    current screen no longer shows), plus noise.
+    """
+
+    base: Workload
+    steps: List[int]
+    workload: Workload        # the packed batch (one sequence per step)
+    layout: Layout
+    k: Optional[np.ndarray]   # [nl, Hkv, sum L_t, d] bf16 bits (None unless packed)
+    v: Optional[np.ndarray]
+    q: np.ndarray             # [nl, T, Hq, window, d]
+    q_dec: np.ndarray         # [nl, T, Hq, d]
+    element: List[Tuple[int, int, int, int]]        # per step, in frame t
+    anchor: List[Optional[Tuple[int, int, int, int, int]]]  # per step: (frame, u0, v0, h, w) or None
+
+
+def step_prefix_segments(w: Workload, t: int) -> Tuple[Tuple, ...]:
+    """Segments of step t's context: everything before frame t + 1."""
+    segs = w.seqs[0]
+    frames = [i for i, s in enumerate(segs) if s[0] == FRAME]
+    end = frames[t + 1] if t + 1 < len(frames) else len(segs)
+    return tuple(segs[:end])
+
+
+def make_step_inputs(w: Workload, steps: Optional[Sequence[int]] = None,
+                     layers: Optional[Sequence[int]] = None, base=None, pack: bool = True) -> StepInputs:
+    """Inputs of the recompression at the listed steps (default: every frame)
+    of the single trajectory of ``w``.  ``base`` = make_inputs(w, layers) may be
+    passed to reuse already drawn caches.  With pack=False the packed k and v
+    are not built (None): the caller slices each step's rows from the
+    trajectory's own arrays."""
+    if len(w.seqs) != 1:
+        raise ValueError("make_step_inputs takes a single-trajectory workload")
+    scene, kb, vb, _ = make_inputs(w, layers) if base is None else base
+    lay0 = scene.layout
+    fm = lay0.seq_frames(0)
+    nf = len(fm)
+    steps = list(range(nf)) if steps is None else [int(t) for t in steps]
+    if not steps or min(steps) < 0 or max(steps) >= nf:
+        raise ValueError("steps must index frames of the trajectory")
+    packed = dataclasses.replace(w, seqs=tuple(step_prefix_segments(w, t) for t in steps))
+    lay = make_layout(packed)
+    lens = np.diff(lay.cu_seqlens)
+    if (lens < w.window).any():
+        raise ValueError("every step's context must hold the observation window")
+    layers = list(range(w.n_layers)) if layers is None else list(layers)
+    nl, hk, d, G = len(layers), w.n_kv_heads, w.head_dim, w.group
+    L = lay.total_tokens
+    k = v = None
+    if pack:
+        k = np.empty((nl, hk, L, d), np.uint16)
+        v = np.empty_like(k)
+        for i, t in enumerate(steps):
+            a, n = int(lay.cu_seqlens[i]), int(lens[i])
+            k[:, :, a:a + n] = kb[:, :, :n]
+            v[:, :, a:a + n] = vb[:, :, :n]
+
+    # per-step element and anchor rectangles (layer independent); every step,
+    # and every (step, layer), has a stream of its own, so a step regenerates
+    # alone whatever other steps are listed
+    (hlo, hhi), (wlo, whi) = w.element
+    elems, anchors = [], []
+    for t in steps:
+        rng = _rng(np.random.SeedSequence([w.seed, STEP_STREAM, t]))
+        r, c = int(fm[t, 1]), int(fm[t, 2])
+        h = int(rng.integers(hlo, hhi + 1))
+        ww = int(rng.integers(wlo, whi + 1))
+        elems.append(_random_rect(rng, r, c, h, ww))
+        anchor = None
+        if t > 0:
+            f = int(rng.integers(0, t))
+            ef, et = scene.frame_emb[f], scene.frame_emb[t]
+            if ef.shape == et.shape:
+                changed = np.flatnonzero((ef != et).any(axis=1))
+                rf, cf = int(fm[f, 1]), int(fm[f, 2])
+                if len(changed):
+                    p = int(changed[int(rng.integers(0, len(changed)))])
+                    h = min(int(rng.integers(hlo, hhi + 1)), rf)
+                    ww = min(int(rng.integers(wlo, whi + 1)), cf)
+                    u0 = min(max(p // cf - h // 2, 0), rf - h)
+                    v0 = min(max(p % cf - ww // 2, 0), cf - ww)
+                    anchor = (f, u0, v0, h, ww)
+        anchors.append(anchor)
+
+    def cells(frame, u0, v0, h, ww):
+        off, _, c = (int(x) for x in fm[frame])
+        return np.array([off + (u0 + i) * c + (v0 + j) for i in range(h) for j in range(ww)])
+
+    q = np.empty((nl, len(steps), w.n_q_heads, w.window, d), np.uint16)
+    q_dec = np.empty((nl, len(steps), w.n_q_heads, d), np.uint16)
+    k32 = lambda li, h, idx: bf16_bits_to_f32(kb[li, h, idx])
+    for li in range(nl):
+        for i, t in enumerate(steps):
+            lrng = _rng(np.random.SeedSequence([w.seed, STEP_STREAM, t, layers[li] + 1]))
+            el = cells(t, *elems[i])
+            an = cells(*anchors[i]) if anchors[i] is not None else None
+            noise = lrng.standard_normal((w.n_q_heads, w.window + 1, d), dtype=np.float32) * np.float32(0.1)
+            qs = np.empty((w.n_q_heads, w.window, d), np.float32)
+            qd = np.empty((w.n_q_heads, d), np.float32)
+            for g in range(w.n_q_heads):
+                target = k32(li, g // G, el).sum(axis=0)
+                qs[g] = target[None, :] + noise[g, :w.window]
+                extra = k32(li, g // G, an).sum(axis=0) if an is not None else 0.0
+                qd[g] = target + extra + noise[g, w.window]
+            q[li, i] = to_bf16_bits(qs)
+            q_dec[li, i] = to_bf16_bits(qd)
+    return StepInputs(w, steps, packed, lay, k, v, q, q_dec, elems, anchors)

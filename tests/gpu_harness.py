@@ -42,11 +42,16 @@ def log(msg: str):
 class Case:
     """Seeded inputs of one workload, on the host and on the device."""
 
-    def __init__(self, w: W.Workload, layers=None, device="cuda"):
+    def __init__(self, w: W.Workload, layers=None, device="cuda", inputs=None):
+        """inputs = (layout, k, v, q) of already drawn arrays (e.g. the per-step
+        batch of W.make_step_inputs, whose ``workload`` is then ``w``)."""
         import torch
         self.w = w
-        self.scene, self.k, self.v, self.q = W.make_inputs(w, layers)
-        self.lay = self.scene.layout
+        if inputs is None:
+            scene, self.k, self.v, self.q = W.make_inputs(w, layers)
+            self.lay = scene.layout
+        else:
+            self.lay, self.k, self.v, self.q = inputs
         self.n_layers = self.k.shape[0]
         self.cu_budget = S.budgets(self.lay.cu_seqlens, *w.beta)
         self.prob = S.Problem(self.n_layers, w.n_q_heads, w.n_kv_heads, w.window, self.lay.cu_seqlens,

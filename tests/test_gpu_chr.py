@@ -38,15 +38,20 @@ def _mods():
     return O, S, H, SMALL
 
 
-def run_chr(case):
-    """Kept sets of ST-Lite and of SnapKV mode, I*, and both hit counts, on the GPU."""
+def run_chr(case, q_dec_bits=None):
+    """Kept sets of ST-Lite and of SnapKV mode, I*, and both hit counts, on the GPU.
+    q_dec_bits [layers][seqs][Hq][d]: the decode queries (default: each head's
+    last window query)."""
     import torch
     O, S, H, _ = _mods()
     res = case.run()
     out = case.out
     snap = torch.empty_like(out.kept)
     S.stlite_select_topk(case.prob, out.a_base, None, None, 0.0, snap, None, out.ws)
-    q_dec = torch.from_numpy(np.ascontiguousarray(W.decode_queries(case.q)).view(np.int16)).cuda()
+    if q_dec_bits is None:
+        q_dec_bits = W.decode_queries(case.q)
+    q_dec_bits = np.ascontiguousarray(q_dec_bits)
+    q_dec = torch.from_numpy(q_dec_bits.view(np.int16)).cuda()
     p1 = S.decode_problem(case.prob)
     star, _ = S.oracle_set(p1, q_dec, case.dk)
     hits_st = S.kept_overlap(case.prob, out.kept, star)
@@ -54,7 +59,7 @@ def run_chr(case):
     torch.cuda.synchronize()
     Bt = case.prob.total_budget
     return dict(res=res, snap=snap[:, :Bt].cpu().numpy(), star=star[:, :Bt].cpu().numpy(),
-                hits_st=hits_st.cpu().numpy(), hits_sn=hits_sn.cpu().numpy())
+                hits_st=hits_st.cpu().numpy(), hits_sn=hits_sn.cpu().numpy(), q_dec=q_dec_bits)
 
 
 def check_chr_unit(case, r, layer, kv, s, ref=None):
@@ -76,7 +81,7 @@ def check_chr_unit(case, r, layer, kv, s, ref=None):
     if B == 0:
         return {}
     # I* against the oracle's top-B of the decode attention
-    Qd = O.bf16_to_f64(W.decode_queries(case.q)[layer, s, kv * w.group:(kv + 1) * w.group])
+    Qd = O.bf16_to_f64(r["q_dec"][layer, s, kv * w.group:(kv + 1) * w.group])
     K = O.bf16_to_f64(case.k[layer, kv, a:b])
     a_dec = O.decode_attention_scores(Qd, K)
     star_ref = O.chr_oracle_set(a_dec, B)

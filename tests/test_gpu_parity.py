@@ -285,8 +285,8 @@ def _full(idx, beta=None, samples=((0, 0, 0), (27, 3, 0))):
 @pytest.mark.timeout(900)
 def test_config2_sampled(torch_cuda):
     H = _H()
-    case, res = _full(2, (1, 5), samples=((3, 1, 0),))
-    for beta in ((1, 10), (2, 5)):
+    case, res = _full(2, (1, 5), samples=((3, 1, 0), (20, 3, 0)))
+    for beta, units in (((1, 10), ((14, 2), (27, 0))), ((2, 5), ((14, 2), (0, 3)))):
         import dataclasses as dc
         w = dc.replace(case.w, beta=beta)
         case2 = H.Case.__new__(H.Case)
@@ -298,8 +298,9 @@ def test_config2_sampled(torch_cuda):
                                case.lay.cu_frames, case.lay.frame_meta, case2.cu_budget)
         case2.out = S.Buffers(case2.prob)
         res2 = case2.run()
-        st = H.compare_unit(case2, res2, 14, 2, 0)
-        H.log(f"config 2 beta {beta}: {st}")
+        for layer, kv in units:
+            st = H.compare_unit(case2, res2, layer, kv, 0)
+            H.log(f"config 2 beta {beta} unit ({layer},{kv},0): {st}")
 
 
 @pytest.mark.timeout(900)
@@ -307,9 +308,11 @@ def test_config3_sampled(torch_cuda):
     """The 150,528-token trajectory in the benchmark's launch configuration,
     and decode attention over its full and compacted caches."""
     H = _H()
-    case, res = _full(3)
+    # first, last and middle layers; every kv head twice
+    samples = ((0, 0, 0), (4, 1, 0), (9, 2, 0), (13, 3, 0), (14, 0, 0), (18, 1, 0), (23, 2, 0), (27, 3, 0))
+    case, res = _full(3, samples=samples)
     dec = H.run_decode(case)
-    for unit in ((0, 0, 0), (13, 2, 0), (27, 3, 0)):
+    for unit in samples:
         H.log(f"config 3 decode unit {unit}: worst error / tolerance {H.compare_decode(case, res, dec, *unit):.3g}")
 
 
@@ -317,7 +320,8 @@ def test_config3_sampled(torch_cuda):
 def test_config4_sampled(torch_cuda):
     """The ragged batch of 8 trajectories, and decode attention over its caches."""
     H = _H()
-    samples = ((0, 0, 0), (13, 2, 4), (27, 3, 7))
+    # four units spread over layers and kv heads, each compared on all 8 sequences
+    samples = tuple((layer, kv, s) for layer, kv in ((0, 0), (7, 1), (13, 2), (27, 3)) for s in range(8))
     case, res = _full(4, samples=samples)
     dec = H.run_decode(case)
     for unit in samples:

@@ -838,3 +838,101 @@ def test_compress_sequence_packed_batch_matches_hand_slices():
     Qi = np.stack([Qf[0, 0, kv_g] for kv_g in (1, 1 + Hkv)])
     Qc = np.stack([Qf[0, 0, 1 * G + g] for g in range(G)])
     assert not np.array_equal(Qi, Qc)
+
+
+# ------------------------------------------------- recompression per step ----
+
+def test_trajectory_cache_hit_rate_average_by_hand():
+    """Eq. chr averages the per-step rates over the T steps: hit rates 1/2, 1/3
+    and 3/3 average to (1/2 + 1/3 + 1) / 3 = 11/18; a step with an empty oracle
+    set (B = 0) is not an evaluation step."""
+    rates = [O.cache_hit_rate(np.array([1, 4]), np.array([1, 2])),          # 1 of 2
+             O.cache_hit_rate(np.array([0, 5, 9]), np.array([5, 6, 7])),    # 1 of 3
+             O.cache_hit_rate(np.array([2, 3, 8]), np.array([2, 3, 8]))]    # 3 of 3
+    assert rates == [0.5, 1 / 3, 1.0]
+    assert O.trajectory_cache_hit_rate(rates) == pytest.approx(11 / 18, abs=1e-15)
+    empty = O.cache_hit_rate(np.array([], int), np.array([], int))
+    assert O.trajectory_cache_hit_rate(rates + [empty]) == pytest.approx(11 / 18, abs=1e-15)
+    assert math.isnan(O.trajectory_cache_hit_rate([empty]))
+    assert O.trajectory_cache_hit_rate([Fraction(1, 4), 0.75]) == 0.5
+
+
+def _trajectory_fixture(seed=7):
+    """A hand-built trajectory: 4 frames of 2 x 3 patches, 3 text tokens after
+    each, keys with a frame copied forward (the snap class), per-step window
+    queries (G = 2, delta = 3) and decode queries; exact bf16 values."""
+    rng = np.random.default_rng(seed)
+    d, G, delta, nf, R, C, T = 128, 2, 3, 4, 2, 3, 3
+    frames = [(f * (R * C + T), R, C) for f in range(nf)]
+    L = nf * (R * C + T)
+    coarse = lambda *shape: np.round(rng.standard_normal(shape) * 8) / 64.0
+    K, V = coarse(L, d), coarse(L, d)
+    K[frames[2][0]:frames[2][0] + 6] = K[frames[1][0]:frames[1][0] + 6]   # frame 2 repeats frame 1
+    K[frames[3][0] + 4] = K[frames[0][0] + 1]                             # a patch seen in frame 0 returns
+    Qs = coarse(nf, G, delta, d)
+    Qd = coarse(nf, G, d)
+    ends = [o + R * C + T for o, _, _ in frames]
+    return frames, ends, K, V, Qs, Qd, G
+
+
+def test_recompress_steps_each_step_is_its_own_prefix():
+    """Step t is the procedure on the first L_t = (t + 1)(R C + text) rows with
+    frames 0..t (frame t current): the same as compress_unit and the literal
+    twin on that prefix sliced by hand; its oracle set is the top-B_t of the
+    literal decode attention over the prefix, and its rate a plain count."""
+    frames, ends, K, V, Qs, Qd, G = _trajectory_fixture()
+    beta = (1, 3)
+    steps = [0, 1, 2, 3]
+    got = O.recompress_steps(_bits(Qs), _bits(Qd), _bits(K), _bits(V), frames, ends, steps, beta)
+    rates = []
+    for i, t in enumerate(steps):
+        L_t = (t + 1) * 9
+        assert ends[t] == L_t
+        fr = frames[:t + 1]
+        ref = O.compress_unit(_bits(Qs[t]), _bits(K[:L_t]), _bits(V[:L_t]), fr, beta)
+        g = got["steps"][i]
+        assert g["B"] == L_t // 3 == ref["B"]
+        np.testing.assert_array_equal(g["kept"], ref["kept"])
+        np.testing.assert_array_equal(g["A"], ref["A"])
+        lit = O1.compress([[list(map(float, r)) for r in Qs[t, h]] for h in range(G)],
+                          [list(map(float, r)) for r in K[:L_t]], fr, L_t // 3)
+        assert g["kept"].tolist() == lit["kept"]
+        assert g["gate"].tolist() == lit["gate"]
+        if t == 0:
+            assert (g["gate"] == 1).all(), "a single frame has no history: TSG is a no-op"
+        a_lit = O1.decode_scores([list(map(float, Qd[t, h])) for h in range(G)],
+                                 [list(map(float, r)) for r in K[:L_t]])
+        star = O1.top_b(a_lit, L_t // 3)
+        assert g["star"].tolist() == star
+        hits = sum(1 for x in star if x in set(lit["kept"]))
+        assert g["chr"] == hits / len(star)
+        rates.append(hits / len(star))
+    assert got["rates"] == rates
+    assert got["chr"] == pytest.approx(sum(rates) / len(rates), abs=1e-15)
+
+
+def test_recompress_steps_packed_batch_equals_single_runs():
+    """The steps packed as one varlen batch (sequence i = the prefix of step
+    steps[i], frames with absolute offsets) give, through compress_sequence,
+    exactly the single-step runs; the last step is the whole trajectory."""
+    frames, ends, K, V, Qs, Qd, G = _trajectory_fixture(8)
+    beta = (2, 5)
+    steps = [1, 3, 2]
+    single = O.recompress_steps(_bits(Qs[steps]), _bits(Qd[steps]), _bits(K), _bits(V), frames, ends,
+                                steps, beta)
+    lens = [ends[t] for t in steps]
+    cu_seqlens = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    cu_frames = np.concatenate([[0], np.cumsum([t + 1 for t in steps])]).astype(np.int32)
+    frame_meta = np.array([(int(cu_seqlens[i]) + o, r, c) for i, t in enumerate(steps)
+                           for (o, r, c) in frames[:t + 1]], np.int32)
+    Kp = np.concatenate([K[:n] for n in lens])[None, None]       # [1 layer, 1 kv head, sum L, d]
+    Vp = np.concatenate([V[:n] for n in lens])[None, None]
+    Qp = Qs[steps][None]                                          # [1 layer, steps, G heads, delta, d]
+    for i, t in enumerate(steps):
+        got = O.compress_sequence(_bits(Qp), _bits(Kp), _bits(Vp), cu_seqlens, cu_frames, frame_meta, i,
+                                  0, 0, G, beta)
+        ref = single["steps"][i]
+        for key in ("A", "phi", "rho", "gate", "S", "kept", "k_out", "v_out"):
+            np.testing.assert_array_equal(got[key], ref[key], err_msg=f"step {t} {key}")
+    whole = O.compress_unit(_bits(Qs[3]), _bits(K), _bits(V), frames, beta)
+    np.testing.assert_array_equal(single["steps"][1]["kept"], whole["kept"])

@@ -60,3 +60,42 @@ def test_bf16_rounding_is_rne():
     assert (got[:512] & 1 == 0).all()
     back = W.bf16_bits_to_f32(got)
     assert (np.abs(back - x) <= np.abs(x) * 2.0 ** -8).all()
+
+
+def test_step_inputs_are_prefixes_of_the_trajectory():
+    """Sequence i of the per-step batch is the trajectory's first L_t rows
+    (frames 0..t and the text after each), frame t is its current frame, and
+    the draws are deterministic and per step (a step regenerates alone); anchors lie on patches that changed between
+    their frame and the step's current frame."""
+    w = W.config(0)
+    base = W.make_inputs(w)
+    si = W.make_step_inputs(w, base=base)
+    scene, kb, vb, _ = base
+    fm0 = scene.layout.seq_frames(0)
+    assert si.steps == [0, 1, 2]
+    ends = list(fm0[1:, 0]) + [scene.layout.total_tokens]
+    assert list(np.diff(si.layout.cu_seqlens)) == ends
+    for i, t in enumerate(si.steps):
+        a, n = int(si.layout.cu_seqlens[i]), ends[t]
+        assert np.array_equal(si.k[:, :, a:a + n], kb[:, :, :n])
+        assert np.array_equal(si.v[:, :, a:a + n], vb[:, :, :n])
+        fr = si.layout.seq_frames(i)
+        assert len(fr) == t + 1
+        assert np.array_equal(fr[:, 0] - a, fm0[:t + 1, 0]) and np.array_equal(fr[:, 1:], fm0[:t + 1, 1:])
+        if si.anchor[i] is not None:
+            f, u0, v0, h, ww = si.anchor[i]
+            assert f < t
+            c = int(fm0[f, 2])
+            cells = [(u0 + x) * c + (v0 + y) for x in range(h) for y in range(ww)]
+            ef, et = scene.frame_emb[f][cells], scene.frame_emb[t][cells]
+            assert (ef != et).any(axis=1).any(), "the anchor shows content the current frame lost"
+    assert si.anchor[0] is None
+    again = W.make_step_inputs(w, base=base)
+    assert np.array_equal(si.q, again.q) and np.array_equal(si.q_dec, again.q_dec)
+    # the decode query is not one of the window queries
+    for i in range(len(si.steps)):
+        for g in range(w.n_q_heads):
+            assert not (si.q[0, i, g] == si.q_dec[0, i, g][None, :]).all(axis=1).any()
+    sub = W.make_step_inputs(w, steps=[2, 0], base=base)
+    assert np.array_equal(sub.q[:, 0], si.q[:, 2]) and np.array_equal(sub.q_dec[:, 1], si.q_dec[:, 0])
+    assert list(np.diff(sub.layout.cu_seqlens)) == [ends[2], ends[0]]
