@@ -211,7 +211,8 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
     """The paper's ablation variants on the same workload, each timed apart
     (HIP events on the launch stream) against its own roofline: rho under the
     dot product and the negative L2 distance (the rho contraction's work),
-    the fixed-threshold gate (rho of the history read, the gate written) and
+    the fixed-threshold gate (rho of the history read, the gate written), the
+    Mean-Attention prior (A_base read, the pooled prior written) and
     CSS over 5x5, 7x7 and 9x9 neighbourhoods (every visual key read once and
     Phi written; the (k^2 - 1)/2 cosines per token are far below the MFMA
     roofline at these sizes)."""
@@ -243,6 +244,9 @@ def variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream, reps=10):
     entry["tsg_fixed_gate"] = roofline_entry(model["tsg_threshold"], ms)
     ms = timed(lambda: S.stlite_css_saliency(prob, dk, out.phi, None, stream))
     entry["css_saliency_ungated"] = roofline_entry(model["css_saliency"], ms)
+    # Mean-Attention prior (pooling width 7): A_base read, A_mean written
+    ms = timed(lambda: S.stlite_mean_attention(prob, out.a_base, 7, tmp, stream))
+    entry["mean_attention_w7"] = roofline_entry({"bound": "hbm", "bytes": units * 8.0 * lay.total_tokens}, ms)
     for k in (5, 7, 9):
         ms = timed(lambda: S.stlite_css_saliency_nbhd(prob, k, dk, out.phi, stream))
         e = roofline_entry({"bound": "hbm", "bytes": model["css_saliency"]["bytes"]}, ms)

@@ -21,6 +21,8 @@
  *
  * the variants of the paper's ablations,
  *
+ *   stlite_mean_attention    the Mean-Attention base prior: A_base pooled along
+ *                            the sequence (base scoring function ablation)
  *   stlite_tsg_similarity    rho under the dot product or -L2 (similarity ablation)
  *   stlite_tsg_fixed_gate    gate = 1[rho <= tau] for a fixed tau (necessity controls)
  *   stlite_css_saliency_nbhd CSS over 5x5, 7x7, 9x9 windows (neighbourhood ablation)
@@ -353,6 +355,32 @@ stlite_status stlite_css_saliency_concat(const stlite_problem* p, const uint16_t
 stlite_status stlite_compact_kv_layer(const stlite_problem* p, const uint16_t* k, const uint16_t* v,
                                       const int32_t* kept_layer, uint16_t* k_out, uint16_t* v_out,
                                       void* stream);
+
+/*
+ * The Mean-Attention base prior of the paper's base-scoring ablation (appendix
+ * "Sensitivity to the Base Attention Scoring Function": one-dimensional
+ * average pooling of the attention over the prompt sequence).  Reading: the
+ * window-aggregated A_base that stlite_score_window writes (Eq. base_attention,
+ * so the prior keeps its dependence on the observation window) is averaged
+ * along each sequence's token axis over a centred window of `width` positions;
+ * positions outside the sequence count as 0 and the divisor is always width:
+ *
+ *   a_mean[i] = (1/width) * sum_{j = i-r .. i+r, j inside i's sequence} a_base[j],
+ *   r = (width - 1) / 2.
+ *
+ * The pooling runs over every token (text and visual alike) and never crosses
+ * from one packed sequence into the next.  a_mean then takes A_base's place in
+ * stlite_select_topk.
+ *
+ * a_base, a_mean  fp32 [n_layers][n_kv_heads][total_tokens]; a_mean must not
+ *                 alias a_base; every element of a_mean is written.
+ * width           odd, 1 <= width <= 255 (width 1 copies a_base).
+ * Errors: STLITE_ERR_INVALID_ARG for a NULL or aliased pointer or a width
+ * outside the range, nothing enqueued; STLITE_ERR_HIP for a failed launch.
+ * No workspace.
+ */
+stlite_status stlite_mean_attention(const stlite_problem* p, const float* a_base, int32_t width,
+                                    float* a_mean, void* stream);
 
 /*
  * Cache hit rate numerator (Sec. cache hit rate evaluation, Eq. chr):

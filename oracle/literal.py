@@ -13,6 +13,7 @@ so that a vectorisation slip in the NumPy oracle shows up as a disagreement:
               -||k_i - k_j|| in place of the cosine (similarity-metric ablation; R8b)
   gate      = the m = min(B, |pool|) smallest rho by (rho, index)       (Eqs. budget_threshold,
                                                                         temporal_mask; R7)
+  A_mean_i  = (1/w) sum_{|j - i| <= (w-1)/2, 0 <= j < L} A_j  (Mean-Attention prior; R-mean)
   S         = A (text) | M (A + alpha Phi) (visual)  (Eq. modal_scoring)
   I_keep    = first B by (S descending, index ascending), ascending  (Top_B; R16)
   out_g     = sum_j exp(z_gj) v_j / sum_j exp(z_gj), z = q_g . k_j / sqrt(d)
@@ -142,9 +143,25 @@ def top_b(S, B):
     return sorted(ranked[:B])
 
 
-def compress(Q, K, frames, B, alpha=1.0, use_css=True, use_tsg=True):
+def mean_pool(A, width):
+    """(1/width) sum of A over the centred window of width positions, the
+    positions outside 0..L-1 counting as 0."""
+    r = (width - 1) // 2
+    out = []
+    for i in range(len(A)):
+        acc = 0.0
+        for j in range(i - r, i + r + 1):
+            if 0 <= j < len(A):
+                acc += A[j]
+        out.append(acc / width)
+    return out
+
+
+def compress(Q, K, frames, B, alpha=1.0, use_css=True, use_tsg=True, mean_width=0):
     L = len(K)
     A = base_score(Q, K)
+    if mean_width:
+        A = mean_pool(A, mean_width)
     hist, cur, visual = partition(L, frames)
     phi = css(K, frames) if use_css else [0.0] * L
     r = rho(K, hist, cur)

@@ -12,6 +12,9 @@ takes them:
 
   budget           B = floor(beta * L)                      (problem setup)
   base_score       A_base, window voting of softmax rows      (Eq. base_attention)
+  mean_attention   the Mean-Attention base prior: 1D average
+                   pooling of A_base along the sequence       (appendix on the base
+                                                               scoring function; R-mean)
   css_saliency     H = mean Moore-neighbour cosine, Phi = 1-H (Eq. css_calc, Sec. CSS);
                    k x k neighbourhoods for the neighbourhood-size ablation
   tsg_rho          rho_i = max cosine to the current frame    (Sec. TSG)
@@ -58,6 +61,10 @@ Readings where the paper is silent (each is also listed in the design notes):
   R9  beta is a rational num/den and B = floor(L*num/den) in integers;
   R11 no forced keep of the window; R13 gated-out visual tokens score 0;
   R16 I_keep is emitted in ascending token order;
+  R-mean the Mean-Attention base prior is the window-aggregated A_base of
+      Eq. base_attention averaged over a centred window of `width` (odd)
+      positions along the sequence's token axis, zero outside the sequence,
+      divided by width (pooling with zero padding and a fixed divisor);
   R-step recompression along a trajectory: step t compresses its own full
       prefill cache (frames 0..t and the text after each, B_t = floor(beta L_t)),
       with no reuse of an earlier step's compacted cache;
@@ -138,6 +145,21 @@ def base_score(Q: np.ndarray, K: np.ndarray, row_chunk: int = 64) -> np.ndarray:
 # ---------------------------------------------------------------------------
 # Cosine helper (R6)
 # ---------------------------------------------------------------------------
+
+def mean_attention(A: np.ndarray, width: int) -> np.ndarray:
+    """Mean-Attention base prior (appendix on the base scoring function,
+    reading R-mean): A_mean_i = (1/width) sum_{j=i-r}^{i+r} A_j with r = (width-1)/2
+    and A_j = 0 for j outside the sequence (0..L-1).  width odd, >= 1."""
+    if width < 1 or width % 2 == 0:
+        raise ValueError("width must be odd and >= 1")
+    A = np.asarray(A, dtype=np.float64)
+    L = len(A)
+    r = (width - 1) // 2
+    out = np.zeros(L)
+    for i in range(L):
+        out[i] = A[max(i - r, 0):min(i + r, L - 1) + 1].sum() / width
+    return out
+
 
 def _cos_matrix(X: np.ndarray, Y: np.ndarray) -> np.ndarray:
     nx = np.sqrt((X * X).sum(axis=1))
@@ -333,17 +355,21 @@ def compact(K_bits: np.ndarray, V_bits: np.ndarray, kept: np.ndarray):
 
 def compress_unit(Q_bits: np.ndarray, K_bits: np.ndarray, V_bits: np.ndarray,
                   frames: Sequence[Tuple[int, int, int]], beta: Tuple[int, int],
-                  alpha: float = 1.0, use_css: bool = True, use_tsg: bool = True) -> Dict:
+                  alpha: float = 1.0, use_css: bool = True, use_tsg: bool = True,
+                  mean_width: int = 0) -> Dict:
     """Run the whole procedure for one unit; local indices.
 
     Q_bits [G, delta, d], K_bits/V_bits [L, d] (bf16 bits); frames local.
     use_css=False drops the Phi term (alpha = 0); use_tsg=False sets M = 1.
+    mean_width > 0 scores with the Mean-Attention prior of that pooling width
+    (returned as A_mean) in place of A_base (returned as A).
     """
     K = bf16_to_f64(K_bits)
     Q = bf16_to_f64(Q_bits)
     L = K.shape[0]
     B = budget(L, *beta)
     A = base_score(Q, K)
+    prior = mean_attention(A, mean_width) if mean_width else A
     hist, cur, text = split_tokens(L, frames)
     visual = np.zeros(L, dtype=bool)
     visual[hist] = True
@@ -354,11 +380,14 @@ def compress_unit(Q_bits: np.ndarray, K_bits: np.ndarray, V_bits: np.ndarray,
         gate, tau = tsg_gate(rho, hist, L, B)
     else:
         gate, tau = np.ones(L, dtype=np.uint8), float("nan")
-    S = integrate(A, phi, gate, visual, alpha if use_css else 0.0)
+    S = integrate(prior, phi, gate, visual, alpha if use_css else 0.0)
     kept = select_topk(S, B)
     k_out, v_out = compact(K_bits, V_bits, kept)
-    return dict(B=B, A=A, phi=phi, hist=hist, cur=cur, rho=rho, gate=gate, tau=tau,
-                S=S, kept=kept, k_out=k_out, v_out=v_out, visual=visual)
+    out = dict(B=B, A=A, phi=phi, hist=hist, cur=cur, rho=rho, gate=gate, tau=tau,
+               S=S, kept=kept, k_out=k_out, v_out=v_out, visual=visual)
+    if mean_width:
+        out["A_mean"] = prior
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -465,7 +494,7 @@ def seq_frames_local(cu_seqlens, cu_frames, frame_meta, s: int):
 
 def compress_sequence(q_bits, k_bits, v_bits, cu_seqlens, cu_frames, frame_meta, s: int,
                       layer: int, kv: int, group: int, beta, alpha=1.0,
-                      use_css=True, use_tsg=True) -> Dict:
+                      use_css=True, use_tsg=True, mean_width=0) -> Dict:
     """One unit of a packed batch.
 
     q_bits [layers, seqs, Hq, delta, d]; k_bits, v_bits [layers, Hkv, L_total, d].
@@ -475,7 +504,7 @@ def compress_sequence(q_bits, k_bits, v_bits, cu_seqlens, cu_frames, frame_meta,
     frames = seq_frames_local(cu_seqlens, cu_frames, frame_meta, s)
     Qg = q_bits[layer, s, kv * group:(kv + 1) * group]
     out = compress_unit(Qg, k_bits[layer, kv, a:b], v_bits[layer, kv, a:b], frames, beta,
-                        alpha, use_css, use_tsg)
+                        alpha, use_css, use_tsg, mean_width)
     out["kept_abs"] = out["kept"] + a
     out["offset"] = a
     return out

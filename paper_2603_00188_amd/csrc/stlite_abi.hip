@@ -535,6 +535,19 @@ stlite_status stlite_compact_kv_layer(const stlite_problem* p, const uint16_t* k
   return compact_common(p, k, v, kept_layer, 1, k_out, v_out, stream);
 }
 
+stlite_status stlite_mean_attention(const stlite_problem* p, const float* a_base, int32_t width, float* a_mean,
+                                   void* stream) {
+  stlite_status st = stlite_validate(p);
+  if (st != STLITE_OK) return st;
+  if (width < 1 || width % 2 == 0 || width > 2 * kMeanMaxRadius + 1)
+    return fail(STLITE_ERR_INVALID_ARG, "width must be odd, 1 <= width <= %d (got %d)", 2 * kMeanMaxRadius + 1,
+                width);
+  if (!a_base || !a_mean) return fail(STLITE_ERR_INVALID_ARG, "a_base and a_mean must be non-NULL");
+  if (a_base == a_mean) return fail(STLITE_ERR_INVALID_ARG, "a_mean must not alias a_base");
+  return hip_status(launch_mean_attention(a_base, a_mean, make_layout(p), width, static_cast<hipStream_t>(stream)),
+                    "mean_attention launch");
+}
+
 stlite_status stlite_layer_mean(const stlite_problem* p, const float* a_base, float* a_layer, void* stream) {
   stlite_status st = stlite_validate(p);
   if (st != STLITE_OK) return st;

@@ -184,6 +184,11 @@ hipError_t launch_css(const CssArgs& a, hipStream_t stream);
 // Phi under a k x k neighbourhood, nbhd = k in {5, 7, 9}.
 hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+// Mean-Attention prior: a_mean = a_base averaged over `width` (odd) positions
+// along each sequence, zero outside it ([units][total_tokens] each).
+constexpr int32_t kMeanMaxRadius = 127;  // width <= 255
+hipError_t launch_mean_attention(const float* a_base, float* a_mean, const Layout& lay, int32_t width,
+                                 hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------

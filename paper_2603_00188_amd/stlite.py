@@ -28,7 +28,7 @@ EXPORTS = (
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
     "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma",
     "stlite_layer_mean", "stlite_tsg_rho_concat", "stlite_css_saliency_concat", "stlite_compact_kv_layer",
-    "stlite_select_topk_noalloc",
+    "stlite_select_topk_noalloc", "stlite_mean_attention",
 )
 
 
@@ -87,6 +87,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_kept_overlap": (st, [P, vp, vp, vp, vp]),
         "stlite_probe_mfma": (st, [st, vp, vp, ctypes.c_int32, ctypes.c_int32, vp]),
         "stlite_layer_mean": (st, [P, vp, vp, vp]),
+        "stlite_mean_attention": (st, [P, vp, ctypes.c_int32, vp, vp]),
         "stlite_tsg_rho_concat": (st, [P, vp, vp, vp, sz, vp]),
         "stlite_css_saliency_concat": (st, [P, vp, vp, vp]),
         "stlite_compact_kv_layer": (st, [P, vp, vp, vp, vp, vp, vp]),
@@ -308,6 +309,11 @@ def stlite_probe_mfma(shape: int, operands, sink, n_groups: int, iters: int, str
                                     _stream(stream)), "stlite_probe_mfma")
 
 
+def stlite_mean_attention(p: Problem, a_base, width: int, a_mean, stream=None) -> None:
+    _check(load().stlite_mean_attention(p.ref, _ptr(a_base), int(width), _ptr(a_mean), _stream(stream)),
+           "stlite_mean_attention")
+
+
 def stlite_layer_mean(p: Problem, a_base, a_layer, stream=None) -> None:
     _check(load().stlite_layer_mean(p.ref, _ptr(a_base), _ptr(a_layer), _stream(stream)), "stlite_layer_mean")
 
@@ -401,8 +407,11 @@ def kept_overlap(p: Problem, kept_a, kept_b, hits=None, stream=None):
 
 
 def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: bool = True,
-             tsg: bool = True, stream=None, overlap: bool = False) -> Buffers:
+             tsg: bool = True, stream=None, overlap: bool = False, mean_width: int = 0) -> Buffers:
     """The whole pass: score, gate, saliency, select, compact (five C calls).
+
+    mean_width > 0 ranks on the Mean-Attention prior (stlite_mean_attention of
+    that width, written to out.a_mean) instead of A_base.
 
     The TSG gate runs before CSS, which skips the tokens the gate leaves out
     (their Phi is 0; Eq. modal_scoring multiplies it by M = 0 anyway).  With
@@ -433,7 +442,13 @@ def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: boo
         done = torch.cuda.Event()
         done.record(side)
         main.wait_event(done)
-    stlite_select_topk(p, out.a_base, out.phi if css else None, out.gate if tsg else None, alpha,
+    prior = out.a_base
+    if mean_width:
+        if getattr(out, "a_mean", None) is None:
+            out.a_mean = torch.empty_like(out.a_base)
+        stlite_mean_attention(p, out.a_base, mean_width, out.a_mean, main)
+        prior = out.a_mean
+    stlite_select_topk(p, prior, out.phi if css else None, out.gate if tsg else None, alpha,
                        out.kept, out.score, out.ws, main)
     stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, main)
     return out

@@ -2,7 +2,7 @@
 seeded workloads and compare it, unit by unit, with the fp64 oracle.
 
 Tolerances (bf16 inputs, fp32 accumulation in the kernels):
-  A_base            |d| <= 1e-3 |ref|
+  A_base, A_mean    |d| <= 1e-3 |ref| (A_mean sums positive A_base terms)
   Phi, rho          |d| <= 1e-3 max(|ref|, 1e-2)   (1 - cos cancels); Phi on
                     the tokens the GPU's gate admits, exactly 0 on the others
   gate              bit-exact, except historical tokens whose oracle rho lies
@@ -60,14 +60,17 @@ class Case:
         self.dk, self.dv, self.dq = as_dev(self.k), as_dev(self.v), as_dev(self.q)
         self.out = S.Buffers(self.prob, device=device)
 
-    def run(self, alpha=None, css=True, tsg=True, overlap=False):
+    def run(self, alpha=None, css=True, tsg=True, overlap=False, mean_width=0):
         import torch
         S.compress(self.prob, self.dq, self.dk, self.dv, self.out,
-                   alpha=self.w.alpha if alpha is None else alpha, css=css, tsg=tsg, overlap=overlap)
+                   alpha=self.w.alpha if alpha is None else alpha, css=css, tsg=tsg, overlap=overlap,
+                   mean_width=mean_width)
         torch.cuda.synchronize()
         o = self.out
         U = self.prob.units
         res = {n: getattr(o, n).cpu().numpy() for n in ("a_base", "phi", "rho", "tau", "gate", "score")}
+        if mean_width:
+            res["a_mean"] = o.a_mean.cpu().numpy().reshape(U, -1)
         Bt = self.prob.total_budget
         res["kept"] = o.kept[:, :Bt].cpu().numpy()
         res["k_out"] = o.k_out[:, :Bt].cpu().numpy().view(np.uint16)
@@ -76,10 +79,10 @@ class Case:
             res[n] = res[n].reshape(U, -1)
         return res
 
-    def oracle(self, layer: int, kv: int, s: int, alpha=None, css=True, tsg=True):
+    def oracle(self, layer: int, kv: int, s: int, alpha=None, css=True, tsg=True, mean_width=0):
         return O.compress_sequence(self.q, self.k, self.v, self.lay.cu_seqlens, self.lay.cu_frames,
                                    self.lay.frame_meta, s, layer, kv, self.w.group, self.w.beta,
-                                   self.w.alpha if alpha is None else alpha, css, tsg)
+                                   self.w.alpha if alpha is None else alpha, css, tsg, mean_width)
 
 
 def _rel_check(name, got, ref, floor, tol, where):
@@ -101,6 +104,8 @@ def compare_unit(case: Case, res, layer: int, kv: int, s: int, alpha=None, css=T
         ref = case.oracle(layer, kv, s, alpha, css, tsg)
     stats = {}
     stats["A"] = _rel_check("A_base", res["a_base"][u, a:b], ref["A"], 1e-30, A_RTOL, where)
+    if "A_mean" in ref:  # sums of positive terms each within A_RTOL stay within A_RTOL
+        stats["A_mean"] = _rel_check("A_mean", res["a_mean"][u, a:b], ref["A_mean"], 1e-30, A_RTOL, where)
     hist = ref["hist"]
     gate_ref = ref["gate"]
     gpu_gate = res["gate"][u, a:b]
@@ -140,7 +145,7 @@ def compare_unit(case: Case, res, layer: int, kv: int, s: int, alpha=None, css=T
     assert (np.diff(kept) > 0).all() and (kept >= a).all() and (kept < b).all(), f"{where}: kept order/range"
     S_ref = ref["S"]
     if len(diff):  # re-score with the GPU's gate so that one band flip cannot cascade
-        S_ref = O.integrate(ref["A"], ref["phi"], gpu_gate, ref["visual"],
+        S_ref = O.integrate(ref.get("A_mean", ref["A"]), ref["phi"], gpu_gate, ref["visual"],
                             (w.alpha if alpha is None else alpha) if css else 0.0)
         kept_ref = O.select_topk(S_ref, B)
     else:

@@ -219,6 +219,22 @@ def test_css_nbhd_rejections():
     assert lib.stlite_css_saliency_nbhd(ref, 9, FAKE_DEV + 8, FAKE_DEV, None) == S.ERR_INVALID_ARG
 
 
+def test_mean_attention_rejections():
+    lib = S.load()
+    p = good()
+    ref = ctypes.byref(p.c)
+    for bad in (0, 2, 8, -1, 257, 1001):
+        assert lib.stlite_mean_attention(ref, FAKE_DEV, bad, FAKE_DEV + 4096, None) == S.ERR_INVALID_ARG
+    assert b"width" in lib.stlite_last_error()
+    assert lib.stlite_mean_attention(ref, None, 7, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_mean_attention(ref, FAKE_DEV, 7, None, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_mean_attention(ref, FAKE_DEV, 7, FAKE_DEV, None) == S.ERR_INVALID_ARG
+    assert b"alias" in lib.stlite_last_error()
+    bad = good()
+    bad.c.n_layers = 0
+    assert lib.stlite_mean_attention(ctypes.byref(bad.c), FAKE_DEV, 7, FAKE_DEV + 4096, None) != S.OK
+
+
 def test_kept_overlap_rejections():
     lib = S.load()
     p = good()

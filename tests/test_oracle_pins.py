@@ -936,3 +936,78 @@ def test_recompress_steps_packed_batch_equals_single_runs():
             np.testing.assert_array_equal(got[key], ref[key], err_msg=f"step {t} {key}")
     whole = O.compress_unit(_bits(Qs[3]), _bits(K), _bits(V), frames, beta)
     np.testing.assert_array_equal(single["steps"][1]["kept"], whole["kept"])
+
+
+# ------------------------------------------------ Mean-Attention prior ----
+
+def test_mean_attention_closed_forms():
+    """Pooling of width w = 2r + 1 with zero padding and divisor w: a constant
+    c stays c wherever the whole window lies inside the sequence and is
+    c (i + r + 1) / w at distance i < r from the start (mirror at the end); a
+    single spike becomes a box of height 1/w; width 1 is the identity; mass at
+    least r from both ends is preserved; reversing the sequence reverses it."""
+    for w in (1, 3, 7, 9):
+        r = (w - 1) // 2
+        L = 25
+        c = 0.375
+        got = O.mean_attention(np.full(L, c), w)
+        for i in range(L):
+            edge = min(i, L - 1 - i)
+            want = c if edge >= r else c * (edge + r + 1) / w
+            assert got[i] == pytest.approx(want, rel=1e-15), (w, i)
+        spike = np.zeros(L)
+        spike[12] = 1.0
+        box = O.mean_attention(spike, w)
+        assert np.array_equal(box, np.where(np.abs(np.arange(L) - 12) <= r, 1.0 / w, 0.0))
+        rng = np.random.default_rng(w)
+        A = rng.uniform(size=L)
+        A[:r] = 0
+        A[L - r:] = 0
+        assert O.mean_attention(A, w).sum() == pytest.approx(A.sum(), rel=1e-13)
+        B = rng.uniform(size=L)
+        assert np.allclose(O.mean_attention(B[::-1], w), O.mean_attention(B, w)[::-1], rtol=1e-14, atol=0)
+    A = np.random.default_rng(3).uniform(size=11)
+    assert np.array_equal(O.mean_attention(A, 1), A)
+    for bad in (0, 2, -1):
+        with pytest.raises(ValueError):
+            O.mean_attention(A, bad)
+
+
+def test_mean_attention_is_library_zero_padded_box_filter():
+    """The definition equals a library routine on every length, including
+    sequences shorter than the window: scipy's 1D correlation with a box of
+    1/w taps and constant-zero boundaries; and the literal twin."""
+    import scipy.ndimage
+    rng = np.random.default_rng(17)
+    for L in (1, 2, 3, 6, 40):
+        A = rng.uniform(size=L) * 1e-3
+        for w in (1, 3, 5, 7, 11):
+            lib = scipy.ndimage.correlate1d(A, np.full(w, 1.0 / w), mode="constant", cval=0.0)
+            np.testing.assert_allclose(O.mean_attention(A, w), lib, rtol=1e-13, atol=1e-300)
+            np.testing.assert_allclose(O.mean_attention(A, w), O1.mean_pool(list(A), w), rtol=1e-14, atol=0)
+
+
+def test_mean_attention_prior_through_the_procedure():
+    """compress_unit with the Mean-Attention prior ranks on the pooled A: the
+    literal twin (pooling inside its loop version of the procedure) agrees on
+    the gate and the kept set, S uses A_mean, and width 1 reproduces the
+    window prior exactly."""
+    rng = np.random.default_rng(99)
+    d, G, delta = 128, 2, 3
+    frames = [(3, 2, 3), (12, 2, 3)]
+    L = 24
+    coarse = lambda *shape: np.round(rng.standard_normal(shape) * 8) / 64.0
+    Q, K, V = coarse(G, delta, d), coarse(L, d), coarse(L, d)
+    for w in (3, 5):
+        got = O.compress_unit(_bits(Q), _bits(K), _bits(V), frames, (1, 3), 1.0, mean_width=w)
+        np.testing.assert_allclose(got["A_mean"], O.mean_attention(got["A"], w), rtol=0, atol=0)
+        lit = O1.compress([[list(map(float, r)) for r in Q[g]] for g in range(G)],
+                          [list(map(float, r)) for r in K], frames, L // 3, 1.0, mean_width=w)
+        assert got["kept"].tolist() == lit["kept"]
+        np.testing.assert_allclose(got["A_mean"], lit["A"], rtol=1e-12, atol=0)
+        vis = got["visual"]
+        np.testing.assert_array_equal(got["S"][~vis], got["A_mean"][~vis])
+    one = O.compress_unit(_bits(Q), _bits(K), _bits(V), frames, (1, 3), 1.0, mean_width=1)
+    plain = O.compress_unit(_bits(Q), _bits(K), _bits(V), frames, (1, 3), 1.0)
+    np.testing.assert_array_equal(one["kept"], plain["kept"])
+    np.testing.assert_array_equal(one["S"], plain["S"])
