@@ -57,14 +57,33 @@ Facts derive(const stlite_problem* p) {
   f.row_blocks = nb >= 2 ? 2 : 1;
   f.waves = (nb + f.row_blocks - 1) / f.row_blocks;
   f.rows_pad = f.waves * f.row_blocks * 32;
-  // Key chunk per work-group: aim for >= 2048 work-groups so that all 256 CUs
-  // stay busy, while keeping each chunk long enough to amortise the load of
-  // the group's window queries (at least 1024 keys: on a 3,392-token step the
-  // 256-key chunks spent more on those loads than on the keys).
+  // Key chunk per work-group of the score passes.  Their window queries fill
+  // the register file (two waves per SIMD), so a CU holds 8 / waves of their
+  // work-groups and the grid drains in rounds of 256 x that many work-groups
+  // of (nearly) equal length: a last round with a few work-groups leaves the
+  // chip idle for a whole chunk.  The chunk (a multiple of 64 keys between
+  // 1024 and 16384; below 1024 keys the load of the group's window queries
+  // outweighs the keys) minimises rounds x (tiles per chunk + ~4 tiles of
+  // query load); with many sequences it is sized for >= 2048 work-groups.
   const int64_t work = f.units * p->total_tokens;
-  int64_t ch = ceil_div(work, 2048);
-  ch = ceil_div(ch, 64) * 64;
-  f.chunk = int32_t(std::min<int64_t>(4096, std::max<int64_t>(1024, ch)));
+  if (p->n_seqs <= 256 && f.units > 0) {
+    const int64_t slots = 256 * std::max(1, 8 / f.waves);
+    int64_t best = -1, best_cost = 0;
+    for (int64_t ch = 1024; ch <= 16384; ch += 64) {
+      int64_t n = 0;
+      for (int s = 0; s < p->n_seqs; ++s) n += ceil_div(p->h_cu_seqlens[s + 1] - p->h_cu_seqlens[s], ch);
+      const int64_t cost = ceil_div(n * f.units, slots) * (ch / 64 + 4);
+      if (best < 0 || cost < best_cost) {
+        best = ch;
+        best_cost = cost;
+      }
+    }
+    f.chunk = int32_t(best);
+  } else {
+    int64_t ch = ceil_div(work, 2048);
+    ch = ceil_div(ch, 64) * 64;
+    f.chunk = int32_t(std::min<int64_t>(4096, std::max<int64_t>(1024, ch)));
+  }
   for (int s = 0; s < p->n_seqs; ++s) {
     const int64_t L = p->h_cu_seqlens[s + 1] - p->h_cu_seqlens[s];
     f.max_seq = std::max(f.max_seq, L);
