@@ -422,6 +422,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pass-only", action="store_true",
+                    help="time the pass only: no measured peaks, decode, variants, cache hit rate or "
+                         "multi-step timings (for counter runs)")
     ap.add_argument("--overlap", action="store_true",
                     help="run score, TSG and CSS on three concurrent streams")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -556,6 +559,11 @@ def main():
         "roofline": roof,
         "stages": stages,
     }
+    if args.pass_only:
+        if not args.no_cpu_baseline:
+            result["cpu_baseline"] = cpu_baseline(w, inputs)
+        print(json.dumps(result), flush=True)
+        return
     peaks = measured_peaks(stream)
     result["measured_peaks"] = peaks
     mp = peaks["mfma_16x16x32_bf16_tflops"] if roof["bound"] == "mfma" else peaks["device_copy_2gib_gbs"]

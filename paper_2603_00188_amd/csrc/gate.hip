@@ -4,6 +4,7 @@
 // the rho of the last one admitted.  The selection is the exact k-selection of
 // segsel.h over the keys order_key(rho).
 #include "segsel.h"
+#include "segsel_resident.h"
 #include "stlite_internal.h"
 
 namespace stlite {
@@ -54,7 +55,7 @@ struct GateProd {
 #pragma unroll
     for (int j = 0; j < kSelJ; ++j) {
       const bool h = ((w.hist >> j) & 1u) && base + 64 * j + lane < hi;
-      key[j] = h ? min(order_key(w.r[j]), kSelNever - 1u) : kSelNever;
+      key[j] = h ? min(order_key(w.r[j]), kSelKeyMax) : kSelNever;
     }
   }
 
@@ -104,9 +105,81 @@ __global__ __launch_bounds__(kSelThreads) void gate_emit_kernel(GateArgs a) {
     a.tau[size_t(blockIdx.z) * lay.n_seqs + c.seq] = c.k > 0 ? order_key_value(T) : __builtin_nanf("");
 }
 
+// The rank gate of one segment held by one work-group (segsel_resident.h).
+struct GateRes {
+  __amdgpu_buffer_rsrc_t rho;
+  __amdgpu_buffer_rsrc_t gate;
+  bool needs_class;
+
+  struct Raw {
+    float r[4];
+  };
+
+  __device__ void load(int32_t base, Raw& w) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w.r[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, (base + 64 * e + lane) * 4, 0, 0));
+  }
+
+  __device__ void keys(int32_t base, const int (&cls)[4], int32_t hi, const Raw& w, uint32_t (&key)[4]) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      key[e] = (cls[e] == kHist && base + 64 * e + lane < hi) ? min(order_key(w.r[e]), kSelKeyMax) : kSelNever;
+  }
+
+  __device__ void emit(int32_t i, int cls, bool take, int32_t) const {
+    __builtin_amdgcn_raw_buffer_store_b8(uint8_t((cls != kHist || take) ? 1 : 0), gate, i, 0, 0);
+  }
+};
+
+// Work-group (sequence, unit): the whole segment's gate bytes and tau.
+__global__ __launch_bounds__(kResThreads) void gate_resident_kernel(GateArgs a) {
+  __shared__ ResShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c;
+  c.seq = blockIdx.x;
+  c.s0 = lay.cu_seqlens[c.seq];
+  c.n = lay.cu_seqlens[c.seq + 1] - c.s0;
+  c.part = 0;
+  c.ubase = size_t(blockIdx.y) * lay.total_tokens;
+  SeqFrames<true> fr;
+  fr.meta = lay.frame_meta;
+  fr.fs = sh.fstart;
+  fr.fe = sh.fend;
+  fr.f0 = lay.cu_frames[c.seq];
+  fr.nf = lay.cu_frames[c.seq + 1] - fr.f0;
+  int32_t nh = 0;  // N_hist: every frame of the sequence but the last
+  for (int32_t f = threadIdx.x; f < fr.nf; f += kResThreads) {
+    const int32_t* m = lay.frame_meta + 3 * (fr.f0 + f);
+    sh.fstart[f] = m[0];
+    sh.fend[f] = m[0] + m[1] * m[2];
+    if (f + 1 < fr.nf) nh += m[1] * m[2];
+  }
+  nh = wave_sum(nh);
+  if ((threadIdx.x & 63) == 0) sh.wlt[threadIdx.x >> 6] = nh;
+  __syncthreads();
+  int32_t n_hist = 0;
+  for (int w = 0; w < kResWaves; ++w) n_hist += sh.wlt[w];
+  c.k = min(lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq], n_hist);
+  __syncthreads();  // every thread has read the partial sums before the selection reuses them
+  GateRes p;
+  gate_buffers(a, c, p.rho, p.gate);
+  p.needs_class = true;
+  const uint32_t T = res_select(p, sh, fr, c);
+  if (a.tau && threadIdx.x == 0)
+    a.tau[size_t(blockIdx.y) * lay.n_seqs + c.seq] = c.k > 0 ? order_key_value(T) : __builtin_nanf("");
+}
+
 }  // namespace
 
 hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
+  if (g.sel.resident) {
+    if (g.lay.n_units == 0 || g.lay.n_seqs == 0) return hipSuccess;
+    hipLaunchKernelGGL(gate_resident_kernel, dim3(g.lay.n_seqs, g.lay.n_units), dim3(kResThreads), 0, stream, g);
+    return hipGetLastError();
+  }
   return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
                            gate_emit_kernel, g, g.sel, g.lay, stream);
 }

@@ -40,6 +40,10 @@ constexpr int kSelJ = 8;              // tokens per lane per produce step (one 4
 constexpr int kSelQ = 8;              // 16-byte key loads per lane per step of the key passes
 
 constexpr uint32_t kSelNever = 0xffffffffu;  // key of a token that is never selected
+// Largest key of a token that can be selected: below every key whose top 16
+// bits are all ones, so that a 16-bit key prefix of 0xffff means "never"
+// (only NaN scores map above it; they rank after every number, as one class).
+constexpr uint32_t kSelKeyMax = 0xfffeffffu;
 
 // Workspace words of one part histogram (fine bins, then the sums of 32-bin groups).
 constexpr int kSelH0 = 2048 + 64;     // levels 0 and 1
@@ -89,15 +93,16 @@ struct SelShared {
 template <bool LDS>
 struct SeqFrames {
   const int32_t* meta;
-  const SelShared* sh;
+  const int32_t* fs;  // LDS: first token of each frame
+  const int32_t* fe;  // LDS: one past its last token
   int32_t f0, nf;
 
   __device__ int32_t start(int32_t f) const {
-    if constexpr (LDS) return sh->fstart[f];
+    if constexpr (LDS) return fs[f];
     else return meta[3 * (f0 + f)];
   }
   __device__ int32_t end(int32_t f) const {
-    if constexpr (LDS) return sh->fend[f];
+    if constexpr (LDS) return fe[f];
     else return meta[3 * (f0 + f)] + meta[3 * (f0 + f) + 1] * meta[3 * (f0 + f) + 2];
   }
   // Last frame whose first token is <= tok, or -1.
@@ -187,7 +192,8 @@ template <bool LDS>
 __device__ inline SeqFrames<LDS> load_frames(SelShared& sh, const Layout& lay, int32_t seq) {
   SeqFrames<LDS> fr;
   fr.meta = lay.frame_meta;
-  fr.sh = &sh;
+  fr.fs = sh.fstart;
+  fr.fe = sh.fend;
   fr.f0 = lay.cu_frames[seq];
   fr.nf = lay.cu_frames[seq + 1] - fr.f0;
   if constexpr (LDS) {

@@ -6,6 +6,7 @@
 // The selection is the per-segment radix select of segsel.h on the keys
 // ~order_key(S) (ascending key = descending S).
 #include "segsel.h"
+#include "segsel_resident.h"
 #include "stlite_internal.h"
 
 namespace stlite {
@@ -68,7 +69,7 @@ struct SelectProd {
         S = r.g[j] == 0 ? 0.0f : x;
       }
       if (score && i < hi) score[i] = S;
-      key[j] = i < hi ? min(~order_key(S), kSelNever - 1u) : kSelNever;
+      key[j] = i < hi ? min(~order_key(S), kSelKeyMax) : kSelNever;
     }
   }
 
@@ -116,9 +117,106 @@ __global__ __launch_bounds__(kSelThreads) void select_emit_kernel(SelectArgs a) 
   sel_emit(p, sh, a.sel, a.lay, c);
 }
 
+// The top-B of one segment held by one work-group (segsel_resident.h).
+struct SelectRes {
+  __amdgpu_buffer_rsrc_t a_base;  // the segment's A, Phi and gate (out-of-range lanes read 0)
+  __amdgpu_buffer_rsrc_t phi;
+  __amdgpu_buffer_rsrc_t gate;
+  bool has_phi, has_gate;
+  bool needs_class;  // Phi or the gate is given: visual tokens must be told from text
+  float alpha;
+  float* score;      // nullable: the segment's S
+  int32_t* kept;     // the segment's kept list
+  int32_t k, s0;
+
+  struct Raw {
+    float A[4], ph[4];
+    uint32_t g[4];
+  };
+
+  __device__ void load(int32_t base, Raw& r) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int32_t i = base + 64 * e + lane;
+      r.A[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
+      r.ph[e] = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
+      r.g[e] = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+    }
+  }
+
+  // S of Eq. modal_scoring, as the four-pass producer computes it.
+  __device__ float score_of(float A, float ph, uint32_t g, bool visual) const {
+    if (!visual) return A;
+    const float x = has_phi ? fmaf(alpha, ph, A) : A;
+    return g == 0 ? 0.0f : x;
+  }
+
+  __device__ void keys(int32_t base, const int (&cls)[4], int32_t hi, const Raw& r, uint32_t (&key)[4]) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int32_t i = base + 64 * e + lane;
+      const float S = score_of(r.A[e], r.ph[e], r.g[e], cls[e] != kText);
+      if (score && i < hi) score[i] = S;
+      key[e] = i < hi ? min(~order_key(S), kSelKeyMax) : kSelNever;
+    }
+  }
+
+  __device__ void emit(int32_t i, int, bool take, int32_t pos) const {
+    if (take && pos < k) kept[pos] = s0 + i;
+  }
+};
+
+// Work-group (sequence, unit): the whole segment's kept list (and S).
+__global__ __launch_bounds__(kResThreads) void select_resident_kernel(SelectArgs a) {
+  __shared__ ResShared sh;
+  const Layout& lay = a.lay;
+  SelCtx c;
+  c.seq = blockIdx.x;
+  c.s0 = lay.cu_seqlens[c.seq];
+  c.n = lay.cu_seqlens[c.seq + 1] - c.s0;
+  c.part = 0;
+  c.ubase = size_t(blockIdx.y) * lay.total_tokens;
+  c.k = lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq];
+  SelectRes p;
+  const size_t seg0 = c.ubase + size_t(c.s0);
+  p.a_base = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.a_base) + seg0, 0, c.n * 4, kBufferFlags);
+  p.has_phi = a.phi != nullptr;
+  p.has_gate = a.gate != nullptr;
+  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0, c.n * 4,
+                                            kBufferFlags);
+  p.gate = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.has_gate ? a.gate + seg0 : nullptr), 0,
+                                             p.has_gate ? c.n : 0, kBufferFlags);
+  p.needs_class = p.has_phi || p.has_gate;
+  p.alpha = a.alpha;
+  p.score = a.score ? a.score + seg0 : nullptr;
+  p.kept = a.kept + size_t(blockIdx.y) * lay.total_budget + lay.cu_budget[c.seq];
+  p.k = c.k;
+  p.s0 = c.s0;
+  SeqFrames<true> fr;
+  fr.meta = lay.frame_meta;
+  fr.fs = sh.fstart;
+  fr.fe = sh.fend;
+  fr.f0 = lay.cu_frames[c.seq];
+  fr.nf = lay.cu_frames[c.seq + 1] - fr.f0;
+  for (int32_t f = threadIdx.x; f < fr.nf; f += kResThreads) {
+    const int32_t* m = lay.frame_meta + 3 * (fr.f0 + f);
+    sh.fstart[f] = m[0];
+    sh.fend[f] = m[0] + m[1] * m[2];
+  }
+  __syncthreads();
+  res_select(p, sh, fr, c);
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
+  if (a.sel.resident) {
+    if (a.lay.n_units == 0 || a.lay.n_seqs == 0) return hipSuccess;
+    hipLaunchKernelGGL(select_resident_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(kResThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   return launch_sel_passes(a.sel.lds_frames ? select_produce_kernel<true> : select_produce_kernel<false>,
                            select_emit_kernel, a, a.sel, a.lay, stream);
 }

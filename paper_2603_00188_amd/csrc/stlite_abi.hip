@@ -126,6 +126,7 @@ SelPlan sel_carve(const stlite_problem* p, const Facts& f, char* w) {
   SelPlan s;
   s.parts = f.sel_parts;
   s.lds_frames = f.max_seq_frames <= kSelFrames ? 1 : 0;
+  s.resident = (s.lds_frames && f.max_seq <= kSelResidentCapacity) ? 1 : 0;
   s.keys = reinterpret_cast<uint32_t*>(w);
   w += align_up(size_t(f.units) * size_t(sel_key_stride(p->total_tokens, p->n_seqs)) * sizeof(uint32_t));
   s.hist0 = reinterpret_cast<uint32_t*>(w);

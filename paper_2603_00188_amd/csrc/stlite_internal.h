@@ -86,7 +86,12 @@ struct SelPlan {
   int32_t* state;        // [units][seqs][8]: k, then prefix and rank after levels 0 and 1
   int32_t parts;         // 1 .. 16
   int32_t lds_frames;    // 1: no sequence has more than kSelFrames frames
+  int32_t resident;      // 1: every segment fits one work-group (segsel_resident.h), which uses no workspace
 };
+
+// Longest sequence whose selections run segment-resident (one work-group per
+// segment, keys kept in registers).
+constexpr int32_t kSelResidentCapacity = 32768;
 
 // Key rows of a selection: a row of sel_key_stride keys per unit; the keys of
 // sequence seq (first token s0) start at sel_key_base, a multiple of 4, and the

@@ -173,17 +173,29 @@ def test_stage_threshold_and_select_exact(torch_cuda):
         assert (kept[u, cb[s]:cb[s + 1]] == want).all(), (u, s)
 
 
-def test_stage_exact_many_parts_and_ties(torch_cuda):
-    """Stage-isolated on sequences long enough that the gate's and the top-B's
-    selections are cut into several parts per segment, with inputs drawn from
-    a few values so that long runs of equal keys straddle part and wave
-    boundaries: gate, tau and kept lists must equal the oracle's exactly."""
+# Layouts of the stage-exact selection tests: (frames, (rows, cols), text) per sequence.
+STAGE_LAYOUTS = {
+    # segments of 27,300 and 5,935 tokens: one work-group per segment keeps them on chip
+    "resident": ((13, (40, 50), 100), (5, (30, 37), 77)),
+    # a 168,000-token segment, longer than the on-chip selection holds: every
+    # segment of the call takes the four-pass selection, cut into parts
+    "four_pass": ((80, (40, 50), 100), (5, (30, 37), 77)),
+}
+
+
+@pytest.mark.parametrize("layout", list(STAGE_LAYOUTS))
+@pytest.mark.parametrize("values", ["few", "many"])
+def test_stage_exact_many_parts_and_ties(torch_cuda, layout, values):
+    """Stage-isolated on long sequences, with inputs drawn from a few values
+    (long runs of equal keys straddling wave and part boundaries; far more
+    tokens share the pivot's top 16 key bits than the on-chip candidate list
+    holds) or from a few hundred (ties that fit the list): gate, tau, S and
+    kept lists must equal the oracle's exactly."""
     import torch
     from oracle import stlite_oracle as O
     from paper_2603_00188_amd import stlite as S
-    # two sequences: 13 frames of 40 x 50 patches + 100 text, and 5 frames of 30 x 37 + 77 text
     seqs, metas, cu = [], [], [0]
-    for nf, (r, c), nt in ((13, (40, 50), 100), (5, (30, 37), 77)):
+    for nf, (r, c), nt in STAGE_LAYOUTS[layout]:
         off = cu[-1]
         fm = []
         for _ in range(nf):
@@ -200,15 +212,21 @@ def test_stage_exact_many_parts_and_ties(torch_cuda):
         prob = S.Problem(n_layers, hkv, hkv, 8, cu_seqlens, cu_frames, frame_meta, cu_budget)
         U, L = prob.units, prob.total_tokens
         rng = np.random.default_rng(5)
-        rho = rng.choice(np.float32([0.1, 0.25, 0.5, 0.75, 1.0]), size=(U, L)).astype(np.float32)
-        A = rng.choice(np.float32([1e-4, 2e-4, 5e-4]), size=(U, L)).astype(np.float32)
-        phi = rng.choice(np.float32([0.9, 1.0, 1.1]), size=(U, L)).astype(np.float32)
+        if values == "few":
+            rho = rng.choice(np.float32([0.1, 0.25, 0.5, 0.75, 1.0]), size=(U, L)).astype(np.float32)
+            A = rng.choice(np.float32([1e-4, 2e-4, 5e-4]), size=(U, L)).astype(np.float32)
+            phi = rng.choice(np.float32([0.9, 1.0, 1.1]), size=(U, L)).astype(np.float32)
+        else:
+            rho = rng.choice(np.linspace(0.2, 0.4, 300, dtype=np.float32), size=(U, L)).astype(np.float32)
+            A = rng.choice(np.linspace(1e-4, 5e-4, 200, dtype=np.float32), size=(U, L)).astype(np.float32)
+            phi = rng.choice(np.linspace(0.9, 1.1, 250, dtype=np.float32), size=(U, L)).astype(np.float32)
         out = S.Buffers(prob)
         dev = lambda x: torch.from_numpy(x).cuda()
         S.stlite_tsg_threshold(prob, dev(rho), out.tau, out.gate, out.ws_tsg)
         S.stlite_select_topk(prob, dev(A), dev(phi), out.gate, 1.0, out.kept, out.score, out.ws)
         torch.cuda.synchronize()
         gate, tau, kept = out.gate.cpu().numpy(), out.tau.cpu().numpy(), out.kept.cpu().numpy()
+        score = out.score.cpu().numpy()
         for u in range(U):
             for s in range(2):
                 a, b = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
@@ -222,6 +240,7 @@ def test_stage_exact_many_parts_and_ties(torch_cuda):
                 assert (gate[u, a:b] == g_ref).all(), (beta, u, s)
                 assert np.float32(tau[u, s]) == np.float32(tau_ref), (beta, u, s)
                 s32 = np.where(vis, np.where(g_ref > 0, A[u, a:b] + phi[u, a:b], np.float32(0)), A[u, a:b])
+                assert np.array_equal(score[u, a:b], s32), (beta, u, s)
                 want = O.select_topk(s32.astype(np.float64), B) + a
                 assert (kept[u, cu_budget[s]:cu_budget[s + 1]] == want).all(), (beta, u, s)
 
