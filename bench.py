@@ -138,8 +138,11 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), flush=True)
 
 
-def cpu_baseline(w, case_inputs, budget_s=12.0, max_units=8):
-    """Time the fp64 oracle on whole (layer, kv head) units until ~budget_s."""
+def cpu_baseline(w, case_inputs, budget_s=6.0, runs=3):
+    """The fp64 oracle on the host, timed the way the baseline plan asks: one
+    untimed unit, then the median of `runs` timed passes over a sample of whole
+    (layer, kv head) units (every sequence) sized to ~budget_s per pass from
+    the untimed unit's time, scaled to all units."""
     from oracle import stlite_oracle as O
     scene, k, v, q = case_inputs
     lay = scene.layout
@@ -150,26 +153,32 @@ def cpu_baseline(w, case_inputs, budget_s=12.0, max_units=8):
     except Exception:  # pragma: no cover
         cores = os.cpu_count()
     units_all = [(l, h) for l in range(w.n_layers) for h in range(w.n_kv_heads)]
-    rng = np.random.default_rng(0)
-    order = rng.permutation(len(units_all))
-    done, t_total = 0, 0.0
-    for i in order[:max_units]:
-        l, h = units_all[i]
-        t0 = time.perf_counter()
+    order = [units_all[i] for i in np.random.default_rng(0).permutation(len(units_all))]
+
+    def one(unit):
+        l, h = unit
         for s in range(lay.n_seqs):
             O.compress_sequence(q, k, v, lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s, l, h, w.group,
                                 w.beta, w.alpha)
-        t_total += time.perf_counter() - t0
-        done += 1
-        log(f"cpu baseline: unit ({l},{h}) done, {t_total:.1f} s so far")
-        if t_total >= budget_s:
-            break
-    per_unit = t_total / done
-    rate = lay.total_tokens / (per_unit * len(units_all))
+
+    t0 = time.perf_counter()
+    one(order[0])  # untimed
+    t_unit = time.perf_counter() - t0
+    n = int(min(len(units_all), max(1, round(budget_s / max(t_unit, 1e-9)))))
+    sample = order[:n]
+    times = []
+    for r in range(runs):
+        t0 = time.perf_counter()
+        for unit in sample:
+            one(unit)
+        times.append(time.perf_counter() - t0)
+        log(f"cpu baseline: timed run {r + 1} of {runs}: {n} units in {times[-1]:.3g} s")
+    med = float(np.median(times))
+    rate = lay.total_tokens / (med / n * len(units_all))
     return {"value": round(rate, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{done} of {len(units_all)} (layer, kv head) units of the full workload, "
-                      f"every sequence, fp64 NumPy oracle; rate scaled to all {len(units_all)} units "
-                      f"({t_total:.1f} s measured)"}
+            "sample": f"{n} of {len(units_all)} (layer, kv head) units of the full workload, every sequence, "
+                      f"fp64 NumPy oracle; one untimed unit, then the median of {runs} timed passes "
+                      f"({', '.join(f'{t:.3g}' for t in times)} s), rate scaled to all {len(units_all)} units"}
 
 
 def decode_timing(prob, w, q, dk, dv, out, stream, reps=20):
@@ -421,7 +430,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--beta", default=None, metavar="NUM/DEN",
+                    help="budget ratio as a fraction (default: the workload's own)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline-only", action="store_true",
+                    help="only time the fp64 oracle on the host for --config (no GPU work) and print it")
     ap.add_argument("--pass-only", action="store_true",
                     help="time the pass only: no measured peaks, decode, variants, cache hit rate or "
                          "multi-step timings (for counter runs)")
@@ -435,16 +448,24 @@ def main():
                          "this build runs it on a single MI355X; --gpus must be 1\n")
         sys.exit(2)
 
+    from paper_2603_00188_amd import workload as W
+    beta = tuple(int(x) for x in args.beta.split("/")) if args.beta else None
+    if args.cpu_baseline_only:
+        w = W.config(args.config, beta)
+        log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
+        base = cpu_baseline(w, W.make_inputs(w, workers=16))
+        print(json.dumps({"config": w.name, "tokens": w.total_tokens, "cpu_baseline": base}), flush=True)
+        return
+
     import torch
     from paper_2603_00188_amd import stlite as S
-    from paper_2603_00188_amd import workload as W
 
     S.load()  # fails loudly without the HIP library
     torch.cuda.set_device(0)
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
-    w = W.config(args.config)
+    w = W.config(args.config, beta)
     log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
     inputs = W.make_inputs(w, workers=16)
     scene, k, v, q = inputs
@@ -533,6 +554,7 @@ def main():
     roof["call"] = "stlite_" + dom
     roof["ms_per_launch"] = round(per_call[dom], 4)
 
+    grid = (f"{int(lay.frame_meta[0][1])}x{int(lay.frame_meta[0][2])}" if len(lay.frame_meta) else "no")
     result = {
         "metric": METRIC,
         "value": round(lay.total_tokens / (ms_step * 1e-3), 1),
@@ -548,7 +570,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}: {lay.n_seqs} sequence(s), {len(lay.frame_meta)} frames of "
-                        f"36x80 patches + text, {lay.total_tokens} tokens, {w.n_layers} layers, "
+                        f"{grid} patches + text, {lay.total_tokens} tokens, {w.n_layers} layers, "
                         f"{w.n_q_heads}/{w.n_kv_heads} heads, head_dim {w.head_dim}, window {w.window}, "
                         f"beta {w.beta[0]}/{w.beta[1]}, alpha {w.alpha}",
             "tokens": lay.total_tokens, "layers": w.n_layers, "kv_heads": w.n_kv_heads,
