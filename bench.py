@@ -550,6 +550,9 @@ def main():
     roof = dict(stages[dom])
     roof.pop("ms")
     roof["traffic"] = measured_traffic(kernel_of[dom], w.name)
+    roof["traffic_source"] = (f"profiles/{kernel_of[dom]}_{w.name}_traffic.md: rocprofv3 FETCH_SIZE + WRITE_SIZE "
+                              "per launch, each scaled by a 1 GiB copy; taken in a separate counter run of the "
+                              "same sources (null when the kernel's sources have changed since)")
     roof["kernel"] = kernel_of[dom]
     roof["call"] = "stlite_" + dom
     roof["ms_per_launch"] = round(per_call[dom], 4)

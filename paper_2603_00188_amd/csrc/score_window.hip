@@ -29,6 +29,13 @@ namespace {
 constexpr float kNegBig = -1.0e30f;
 constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
+// Minimum work-groups per CU in the launch bound (what the register allocator
+// budgets for): ceil(8 / NW), about two waves per SIMD, for groups of three or
+// more waves; one for the one- and two-wave groups of the smallest windows,
+// whose resident queries need more registers than a higher target leaves.
+template <int NW>
+constexpr int kScoreMinGroups = NW <= 2 ? 1 : (8 + NW - 1) / NW;
+
 struct ChunkPos {
   int32_t seq, seq_start, seq_len, c0, c1, gchunk;
 };
@@ -137,7 +144,7 @@ __device__ inline int scatter_reg(int lane) {
 // chunk (and flags the chunk if a sum overflowed); PASS 2 writes A for the
 // chunk's keys.
 template <int PASS, int RB, int NW>
-__global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_pass_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
   __shared__ int32_t lim_s[NW * RB * 32];
   __shared__ float red_s[2][NW][kTileKeys];
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_pass_kernel(
 // a chunk's logits rise far enough above the first tile's to overflow the lean
 // pass's sums).
 template <int RB, int NW>
-__global__ __launch_bounds__(NW * 64, (8 + NW - 1) / NW) void score_rowstats_exact_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_rowstats_exact_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems];
   __shared__ int32_t lim_s[NW * RB * 32];
   const int unit = blockIdx.y;
