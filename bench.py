@@ -357,6 +357,41 @@ def chr_harness(prob, q, dk, a_base, out, stream):
     return entry
 
 
+def graph_timing(prob, w, dq, dk, dv, out, reps):
+    """The whole pass (compress(), five C calls on one stream) eagerly and as a
+    HIP graph captured once and replayed, `reps` times each after one warm-up;
+    the replay's kept sets must equal the eager ones bit for bit."""
+    import torch
+    from paper_2603_00188_amd import stlite as S
+    st = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    S.compress(prob, dq, dk, dv, out, alpha=w.alpha, stream=st)
+    e0, e1 = ev(), ev()
+    e0.record(st)
+    for _ in range(reps):
+        S.compress(prob, dq, dk, dv, out, alpha=w.alpha, stream=st)
+    e1.record(st)
+    torch.cuda.synchronize()
+    kept_eager = out.kept.clone()
+    graph = S.capture_compress(prob, dq, dk, dv, out, alpha=w.alpha)
+    graph.replay()
+    g0, g1 = ev(), ev()
+    g0.record(st)
+    for _ in range(reps):
+        graph.replay()
+    g1.record(st)
+    torch.cuda.synchronize()
+    if not torch.equal(out.kept, kept_eager):
+        raise RuntimeError("graph replay kept a different set than the eager pass")
+    eager_ms, graph_ms = e0.elapsed_time(e1) / reps, g0.elapsed_time(g1) / reps
+    del graph
+    log(f"compress(): eager {eager_ms:.3f} ms, graph replay {graph_ms:.3f} ms")
+    return {"eager_ms": round(eager_ms, 4), "replay_ms": round(graph_ms, 4),
+            "replay_tokens_per_s": round(int(prob.total_tokens) / (graph_ms * 1e-3), 1),
+            "note": "compress() with stlite_tsg_gate (rho, threshold and gate in one call); kept sets of the "
+                    "replays equal to the eager pass's"}
+
+
 def multistep_timing(w, inputs, dk, dv, stream, reps=2):
     """Recompression at every step of the trajectory (problem setup, Eq.
     history_context): step t compresses its own context, frames 0..t with the
@@ -373,7 +408,7 @@ def multistep_timing(w, inputs, dk, dv, stream, reps=2):
     from paper_2603_00188_amd import stlite as S
     from paper_2603_00188_amd import workload as W
     si = W.make_step_inputs(w, base=inputs, pack=False)
-    toks, ms, chr_st, chr_sn = [], [], [], []
+    toks, ms, ms_graph, chr_st, chr_sn = [], [], [], [], []
     for i, t in enumerate(si.steps):
         wt = dataclasses.replace(w, seqs=(W.step_prefix_segments(w, t),))
         lay = W.make_layout(wt)
@@ -393,6 +428,22 @@ def multistep_timing(w, inputs, dk, dv, stream, reps=2):
         for _ in range(reps):
             S.compress(p, qt, kt, vt, o, alpha=w.alpha, stream=stream)
         e1.record(stream)
+        # the same pass captured once into a HIP graph and replayed: one launch
+        # per pass instead of its kernels one by one (what a serving loop that
+        # recompresses a fixed-shape cache would do); its kept sets must be the
+        # eager ones, bit for bit
+        kept_eager = o.kept.clone()
+        graph = S.capture_compress(p, qt, kt, vt, o, alpha=w.alpha)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gs = torch.cuda.current_stream()
+        graph.replay()
+        g0.record(gs)
+        for _ in range(reps):
+            graph.replay()
+        g1.record(gs)
+        torch.cuda.synchronize()
+        if not torch.equal(o.kept, kept_eager):
+            raise RuntimeError(f"step {t}: graph replay kept a different set than the eager pass")
         snap = torch.empty_like(o.kept)
         S.stlite_select_topk(p, o.a_base, None, None, 0.0, snap, None, o.ws, stream)
         star, _ = S.oracle_set(S.decode_problem(p), qd, kt, stream=stream)
@@ -402,15 +453,21 @@ def multistep_timing(w, inputs, dk, dv, stream, reps=2):
         B = int(cu_b[-1])
         toks.append(n)
         ms.append(e0.elapsed_time(e1) / reps)
+        ms_graph.append(g0.elapsed_time(g1) / reps)
         chr_st.append(float(h_st.cpu().numpy().mean()) / B if B else float("nan"))
         chr_sn.append(float(h_sn.cpu().numpy().mean()) / B if B else float("nan"))
-        del kt, vt, o, snap, star
+        del kt, vt, o, snap, star, graph
     mean = lambda r: float(np.mean([x for x in r if x == x]))
     entry = {
         "workload": f"{w.name} recompressed at each of its {len(si.steps)} steps; step t: frames 0..t "
                     f"and their text, one problem per step, beta {w.beta[0]}/{w.beta[1]}",
         "steps": len(si.steps), "tokens_total": int(sum(toks)), "ms_total": round(float(sum(ms)), 3),
         "tokens_per_s": round(sum(toks) / (sum(ms) * 1e-3), 1),
+        "graph": {"ms_total": round(float(sum(ms_graph)), 3),
+                  "tokens_per_s": round(sum(toks) / (sum(ms_graph) * 1e-3), 1),
+                  "ms_per_step": [round(x, 4) for x in ms_graph],
+                  "note": "each step's pass captured into one HIP graph and replayed; kept sets equal "
+                          "to the eager pass's"},
         "per_step": {"tokens": toks, "ms": [round(x, 4) for x in ms],
                      "tokens_per_s": [round(n / (m * 1e-3), 1) for n, m in zip(toks, ms)]},
         "chr_st_lite": round(mean(chr_st), 4), "chr_snapkv": round(mean(chr_sn), 4),
@@ -419,7 +476,7 @@ def multistep_timing(w, inputs, dk, dv, stream, reps=2):
         "decode_query": "sum of the step's element keys and of an earlier frame's changed region, plus noise",
     }
     log(f"multi-step: {entry['steps']} steps, {entry['tokens_total']} tokens in {entry['ms_total']:.2f} ms "
-        f"({entry['tokens_per_s'] / 1e6:.2f} M tokens/s); CHR ST-Lite {entry['chr_st_lite']:.4f}, "
+        f"({entry['tokens_per_s'] / 1e6:.2f} M tokens/s; graph replay {entry['graph']['ms_total']:.2f} ms); CHR ST-Lite {entry['chr_st_lite']:.4f}, "
         f"SnapKV mode {entry['chr_snapkv']:.4f}")
     return entry
 
@@ -600,6 +657,7 @@ def main():
     sw["executed_tflops"] = round(2.0 * sw["achieved"], 2)
     sw["measured_peak"] = peaks["mfma_32x32x16_bf16_exp2_mix_tflops"]
     sw["executed_frac_of_measured_peak"] = round(2.0 * sw["achieved"] / sw["measured_peak"], 4)
+    result["graph"] = graph_timing(prob, w, dq, dk, dv, out, args.steps)
     result["decode"] = decode_timing(prob, w, q, dk, dv, out, stream)
     result["variants"] = variants_timing(prob, w, lay, cu_budget, dk, rho, out, stream)
     step()  # the pass's kept sets again (the variants overwrote phi and gate)

@@ -452,3 +452,27 @@ def compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: boo
                        out.kept, out.score, out.ws, main)
     stlite_compact_kv(p, k, v, out.kept, out.k_out, out.v_out, main)
     return out
+
+
+def capture_compress(p: Problem, q_win, k, v, out: Buffers, alpha: float = 1.0, css: bool = True,
+                     tsg: bool = True, mean_width: int = 0):
+    """The whole pass (compress() on one stream) captured once into a HIP graph
+    (torch.cuda.CUDAGraph); ``graph.replay()`` then runs every kernel of the pass
+    with one launch.  Every call of the pass only enqueues kernels on its stream
+    (no allocation, copy, memset or synchronisation), and ``out`` holds every
+    buffer, so the graph stays valid while p, the inputs and ``out`` live; a
+    replay recomputes from whatever the input tensors hold."""
+    import torch
+    if mean_width and getattr(out, "a_mean", None) is None:
+        out.a_mean = torch.empty_like(out.a_base)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # one eager pass first, as torch asks before a capture
+        compress(p, q_win, k, v, out, alpha, css, tsg, stream=side, mean_width=mean_width)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        compress(p, q_win, k, v, out, alpha, css, tsg, stream=torch.cuda.current_stream(), mean_width=mean_width)
+    return graph
+
