@@ -5,6 +5,7 @@
 // segsel.h over the keys order_key(rho).
 #include "segsel.h"
 #include "segsel_resident.h"
+#include "segsel_split.h"
 #include "stlite_internal.h"
 
 namespace stlite {
@@ -107,9 +108,12 @@ __global__ __launch_bounds__(kSelThreads) void gate_emit_kernel(GateArgs a) {
 
 // The rank gate of one segment held by one work-group (segsel_resident.h).
 struct GateRes {
+  static constexpr int kGroup = 4;      // tiles a classifying wave loads at once (segsel_split.h)
+  static constexpr bool kDirect = true;  // the splitter path writes the gate bytes directly
   __amdgpu_buffer_rsrc_t rho;
   __amdgpu_buffer_rsrc_t gate;
   bool needs_class;
+  bool aligned;  // the segment's gate bytes start 4-byte aligned
 
   struct Raw {
     float r[4];
@@ -132,7 +136,46 @@ struct GateRes {
   __device__ void emit(int32_t i, int cls, bool take, int32_t) const {
     __builtin_amdgcn_raw_buffer_store_b8(uint8_t((cls != kHist || take) ? 1 : 0), gate, i, 0, 0);
   }
+
+  // Whether a token of class cls can be selected (segsel_split.h).
+  __device__ bool selectable(int cls) const { return cls == kHist; }
+
+  // keys() for a whole tile of one class (cls, wave-uniform) inside the segment.
+  __device__ void keys_uniform(int32_t, int cls, const Raw& w, uint32_t (&key)[4]) const {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) key[e] = cls == kHist ? min(order_key(w.r[e]), kSelKeyMax) : kSelNever;
+  }
+
+  // The splitter path (segsel_split.h): one token's input and key, and the
+  // gate byte from its code (never selected = not historical).
+  struct Raw1 {
+    float r;
+  };
+
+  __device__ void load1(int32_t i, Raw1& w) const {
+    w.r = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, i * 4, 0, 0));
+  }
+
+  __device__ uint32_t key1(const Raw1& w, int cls) const {
+    return cls == kHist ? min(order_key(w.r), kSelKeyMax) : kSelNever;
+  }
+
+  __device__ void emit_code(int32_t i, bool never, bool take, int32_t) const {
+    __builtin_amdgcn_raw_buffer_store_b8(uint8_t((never || take) ? 1 : 0), gate, i, 0, 0);
+  }
+
+  __device__ void put_byte(int32_t i, uint8_t b) const { __builtin_amdgcn_raw_buffer_store_b8(b, gate, i, 0, 0); }
+  __device__ void put_word(int32_t off, uint32_t w) const { __builtin_amdgcn_raw_buffer_store_b32(w, gate, off, 0, 0); }
 };
+
+// The gate producer of segment c.
+__device__ inline GateRes gate_res(const GateArgs& a, const SelCtx& c) {
+  GateRes p;
+  gate_buffers(a, c, p.rho, p.gate);
+  p.needs_class = true;
+  p.aligned = (reinterpret_cast<uintptr_t>(a.gate + c.ubase + size_t(c.s0)) & 3u) == 0;
+  return p;
+}
 
 // Work-group (sequence, unit): the whole segment's gate bytes and tau.
 __global__ __launch_bounds__(kResThreads) void gate_resident_kernel(GateArgs a) {
@@ -172,16 +215,59 @@ __global__ __launch_bounds__(kResThreads) void gate_resident_kernel(GateArgs a) 
     a.tau[size_t(blockIdx.y) * lay.n_seqs + c.seq] = c.k > 0 ? order_key_value(T) : __builtin_nanf("");
 }
 
+// Splitter path (segsel_split.h).  Work-group (1, seq, unit): k = min(B,
+// N_hist) and the splitters of the segment.
+template <bool LDS>
+__global__ __launch_bounds__(kSpThreads) void gate_split_sample_kernel(GateArgs a) {
+  __shared__ SpSampleShared sh;
+  __shared__ int32_t nh_s;
+  const Layout& lay = a.lay;
+  SelCtx c = sel_ctx(lay);
+  const SeqFrames<LDS> fr = sp_frames<LDS>(sh.fstart, sh.fend, lay, c.seq);
+  if (threadIdx.x < 64) {  // N_hist: every frame of the sequence but the last
+    int32_t nh = 0;
+    for (int32_t f = threadIdx.x; f + 1 < fr.nf; f += 64) nh += frame_size(lay, fr.f0 + f);
+    nh = wave_sum(nh);
+    if (threadIdx.x == 0) nh_s = nh;
+  }
+  __syncthreads();
+  c.k = min(lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq], nh_s);
+  split_sample(gate_res(a, c), sh, fr, a.sel, lay, c, nh_s);
+}
+
+// Work-group (part, seq, unit): the gate bytes the splitters decide.
+__global__ __launch_bounds__(kSpPassThreads) void gate_split_classify_kernel(GateArgs a) {
+  __shared__ SpPassShared sh;
+  const SelCtx c = sel_ctx(a.lay);
+  split_classify(gate_res(a, c), sh, a.sel, a.lay, c);
+}
+
+// Work-group (1, seq, unit): T, the open gate bytes and tau.
+__global__ __launch_bounds__(kSpThreads) void gate_split_resolve_kernel(GateArgs a) {
+  __shared__ SpResolveShared sh;
+  const SelCtx c = sel_ctx(a.lay);
+  int32_t mode;
+  const uint32_t T = split_resolve<false>(gate_res(a, c), sh, a.sel, a.lay, c, &mode);
+  if (a.tau && threadIdx.x == 0)
+    a.tau[size_t(blockIdx.z) * a.lay.n_seqs + c.seq] = mode != kModeNone ? order_key_value(T) : __builtin_nanf("");
+}
+
 }  // namespace
 
 hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
-  if (g.sel.resident) {
-    if (g.lay.n_units == 0 || g.lay.n_seqs == 0) return hipSuccess;
-    hipLaunchKernelGGL(gate_resident_kernel, dim3(g.lay.n_seqs, g.lay.n_units), dim3(kResThreads), 0, stream, g);
-    return hipGetLastError();
+  switch (g.sel.path) {
+    case kSelPathResident:
+      if (g.lay.n_units == 0 || g.lay.n_seqs == 0) return hipSuccess;
+      hipLaunchKernelGGL(gate_resident_kernel, dim3(g.lay.n_seqs, g.lay.n_units), dim3(kResThreads), 0, stream, g);
+      return hipGetLastError();
+    case kSelPathSplit:
+      return launch_split(g.sel.lds_frames ? gate_split_sample_kernel<true> : gate_split_sample_kernel<false>,
+                          gate_split_classify_kernel, gate_split_resolve_kernel,
+                          static_cast<void (*)(GateArgs)>(nullptr), g, g.sel, g.lay, stream);
+    default:
+      return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
+                               gate_emit_kernel, g, g.sel, g.lay, stream);
   }
-  return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
-                           gate_emit_kernel, g, g.sel, g.lay, stream);
 }
 
 }  // namespace stlite

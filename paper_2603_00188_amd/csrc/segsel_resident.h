@@ -44,7 +44,8 @@ struct ResShared {
 
 // Classes of the lane's four tokens base + lane + 64 e (e = 0..3) of the wave
 // step starting at segment token `base`; cur is the wave-uniform frame cursor.
-__device__ __forceinline__ void res_classify(const SeqFrames<true>& fr, int32_t& cur, int32_t s0, int32_t base,
+template <bool LDS>
+__device__ __forceinline__ void res_classify(const SeqFrames<LDS>& fr, int32_t& cur, int32_t s0, int32_t base,
                                              int (&cls)[4]) {
   const int lane = threadIdx.x & 63;
   const StepFrames st = step_frames(fr, cur, s0 + base, kResStep);

@@ -7,6 +7,7 @@
 // ~order_key(S) (ascending key = descending S).
 #include "segsel.h"
 #include "segsel_resident.h"
+#include "segsel_split.h"
 #include "stlite_internal.h"
 
 namespace stlite {
@@ -119,6 +120,9 @@ __global__ __launch_bounds__(kSelThreads) void select_emit_kernel(SelectArgs a) 
 
 // The top-B of one segment held by one work-group (segsel_resident.h).
 struct SelectRes {
+  static constexpr int kGroup = 2;        // tiles a classifying wave loads at once (segsel_split.h)
+  static constexpr bool kDirect = false;  // a ranked list: the splitter path emits it from codes
+  static constexpr bool aligned = false;
   __amdgpu_buffer_rsrc_t a_base;  // the segment's A, Phi and gate (out-of-range lanes read 0)
   __amdgpu_buffer_rsrc_t phi;
   __amdgpu_buffer_rsrc_t gate;
@@ -166,7 +170,65 @@ struct SelectRes {
   __device__ void emit(int32_t i, int, bool take, int32_t pos) const {
     if (take && pos < k) kept[pos] = s0 + i;
   }
+
+  // Whether a token of class cls can be selected (segsel_split.h): all can.
+  __device__ bool selectable(int) const { return true; }
+
+  // keys() for a whole tile of one class (cls, wave-uniform) inside the segment.
+  __device__ void keys_uniform(int32_t base, int cls, const Raw& r, uint32_t (&key)[4]) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float S = score_of(r.A[e], r.ph[e], r.g[e], cls != kText);
+      if (score) score[base + 64 * e + lane] = S;
+      key[e] = min(~order_key(S), kSelKeyMax);
+    }
+  }
+
+  // The splitter path (segsel_split.h): one token's inputs and key, and a
+  // taken token's kept entry at its rank.
+  struct Raw1 {
+    float A, ph;
+    uint32_t g;
+  };
+
+  __device__ void load1(int32_t i, Raw1& r) const {
+    r.A = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
+    r.ph = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
+    r.g = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+  }
+
+  __device__ uint32_t key1(const Raw1& r, int cls) const {
+    return min(~order_key(score_of(r.A, r.ph, r.g, cls != kText)), kSelKeyMax);
+  }
+
+  __device__ void emit_code(int32_t i, bool, bool take, int32_t pos) const {
+    if (take && pos < k) kept[pos] = s0 + i;
+  }
+
+  __device__ void put_byte(int32_t, uint8_t) const {}  // (kDirect only)
+  __device__ void put_word(int32_t, uint32_t) const {}
 };
+
+// The producer of segment c of `unit` (score: write S, when the call asks for it).
+__device__ inline SelectRes select_res(const SelectArgs& a, const SelCtx& c, int32_t unit, bool score) {
+  SelectRes p;
+  const size_t seg0 = c.ubase + size_t(c.s0);
+  p.a_base = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.a_base) + seg0, 0, c.n * 4, kBufferFlags);
+  p.has_phi = a.phi != nullptr;
+  p.has_gate = a.gate != nullptr;
+  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0, c.n * 4,
+                                            kBufferFlags);
+  p.gate = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.has_gate ? a.gate + seg0 : nullptr), 0,
+                                             p.has_gate ? c.n : 0, kBufferFlags);
+  p.needs_class = p.has_phi || p.has_gate;
+  p.alpha = a.alpha;
+  p.score = (score && a.score) ? a.score + seg0 : nullptr;
+  p.kept = a.kept + size_t(unit) * a.lay.total_budget + a.lay.cu_budget[c.seq];
+  p.k = c.k;
+  p.s0 = c.s0;
+  return p;
+}
 
 // Work-group (sequence, unit): the whole segment's kept list (and S).
 __global__ __launch_bounds__(kResThreads) void select_resident_kernel(SelectArgs a) {
@@ -179,21 +241,7 @@ __global__ __launch_bounds__(kResThreads) void select_resident_kernel(SelectArgs
   c.part = 0;
   c.ubase = size_t(blockIdx.y) * lay.total_tokens;
   c.k = lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq];
-  SelectRes p;
-  const size_t seg0 = c.ubase + size_t(c.s0);
-  p.a_base = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.a_base) + seg0, 0, c.n * 4, kBufferFlags);
-  p.has_phi = a.phi != nullptr;
-  p.has_gate = a.gate != nullptr;
-  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0, c.n * 4,
-                                            kBufferFlags);
-  p.gate = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.has_gate ? a.gate + seg0 : nullptr), 0,
-                                             p.has_gate ? c.n : 0, kBufferFlags);
-  p.needs_class = p.has_phi || p.has_gate;
-  p.alpha = a.alpha;
-  p.score = a.score ? a.score + seg0 : nullptr;
-  p.kept = a.kept + size_t(blockIdx.y) * lay.total_budget + lay.cu_budget[c.seq];
-  p.k = c.k;
-  p.s0 = c.s0;
+  const SelectRes p = select_res(a, c, blockIdx.y, true);
   SeqFrames<true> fr;
   fr.meta = lay.frame_meta;
   fr.fs = sh.fstart;
@@ -209,16 +257,55 @@ __global__ __launch_bounds__(kResThreads) void select_resident_kernel(SelectArgs
   res_select(p, sh, fr, c);
 }
 
+// Splitter path (segsel_split.h), grids (1 or parts, seq, unit); k = B of the
+// sequence.
+template <bool LDS>
+__global__ __launch_bounds__(kSpThreads) void select_split_sample_kernel(SelectArgs a) {
+  __shared__ SpSampleShared sh;
+  SelCtx c = sel_ctx(a.lay);
+  c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  const SeqFrames<LDS> fr = sp_frames<LDS>(sh.fstart, sh.fend, a.lay, c.seq);
+  __syncthreads();
+  split_sample(select_res(a, c, blockIdx.z, false), sh, fr, a.sel, a.lay, c, c.n);
+}
+
+__global__ __launch_bounds__(kSpPassThreads) void select_split_classify_kernel(SelectArgs a) {
+  __shared__ SpPassShared sh;
+  SelCtx c = sel_ctx(a.lay);
+  c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  split_classify(select_res(a, c, blockIdx.z, true), sh, a.sel, a.lay, c);
+}
+
+__global__ __launch_bounds__(kSpThreads) void select_split_resolve_kernel(SelectArgs a) {
+  __shared__ SpResolveShared sh;
+  SelCtx c = sel_ctx(a.lay);
+  c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  int32_t mode;
+  split_resolve<true>(select_res(a, c, blockIdx.z, false), sh, a.sel, a.lay, c, &mode);
+}
+
+__global__ __launch_bounds__(kSpPassThreads) void select_split_emit_kernel(SelectArgs a) {
+  SelCtx c = sel_ctx(a.lay);
+  c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  split_emit(select_res(a, c, blockIdx.z, false), a.sel, a.lay, c);
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
-  if (a.sel.resident) {
-    if (a.lay.n_units == 0 || a.lay.n_seqs == 0) return hipSuccess;
-    hipLaunchKernelGGL(select_resident_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(kResThreads), 0, stream, a);
-    return hipGetLastError();
+  switch (a.sel.path) {
+    case kSelPathResident:
+      if (a.lay.n_units == 0 || a.lay.n_seqs == 0) return hipSuccess;
+      hipLaunchKernelGGL(select_resident_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(kResThreads), 0, stream, a);
+      return hipGetLastError();
+    case kSelPathSplit:
+      return launch_split(a.sel.lds_frames ? select_split_sample_kernel<true> : select_split_sample_kernel<false>,
+                          select_split_classify_kernel, select_split_resolve_kernel, select_split_emit_kernel, a,
+                          a.sel, a.lay, stream);
+    default:
+      return launch_sel_passes(a.sel.lds_frames ? select_produce_kernel<true> : select_produce_kernel<false>,
+                               select_emit_kernel, a, a.sel, a.lay, stream);
   }
-  return launch_sel_passes(a.sel.lds_frames ? select_produce_kernel<true> : select_produce_kernel<false>,
-                           select_emit_kernel, a, a.sel, a.lay, stream);
 }
 
 }  // namespace stlite

@@ -2,6 +2,7 @@
 // configuration and status codes for the C ABI declared in include/stlite.h.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -110,15 +111,65 @@ Facts derive(const stlite_problem* p) {
   return f;
 }
 
-// Workspace of one selection (gate or top-B): a row of 32-bit keys per unit
-// (every sequence's keys starting 16-byte aligned), the part histograms of the
-// three radix levels, the parts' counts below the level-1 prefix and the
-// per-segment state.
-size_t seg_bytes(const stlite_problem* p, const Facts& f) {
+// Workspace of the four passes of one selection (gate or top-B): a row of
+// 32-bit keys per unit (every sequence's keys starting 16-byte aligned), the
+// part histograms of the three radix levels, the parts' counts below the
+// level-1 prefix and the per-segment state.
+size_t four_pass_bytes(const stlite_problem* p, const Facts& f) {
   const size_t segparts = size_t(f.units) * p->n_seqs * f.sel_parts;
   return align_up(size_t(f.units) * size_t(sel_key_stride(p->total_tokens, p->n_seqs)) * sizeof(uint32_t)) +
          2 * align_up(segparts * (2048 + 64) * sizeof(uint32_t)) + align_up(segparts * (1024 + 32) * sizeof(uint32_t)) +
          align_up(segparts * sizeof(int32_t)) + align_up(size_t(f.units) * p->n_seqs * 8 * sizeof(int32_t));
+}
+
+// Workspace of the splitter path: a code byte per token, the tile records,
+// the candidate lists and the per-segment state.
+size_t split_bytes(const stlite_problem* p, const Facts& f) {
+  const size_t U = size_t(f.units);
+  return align_up(U * size_t(sp_tile_stride(p->total_tokens, p->n_seqs)) * 256) +
+         align_up(U * size_t(sp_tile_stride(p->total_tokens, p->n_seqs)) * 8 * sizeof(int32_t)) +
+         align_up(U * size_t(sp_cand_stride(p->total_tokens, p->n_seqs)) * sizeof(uint2)) +
+         align_up(U * p->n_seqs * kSpWords * sizeof(int32_t));
+}
+
+// Either path may run a call's selection (the diagnostic override below
+// picks among them), so the workspace holds the larger of the two; they
+// share its bytes.
+size_t seg_bytes(const stlite_problem* p, const Facts& f) { return std::max(four_pass_bytes(p, f), split_bytes(p, f)); }
+
+// Work-groups per segment of the splitter path's classify and emit passes:
+// 32 tiles each (eight per wave) for the longest segment, fewer parts when
+// that would exceed ~16k work-groups.
+int32_t split_parts(const stlite_problem* p, const Facts& f) {
+  const int64_t segs = std::max<int64_t>(f.units * p->n_seqs, 1);
+  const int64_t tiles = std::max<int64_t>(ceil_div(f.max_seq, 256), 1);
+  int64_t parts = ceil_div(tiles, 32);
+  parts = std::min(parts, std::max<int64_t>(ceil_div(16384, segs), 1));
+  return int32_t(std::max<int64_t>(parts, 1));
+}
+
+// The selection path.  By default segments of at most kSelResidentCapacity
+// tokens run resident and longer ones take the splitter path.  The
+// environment variable STLITE_SELECT_PATH overrides this for diagnostics and
+// cross-checks: "four_pass", "split", "split_exact" (the splitter path with
+// every segment resolved by its exact fallback) or "resident" (honoured when
+// every segment fits).
+void sel_path(const Facts& f, SelPlan& s) {
+  const bool resident_ok = s.lds_frames && f.max_seq <= kSelResidentCapacity;
+  s.path = resident_ok ? kSelPathResident : kSelPathSplit;
+  s.split_exact = 0;
+  const char* e = getenv("STLITE_SELECT_PATH");
+  if (!e) return;
+  if (!strcmp(e, "four_pass")) {
+    s.path = kSelPathFourPass;
+  } else if (!strcmp(e, "split")) {
+    s.path = kSelPathSplit;
+  } else if (!strcmp(e, "split_exact")) {
+    s.path = kSelPathSplit;
+    s.split_exact = 1;
+  } else if (!strcmp(e, "resident") && resident_ok) {
+    s.path = kSelPathResident;
+  }
 }
 
 SelPlan sel_carve(const stlite_problem* p, const Facts& f, char* w) {
@@ -126,7 +177,19 @@ SelPlan sel_carve(const stlite_problem* p, const Facts& f, char* w) {
   SelPlan s;
   s.parts = f.sel_parts;
   s.lds_frames = f.max_seq_frames <= kSelFrames ? 1 : 0;
-  s.resident = (s.lds_frames && f.max_seq <= kSelResidentCapacity) ? 1 : 0;
+  sel_path(f, s);
+  s.split_parts = split_parts(p, f);
+  {  // the splitter path's arrays, over the same bytes as the four passes' ones
+    const size_t U = size_t(f.units);
+    char* x = w;
+    s.codes = reinterpret_cast<uint8_t*>(x);
+    x += align_up(U * size_t(sp_tile_stride(p->total_tokens, p->n_seqs)) * 256);
+    s.tiles = reinterpret_cast<int32_t*>(x);
+    x += align_up(U * size_t(sp_tile_stride(p->total_tokens, p->n_seqs)) * 8 * sizeof(int32_t));
+    s.cands = reinterpret_cast<uint2*>(x);
+    x += align_up(U * size_t(sp_cand_stride(p->total_tokens, p->n_seqs)) * sizeof(uint2));
+    s.sstate = reinterpret_cast<int32_t*>(x);
+  }
   s.keys = reinterpret_cast<uint32_t*>(w);
   w += align_up(size_t(f.units) * size_t(sel_key_stride(p->total_tokens, p->n_seqs)) * sizeof(uint32_t));
   s.hist0 = reinterpret_cast<uint32_t*>(w);

@@ -75,9 +75,17 @@ struct RhoArgs {
 // Frames of one sequence that the selection kernels keep in LDS.
 constexpr int kSelFrames = 1024;
 
-// Workspace of one exact k-selection over (unit, sequence) segments, each cut
-// into `parts` parts (segsel.h).
+// How a call's selections run.
+enum SelPath : int32_t {
+  kSelPathResident = 0,  // one work-group per segment, keys in registers (segsel_resident.h); no workspace
+  kSelPathSplit = 1,     // splitters from a sample, then one classifying pass (segsel_split.h)
+  kSelPathFourPass = 2,  // four radix passes over stored keys (segsel.h)
+};
+
+// Workspace and launch shape of one exact k-selection over (unit, sequence)
+// segments.
 struct SelPlan {
+  // four passes (segsel.h), each segment cut into `parts` parts
   uint32_t* keys;        // [units][sel_key_stride]: one key per token
   uint32_t* hist0;       // [units][seqs][parts][2048 + 64]: level-0 part histograms (bins, 32-bin sums)
   uint32_t* hist1;       // [units][seqs][parts][2048 + 64]: level 1
@@ -85,9 +93,32 @@ struct SelPlan {
   int32_t* below;        // [units][seqs][parts]: keys below the level-1 prefix
   int32_t* state;        // [units][seqs][8]: k, then prefix and rank after levels 0 and 1
   int32_t parts;         // 1 .. 16
+  // splitters (segsel_split.h); the same workspace bytes as the four passes' arrays
+  uint8_t* codes;        // [units][256 * sp_tile_stride]: each token's class against the splitters, per tile
+  int32_t* tiles;        // [units][sp_tile_stride][8]: per 256-token tile counts and output offset
+  uint2* cands;          // [units][sp_cand_stride]: (key, token) of the tokens between the splitters
+  int32_t* sstate;       // [units][seqs][kSpWords]: splitters, counts, mode, T, tie cut
+  int32_t split_parts;   // work-groups per segment of the classify and emit passes
+  int32_t split_exact;   // 1: resolve every segment by the exact streaming selection (diagnostic)
   int32_t lds_frames;    // 1: no sequence has more than kSelFrames frames
-  int32_t resident;      // 1: every segment fits one work-group (segsel_resident.h), which uses no workspace
+  int32_t path;          // SelPath
 };
+
+// Splitter selection layout: per unit, one tile record per 256 tokens of each
+// sequence (sequence seq's first record at sp_tile_base) and a candidate list
+// per sequence sized 40/256 (~15.6 %) of its tokens + 256 (from
+// sp_cand_base(s0, seq) to sp_cand_base(s0 + n, seq + 1)).  Both bases are
+// monotone in (s0, seq), and a sequence's range ends at or before the next
+// sequence's base.
+constexpr int kSpWords = 16;
+__host__ __device__ inline int64_t sp_tile_stride(int64_t total_tokens, int32_t n_seqs) {
+  return total_tokens / 256 + int64_t(n_seqs) + 1;
+}
+__host__ __device__ inline int64_t sp_tile_base(int64_t s0, int32_t seq) { return s0 / 256 + int64_t(seq); }
+__host__ __device__ inline int64_t sp_cand_base(int64_t s0, int32_t seq) { return (s0 * 40) / 256 + 256 * int64_t(seq); }
+__host__ __device__ inline int64_t sp_cand_stride(int64_t total_tokens, int32_t n_seqs) {
+  return sp_cand_base(total_tokens, n_seqs) + 256;
+}
 
 // Longest sequence whose selections run segment-resident (one work-group per
 // segment, keys kept in registers).
@@ -208,8 +239,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // Total order of fp32 values as unsigned integers (ascending key = ascending
 // value); -0 is folded onto +0 so that the two zeros tie.
 __device__ __forceinline__ uint32_t order_key(float x) {
-  uint32_t u = __float_as_uint(x + 0.0f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t u = __float_as_uint(x + 0.0f);
+  // negative: all bits flipped; non-negative: the sign bit set
+  return u ^ (uint32_t(int32_t(u) >> 31) | 0x80000000u);
 }
 
 __device__ __forceinline__ float order_key_value(uint32_t key) {

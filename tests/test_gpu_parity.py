@@ -176,24 +176,30 @@ def test_stage_threshold_and_select_exact(torch_cuda):
 # Layouts of the stage-exact selection tests: (frames, (rows, cols), text) per sequence.
 STAGE_LAYOUTS = {
     # segments of 27,300 and 5,935 tokens: one work-group per segment keeps them on chip
-    "resident": ((13, (40, 50), 100), (5, (30, 37), 77)),
+    "short": ((13, (40, 50), 100), (5, (30, 37), 77)),
     # a 168,000-token segment, longer than the on-chip selection holds: every
-    # segment of the call takes the four-pass selection, cut into parts
-    "four_pass": ((80, (40, 50), 100), (5, (30, 37), 77)),
+    # segment of the call takes the splitter selection by default
+    "long": ((80, (40, 50), 100), (5, (30, 37), 77)),
 }
 
+# (layout, selection path forced through STLITE_SELECT_PATH; None = the default)
+STAGE_CASES = [("short", None), ("long", None), ("long", "four_pass"), ("long", "split_exact"),
+               ("short", "split"), ("short", "split_exact"), ("short", "four_pass")]
 
-@pytest.mark.parametrize("layout", list(STAGE_LAYOUTS))
+
+@pytest.mark.parametrize("layout,path", STAGE_CASES)
 @pytest.mark.parametrize("values", ["few", "many"])
-def test_stage_exact_many_parts_and_ties(torch_cuda, layout, values):
+def test_stage_exact_many_parts_and_ties(torch_cuda, monkeypatch, layout, path, values):
     """Stage-isolated on long sequences, with inputs drawn from a few values
-    (long runs of equal keys straddling wave and part boundaries; far more
-    tokens share the pivot's top 16 key bits than the on-chip candidate list
-    holds) or from a few hundred (ties that fit the list): gate, tau, S and
-    kept lists must equal the oracle's exactly."""
+    (long runs of equal keys straddling wave, tile and part boundaries; the
+    splitters land on tied keys) or from a few hundred (the k-th key among the
+    splitter candidates, with ties there): gate, tau, S and kept lists must
+    equal the oracle's exactly, on every selection path."""
     import torch
     from oracle import stlite_oracle as O
     from paper_2603_00188_amd import stlite as S
+    if path:
+        monkeypatch.setenv("STLITE_SELECT_PATH", path)
     seqs, metas, cu = [], [], [0]
     for nf, (r, c), nt in STAGE_LAYOUTS[layout]:
         off = cu[-1]
@@ -243,6 +249,22 @@ def test_stage_exact_many_parts_and_ties(torch_cuda, layout, values):
                 assert np.array_equal(score[u, a:b], s32), (beta, u, s)
                 want = O.select_topk(s32.astype(np.float64), B) + a
                 assert (kept[u, cu_budget[s]:cu_budget[s + 1]] == want).all(), (beta, u, s)
+
+
+@pytest.mark.parametrize("path", ["four_pass", "split", "split_exact"])
+def test_selection_paths_agree(torch_cuda, monkeypatch, path):
+    """The whole pass on the small cases (ragged batches, sequences shorter
+    than a tile, a 1 x 1 frame, a zero budget) under each forced selection
+    path gives the same bits as under the default path."""
+    H = _H()
+    for name in ("ragged", "tiles", "dups", "beta_tiny"):
+        case = H.Case(SMALL[name])
+        monkeypatch.delenv("STLITE_SELECT_PATH", raising=False)
+        ref = case.run()
+        monkeypatch.setenv("STLITE_SELECT_PATH", path)
+        got = case.run()
+        for key in ("gate", "tau", "kept", "score", "k_out", "v_out"):
+            assert np.array_equal(got[key], ref[key], equal_nan=True), (name, path, key)
 
 
 def test_split_tsg_matches_fused(torch_cuda):
