@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kSelThreads) void gate_emit_kernel(GateArgs a) {
 
 // The rank gate of one segment held by one work-group (segsel_resident.h).
 struct GateRes {
-  static constexpr int kGroup = 4;      // tiles a classifying wave loads at once (segsel_split.h)
+  static constexpr int kGroup = 1;      // tiles a classifying wave loads at once (segsel_split.h)
   static constexpr bool kDirect = true;  // the splitter path writes the gate bytes directly
   __amdgpu_buffer_rsrc_t rho;
   __amdgpu_buffer_rsrc_t gate;
@@ -155,6 +155,7 @@ struct GateRes {
   __device__ void load1(int32_t i, Raw1& w) const {
     w.r = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rho, i * 4, 0, 0));
   }
+  __device__ void load1_rest(int32_t, int, Raw1&) const {}
 
   __device__ uint32_t key1(const Raw1& w, int cls) const {
     return cls == kHist ? min(order_key(w.r), kSelKeyMax) : kSelNever;
@@ -223,16 +224,21 @@ __global__ __launch_bounds__(kSpThreads) void gate_split_sample_kernel(GateArgs 
   __shared__ int32_t nh_s;
   const Layout& lay = a.lay;
   SelCtx c = sel_ctx(lay);
+  const int32_t budget = lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq];
+  const GateRes p = gate_res(a, c);
+  SpGather<GateRes> g;
+  sp_gather(p, lay, c, g);  // the sample's loads first: the frame table's overlap them
   const SeqFrames<LDS> fr = sp_frames<LDS>(sh.fstart, sh.fend, lay, c.seq);
+  if (LDS) __syncthreads();
   if (threadIdx.x < 64) {  // N_hist: every frame of the sequence but the last
     int32_t nh = 0;
-    for (int32_t f = threadIdx.x; f + 1 < fr.nf; f += 64) nh += frame_size(lay, fr.f0 + f);
+    for (int32_t f = threadIdx.x; f + 1 < fr.nf; f += 64) nh += fr.end(f) - fr.start(f);
     nh = wave_sum(nh);
     if (threadIdx.x == 0) nh_s = nh;
   }
   __syncthreads();
-  c.k = min(lay.cu_budget[c.seq + 1] - lay.cu_budget[c.seq], nh_s);
-  split_sample(gate_res(a, c), sh, fr, a.sel, lay, c, nh_s);
+  c.k = min(budget, nh_s);
+  split_sample(p, sh, fr, a.sel, lay, c, nh_s, g);
 }
 
 // Work-group (part, seq, unit): the gate bytes the splitters decide.

@@ -67,7 +67,9 @@ enum : int32_t {
   kModeNone = 0, kModeTieLo = 1, kModeMid = 2, kModeTieHi = 3, kModeExact = 4, kModeAll = 5, kModeOpen = 6
 };
 // Segment state words.
-enum : int { kSpLo = 0, kSpHi, kSpK, kSpCount, kSpMode, kSpT, kSpCut, kSpNeed };
+enum : int { kSpLo = 0, kSpHi, kSpK, kSpCount, kSpMode, kSpT, kSpCut, kSpNeed, kSpLe, kSpEqLo, kSpEqHi };
+// (kSpLe, kSpEqLo, kSpEqHi: a direct output's totals of keys <= lo, == lo and
+// == hi, summed by classify; a ranked list's come from its tile records.)
 // Tile record words: counts of codes 0..3, taken candidates, output offset,
 // and (kModeAll) the largest selectable key plus one (0: none).
 enum : int { kTileLess = 0, kTileEqLo, kTileMid, kTileEqHi, kTileTaken, kTileOut, kTileMax, kTileWords = 8 };
@@ -143,6 +145,95 @@ __device__ __forceinline__ int32_t sp_block_inscan(int32_t v, int32_t* wtot, int
   *total = __builtin_amdgcn_readlane(ts, kSpWaves - 1);
   __syncthreads();  // wtot is free again
   return incl + before;
+}
+
+// The same scan without the closing barrier: the caller synchronises before
+// wtot is written again.
+__device__ __forceinline__ int32_t sp_block_inscan1(int32_t v, int32_t* wtot, int32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t incl = sp_wave_inscan(v);
+  if (lane == 63) wtot[wave] = incl;
+  __syncthreads();
+  const int32_t t = lane < kSpWaves ? wtot[lane] : 0;
+  const int32_t ts = sp_wave_inscan(t);
+  const int32_t before = wave > 0 ? __builtin_amdgcn_readlane(ts, wave - 1) : 0;
+  *total = __builtin_amdgcn_readlane(ts, kSpWaves - 1);
+  return incl + before;
+}
+
+// Bins of two 2048-bin LDS histograms holding ranks ra of ha and rb of hb
+// (1-based; a rank of 0 is not looked for), and the ranks inside them, to
+// out[0..1] and out[2..3], from one scan: thread t takes bins 2t and 2t + 1 of
+// both, their sums packed in the halves of one word (every histogram here
+// counts fewer than 65536 keys).  The caller synchronised after the
+// counting; returns after a barrier.
+__device__ __forceinline__ void sp_pivot2(const uint32_t* ha, int32_t ra, const uint32_t* hb, int32_t rb,
+                                          int32_t* wtot, int32_t* out) {
+  const int32_t t = threadIdx.x;
+  const int32_t a0 = int32_t(ha[2 * t]), a1 = int32_t(ha[2 * t + 1]);
+  const int32_t b0 = int32_t(hb[2 * t]), b1 = int32_t(hb[2 * t + 1]);
+  int32_t total;
+  const int32_t incl = sp_block_inscan1((a0 + a1) | ((b0 + b1) << 16), wtot, &total);
+  const int32_t ia = incl & 0xffff, ib = incl >> 16;
+  const int32_t fa = ia - a0 - a1, fb = ib - b0 - b1;
+  if (ra > 0 && ia >= ra && fa < ra) {
+    out[0] = fa + a0 >= ra ? 2 * t : 2 * t + 1;
+    out[1] = fa + a0 >= ra ? ra - fa : ra - fa - a0;
+  }
+  if (rb > 0 && ib >= rb && fb < rb) {
+    out[2] = fb + b0 >= rb ? 2 * t : 2 * t + 1;
+    out[3] = fb + b0 >= rb ? rb - fb : rb - fb - b0;
+  }
+  __syncthreads();
+}
+
+// One histogram's pivot as in sp_pivot2, plus the count of the bin found
+// (out[2]).
+__device__ __forceinline__ void sp_pivot1(const uint32_t* h, int32_t r, int32_t* wtot, int32_t* out) {
+  const int32_t t = threadIdx.x;
+  const int32_t h0 = int32_t(h[2 * t]), h1 = int32_t(h[2 * t + 1]);
+  int32_t total;
+  const int32_t incl = sp_block_inscan1(h0 + h1, wtot, &total);
+  const int32_t f = incl - h0 - h1;
+  if (incl >= r && f < r) {
+    const bool first = f + h0 >= r;
+    out[0] = first ? 2 * t : 2 * t + 1;
+    out[1] = first ? r - f : r - f - h0;
+    out[2] = first ? h0 : h1;
+  }
+  __syncthreads();
+}
+
+// sp_pivot1 over a histogram of `bins` bins (a power of two, at most 8
+// kSpThreads): thread t sums bins [t w, t w + w), w = bins / kSpThreads or 1,
+// and the thread holding rank r walks its own.
+__device__ __forceinline__ void sp_pivot_wide(const uint32_t* h, int32_t bins, int32_t r, int32_t* wtot,
+                                              int32_t* out) {
+  const int32_t t = threadIdx.x;
+  const int32_t w = bins > kSpThreads ? bins / kSpThreads : 1;
+  const int32_t b0 = t * w;
+  int32_t sum = 0;
+  if (w == 8) {
+    const uint4 x = *reinterpret_cast<const uint4*>(h + b0), y = *reinterpret_cast<const uint4*>(h + b0 + 4);
+    sum = int32_t(x.x + x.y + x.z + x.w + y.x + y.y + y.z + y.w);
+  } else if (b0 < bins) {
+    for (int32_t j = 0; j < w; ++j) sum += int32_t(h[b0 + j]);
+  }
+  int32_t total;
+  const int32_t incl = sp_block_inscan1(sum, wtot, &total);
+  int32_t f = incl - sum;
+  if (b0 < bins && incl >= r && f < r) {
+    int32_t j = 0;
+    for (; j + 1 < w; ++j) {
+      const int32_t x = int32_t(h[b0 + j]);
+      if (f + x >= r) break;
+      f += x;
+    }
+    out[0] = b0 + j;
+    out[1] = r - f;
+    out[2] = int32_t(h[b0 + j]);
+  }
+  __syncthreads();
 }
 
 // Bin of a 2048-bin LDS histogram holding rank r (1-based) of its counts, and
@@ -302,23 +393,65 @@ __device__ __forceinline__ void sp_tile_keys(const Prod& p, FrameWin& win, const
 // ---------------------------------------------------------------------------
 
 struct SpSampleShared {
-  uint32_t hlo[2048];
-  uint32_t hhi[2048];
+  uint32_t hist[2][2][2048];  // two sets (alternate levels) of the lo and hi histograms
   int32_t fstart[kSelFrames];
   int32_t fend[kSelFrames];
   int32_t wtot[kSpWaves];
   int32_t piv[4];
 };
 
-// Prod provides Raw1, void load1(int32_t i, Raw1&) and uint32_t key1(const
-// Raw1&, int cls): the inputs and the key of segment token i; needs_class.
-// c.k keys are to be selected among n_sel selectable tokens.  Writes lo, hi,
-// k, the mode and a zero candidate count.
+// The sample positions of one segment and the first step of their loads,
+// issued before anything else of the sample kernel: the n tokens fall in S =
+// min(2048, n) strata [floor(j n / S), floor((j + 1) n / S)), and stratum j
+// (thread j mod kSpThreads, slot j / kSpThreads) gives one hashed position.
+// Prod provides Raw1, void load1(int32_t i, Raw1&), void load1_rest(int32_t
+// i, int cls, Raw1&) and uint32_t key1(const Raw1&, int cls): the inputs of
+// segment token i, in two steps (the second may skip what the first and the
+// class make unneeded), and its key; needs_class.
+template <class Prod>
+struct SpGather {
+  uint32_t valid;
+  int32_t pos[kSpSampleEach];
+  typename Prod::Raw1 raw[kSpSampleEach];
+};
+
+template <class Prod>
+__device__ __forceinline__ void sp_gather(const Prod& p, const Layout& lay, const SelCtx& c, SpGather<Prod>& g) {
+  const int32_t n = c.n, S = min(kSpSample, n);
+  const uint32_t salt = sp_hash(uint32_t(sel_seg(lay)) * 0x9e3779b9u + 0x51ed27u);
+  g.valid = 0u;
+#pragma unroll
+  for (int e = 0; e < kSpSampleEach; ++e) {
+    const int32_t j = int32_t(threadIdx.x) + kSpThreads * e;
+    g.pos[e] = 0;
+    if (j < S) {
+      const int32_t a = S == n ? j : int32_t((int64_t(j) * n) >> 11);
+      const int32_t b = S == n ? j + 1 : int32_t((int64_t(j + 1) * n) >> 11);
+      g.pos[e] = a + int32_t(__umulhi(sp_hash(uint32_t(j) ^ salt), uint32_t(b - a)));
+      g.valid |= 1u << e;
+    }
+    p.load1(g.pos[e], g.raw[e]);  // position 0 of an empty segment reads 0 (buffer bounds)
+  }
+}
+
+// c.k keys are to be selected among n_sel selectable tokens, from the sample
+// sp_gather started.  Writes lo, hi, k, the mode and a zero candidate count.
 template <class Prod, bool LDS>
 __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<LDS>& fr, const SelPlan& s,
-                             const Layout& lay, const SelCtx& c, int32_t n_sel) {
+                             const Layout& lay, const SelCtx& c, int32_t n_sel, SpGather<Prod>& g) {
   int32_t* st = sp_state(s, lay);
   const int32_t n = c.n, k = c.k;
+  if (threadIdx.x == 0) {
+    st[kSpLe] = 0;
+    st[kSpEqLo] = 0;
+    st[kSpEqHi] = 0;
+  }
+  if (Prod::kDirect) {  // classify writes the records of tiles with ties (or of every tile in kModeAll)
+    int32_t* tiles = sp_tiles(s, lay, c);
+    const int32_t ntile = (n + kSpTile - 1) / kSpTile;
+    for (int32_t i = threadIdx.x; i < ntile * (kTileWords / 4); i += kSpThreads)
+      reinterpret_cast<int4*>(tiles)[i] = make_int4(0, 0, 0, 0);
+  }
   if (n <= 0 || k <= 0 || k >= n_sel) {
     if (threadIdx.x == 0) {
       st[kSpLo] = 0;
@@ -330,24 +463,10 @@ __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<
     return;
   }
   const int32_t S = min(kSpSample, n);
-  const uint32_t salt = sp_hash(uint32_t(sel_seg(lay)) * 0x9e3779b9u + 0x51ed27u);
+  const uint32_t valid = g.valid;
+  const int32_t (&pos)[kSpSampleEach] = g.pos;
+  typename Prod::Raw1 (&raw)[kSpSampleEach] = g.raw;
   uint32_t key[kSpSampleEach];
-  int32_t pos[kSpSampleEach];
-  typename Prod::Raw1 raw[kSpSampleEach];
-  uint32_t valid = 0u;
-#pragma unroll
-  for (int e = 0; e < kSpSampleEach; ++e) {  // every load first, then the classes and keys
-    const int32_t j = int32_t(threadIdx.x) + kSpThreads * e;
-    pos[e] = 0;
-    if (j < S) {
-      // stratum j: [floor(j n / S), floor((j + 1) n / S)), S = 2048 or n
-      const int32_t a = S == n ? j : int32_t((int64_t(j) * n) >> 11);
-      const int32_t b = S == n ? j + 1 : int32_t((int64_t(j + 1) * n) >> 11);
-      pos[e] = a + int32_t(__umulhi(sp_hash(uint32_t(j) ^ salt), uint32_t(b - a)));
-      valid |= 1u << e;
-    }
-    p.load1(pos[e], raw[e]);
-  }
   int cls[kSpSampleEach];
 #pragma unroll
   for (int e = 0; e < kSpSampleEach; ++e) cls[e] = kText;
@@ -370,6 +489,8 @@ __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<
       if (f[e] >= 0 && c.s0 + pos[e] < fr.end(f[e])) cls[e] = f[e] == fr.nf - 1 ? kCurrent : kHist;
   }
 #pragma unroll
+  for (int e = 0; e < kSpSampleEach; ++e) p.load1_rest(pos[e], cls[e], raw[e]);
+#pragma unroll
   for (int e = 0; e < kSpSampleEach; ++e) key[e] = ((valid >> e) & 1u) ? p.key1(raw[e], cls[e]) : kSelNever;
   // the sample keys of ranks qlo and qhi (1-based), exactly: three radix levels
   const double pr = double(k) / double(n);
@@ -378,28 +499,28 @@ __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<
   int32_t rlo = rt - delta, rhi = rt + delta;
   const bool has_lo = rlo >= 1, has_hi = rhi <= S;
   uint32_t plo = 0u, phi = 0u;  // the two keys' prefixes so far
+  for (int b = threadIdx.x; b < 2 * 2048; b += kSpThreads) (&sh.hist[0][0][0])[b] = 0u;
+  __syncthreads();
 #pragma unroll 1
   for (int level = 0; level < 3; ++level) {
     const int shift = level == 0 ? 21 : level == 1 ? 10 : 0;
     const uint32_t mask = level == 2 ? 1023u : 2047u;
     const int pshift = level == 1 ? 21 : 10;
-    for (int b = threadIdx.x; b < 2048; b += kSpThreads) {
-      sh.hlo[b] = 0u;
-      sh.hhi[b] = 0u;
-    }
-    __syncthreads();
+    uint32_t* hlo = sh.hist[level & 1][0];
+    uint32_t* hhi = sh.hist[level & 1][1];
     // level 0 counts every key once (both ranks pivot on it); levels 1 and 2
     // the keys matching each rank's prefix
 #pragma unroll
     for (int e = 0; e < kSpSampleEach; ++e) {
       if (!((valid >> e) & 1u)) continue;
       const uint32_t d = (key[e] >> shift) & mask;
-      if (level == 0 || (has_lo && (key[e] >> pshift) == (plo >> pshift))) atomicAdd(&sh.hlo[d], 1u);
-      if (level > 0 && has_hi && (key[e] >> pshift) == (phi >> pshift)) atomicAdd(&sh.hhi[d], 1u);
+      if (level == 0 || (has_lo && (key[e] >> pshift) == (plo >> pshift))) atomicAdd(&hlo[d], 1u);
+      if (level > 0 && has_hi && (key[e] >> pshift) == (phi >> pshift)) atomicAdd(&hhi[d], 1u);
     }
+    // the other set, read by the previous level's pivots, is cleared for the next level
+    for (int b = threadIdx.x; b < 2 * 2048; b += kSpThreads) (&sh.hist[(level + 1) & 1][0][0])[b] = 0u;
     __syncthreads();
-    if (has_lo) sp_pivot(sh.hlo, rlo, sh.wtot, sh.piv + 0);
-    if (has_hi) sp_pivot(level == 0 ? sh.hlo : sh.hhi, rhi, sh.wtot, sh.piv + 2);
+    sp_pivot2(hlo, has_lo ? rlo : 0, level == 0 ? hlo : hhi, has_hi ? rhi : 0, sh.wtot, sh.piv);
     if (has_lo) {
       plo |= uint32_t(sh.piv[0]) << shift;
       rlo = sh.piv[1];
@@ -408,7 +529,6 @@ __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<
       phi |= uint32_t(sh.piv[2]) << shift;
       rhi = sh.piv[3];
     }
-    __syncthreads();  // every thread has read the pivots
   }
   if (threadIdx.x == 0) {
     st[kSpLo] = int32_t(has_lo ? min(plo, kSelKeyMax) : 0u);
@@ -519,28 +639,45 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
       if (j0 + i < nt && !(((g.uni >> i) & 1u) && !p.selectable(int((g.ucls >> (2 * i)) & 3u))))
         p.load((tw + kSpPassWaves * (j0 + i)) * kSpTile, raw[i]);
   };
+  // a direct output's totals (keys <= lo: a per-lane count in the fast path
+  // and a wave count elsewhere; ties at lo and at hi)
+  uint32_t le_lane = 0u;
+  int32_t le_w = 0, eqlo_w = 0, eqhi_w = 0;
+  // cnt: keys <= lo, == lo, strictly between, == hi.  A ranked list records
+  // every tile; a direct output the tiles with ties (its totals go to the
+  // state words) and, in kModeAll, the tiles' largest keys.
   auto finish_tile = [&](int32_t t, int32_t base, uint32_t packed, const int32_t (&cnt)[4], uint32_t kmax) {
     if (Prod::kDirect) put(base, packed);
     else __builtin_amdgcn_raw_buffer_store_b32(packed, codes, base + 4 * lane, 0, 0);
-    if (lane == 0) {
-      int4* rec = reinterpret_cast<int4*>(tiles + size_t(t) * kTileWords);
-      rec[0] = make_int4(cnt[0], cnt[1], cnt[2], cnt[3]);
-      rec[1] = make_int4(0, 0, int32_t(kmax), 0);
+    if (Prod::kDirect) {
+      le_w += cnt[0];
+      eqlo_w += cnt[1];
+      eqhi_w += cnt[3];
+    }
+    if (!Prod::kDirect || cnt[1] + cnt[3] > 0 || mode == kModeAll) {
+      if (lane == 0) {
+        int4* rec = reinterpret_cast<int4*>(tiles + size_t(t) * kTileWords);
+        rec[0] = make_int4(Prod::kDirect ? 0 : cnt[0] - cnt[1], cnt[1], cnt[2], cnt[3]);
+        rec[1] = make_int4(0, 0, int32_t(kmax), 0);
+      }
     }
   };
-  // counts of the four codes and the candidates of one row from its tests
+  // counts and candidates of one row from its tests: cnt[0] gathers the keys
+  // at or below lo (the tile's count below lo is cnt[0] - cnt[1] once the
+  // tile is done); ties at lo or hi are rare, so their masks are tested first
   auto tally = [&](int e, int32_t base, uint32_t key, bool ge_lo, bool gt_lo, bool ge_hi, bool gt_hi,
                    int32_t (&cnt)[4]) {
     const uint64_t mge_lo = __ballot(ge_lo), mgt_lo = __ballot(gt_lo), mge_hi = __ballot(ge_hi),
                    mgt_hi = __ballot(gt_hi);
-    cnt[0] += __popcll(~mge_lo);
-    cnt[1] += __popcll(mge_lo & ~mgt_lo);
-    cnt[2] += __popcll(mgt_lo & ~mge_hi);
-    cnt[3] += __popcll(mge_hi & ~mgt_hi);
-    const uint64_t mid = mgt_lo & ~mge_hi;
+    cnt[0] += __popcll(~mgt_lo);
+    const uint64_t eq_lo = mge_lo & ~mgt_lo, eq_hi = mge_hi & ~mgt_hi, mid = mgt_lo & ~mge_hi;
+    if (eq_lo) cnt[1] += __popcll(eq_lo);
+    if (eq_hi) cnt[3] += __popcll(eq_hi);
     if (mid) {
+      const int32_t nm = __popcll(mid);
+      cnt[2] += nm;
       if (gt_lo && !ge_hi) stage[staged + __popcll(mid & below)] = make_uint2(key, uint32_t(base + 64 * e + lane));
-      staged += __popcll(mid);
+      staged += nm;
     }
   };
   auto process = [&](const typename Prod::Raw (&raw)[G], int32_t j0, const GroupCls& g) {
@@ -560,14 +697,43 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
         }
         uint32_t key[4];
         p.keys_uniform(base, ucls, raw[i], key);
+        // every key is selectable here: each test's compare feeds its ballot
+        // and the lane's code directly; ties are rare, so their masks are only
+        // counted when some row has one
+        const int32_t staged0 = staged;
+        int32_t gt = 0;  // keys above lo (ranked lists)
+        uint64_t eql[4], eqh[4], eq_any = 0u;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool ge_lo = key[e] >= lo, gt_lo = key[e] > lo, ge_hi = key[e] >= hi, gt_hi = key[e] > hi;
-          const uint32_t code =
-              Prod::kDirect ? (gt_lo ? 0u : 1u) : uint32_t(ge_lo) + uint32_t(gt_lo) + uint32_t(ge_hi) + uint32_t(gt_hi);
+          const uint32_t k = key[e];
+          const uint64_t mgt_lo = __ballot(k > lo), mlt_hi = __ballot(k < hi);
+          eql[e] = __ballot(k == lo);
+          eqh[e] = __ballot(k == hi);
+          eq_any |= eql[e] | eqh[e];
+          uint32_t code;
+          if (Prod::kDirect) {
+            code = k > lo ? 0u : 1u;
+            le_lane += code;
+          } else {
+            code = (k >= lo ? 1u : 0u) + (k > lo ? 1u : 0u) + (k >= hi ? 1u : 0u) + (k > hi ? 1u : 0u);
+            gt += __popcll(mgt_lo);
+          }
           packed |= code << (8 * e);
-          tally(e, base, key[e], ge_lo, gt_lo, ge_hi, gt_hi, cnt);
+          const uint64_t mid = mgt_lo & mlt_hi;
+          const uint32_t rank =
+              __builtin_amdgcn_mbcnt_hi(uint32_t(mid >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(mid), 0u));
+          if (k > lo && k < hi) stage[staged + int32_t(rank)] = make_uint2(k, uint32_t(base + 64 * e + lane));
+          staged += __popcll(mid);
         }
+        if (eq_any) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            cnt[1] += __popcll(eql[e]);
+            cnt[3] += __popcll(eqh[e]);
+          }
+        }
+        cnt[0] = Prod::kDirect ? 0 : kSpTile - gt;  // direct: these keys are counted in le_lane
+        cnt[2] = staged - staged0;
         finish_tile(t, base, packed, cnt, 0u);
         continue;
       }
@@ -609,6 +775,14 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
     process(rb, j + G, gb);
   }
   if (staged) flush();
+  if (Prod::kDirect) {  // the wave's totals
+    const int32_t le = __builtin_amdgcn_readlane(sp_wave_inscan(int32_t(le_lane)), 63) + le_w;
+    if (lane == 0) {
+      if (le) atomicAdd(&st[kSpLe], le);
+      if (eqlo_w) atomicAdd(&st[kSpEqLo], eqlo_w);
+      if (eqhi_w) atomicAdd(&st[kSpEqHi], eqhi_w);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -616,12 +790,17 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
 // seqs, units), kSpThreads threads)
 // ---------------------------------------------------------------------------
 
+constexpr int kSpCandBits = 13;  // radix bits per level of the candidate selection
+constexpr int kSpCandBins = 1 << kSpCandBits;
+constexpr int kSpTieList = 256;  // tied candidates ordered by a direct rank count
+
 struct SpResolveShared {
   uint32_t hist[2048];
+  uint32_t hist2[2][kSpCandBins];  // alternate levels of the candidate selection
   int32_t tcount[kSpLdsTiles];  // taken candidates per tile (segments of at most kSpLdsTiles tiles)
   int32_t wtot[kSpWaves];
   int32_t weq[kSpWaves];
-  int32_t piv[2];
+  int32_t piv[3];
   int32_t sum[4];
   int32_t found[2];
   int32_t cut;
@@ -631,10 +810,11 @@ struct SpResolveShared {
 // entries held in v (kSpPerThread per thread, batch i0 of the list), reloaded
 // per batch by reload(i0) when the list has more than one batch.  Every
 // counted key lies in [lo_b, hi_b]: they share the bits above the highest bit
-// where lo_b and hi_b differ, and radix levels of up to 11 bits cover the
-// bits below it (so the first level already spreads the keys over its bins).
-// kSelNever is not counted.  Returns T; *need gets its rank among the keys
-// equal to T, *eq how many there are.
+// where lo_b and hi_b differ, and radix levels of up to kSpCandBits bits cover
+// the bits below it (so the first level already spreads the keys over its
+// bins, and two levels cover 26 varying bits).  kSelNever is not counted.
+// Returns T; *need gets its rank among the keys equal to T, *eq how many there
+// are.
 template <class KeyOf, class Reload>
 __device__ uint32_t sp_cand_select(const KeyOf& kf, const Reload& reload, const uint2 (&v)[kSpPerThread],
                                    int32_t count, bool one, int32_t r, uint32_t lo_b, uint32_t hi_b,
@@ -644,32 +824,99 @@ __device__ uint32_t sp_cand_select(const KeyOf& kf, const Reload& reload, const 
   uint32_t prefix = top >= 32 ? 0u : lo_b & ~((1u << top) - 1u);
   int32_t rem = r;
   *eq = count;
+  int32_t bins = top > 0 ? 1 << min(top, kSpCandBits) : 0;
+  for (int b = threadIdx.x; b < bins; b += kSpThreads) sh.hist2[0][b] = 0u;
+  __syncthreads();
+  int cur = 0;
+#pragma unroll 1
+  while (top > 0) {
+    const int shift = max(top - kSpCandBits, 0);
+    const uint32_t mask = (1u << (top - shift)) - 1u;
+    uint32_t* h = sh.hist2[cur];
+    for (int32_t i0 = 0; i0 < count; i0 += kSpBatch) {
+      if (!one) reload(i0);
+#pragma unroll
+      for (int e = 0; e < kSpPerThread; ++e) {
+        const uint32_t key = kf(v[e]);
+        if (key != kSelNever && (top >= 32 || (key >> top) == (prefix >> top))) atomicAdd(&h[(key >> shift) & mask], 1u);
+      }
+    }
+    // the other set, read by the previous level's pivot, is cleared for the next level
+    const int32_t next = shift > 0 ? 1 << min(shift, kSpCandBits) : 0;
+    for (int b = threadIdx.x; b < next; b += kSpThreads) sh.hist2[cur ^ 1][b] = 0u;
+    __syncthreads();
+    sp_pivot_wide(h, int32_t(mask) + 1, rem, sh.wtot, sh.piv);
+    prefix |= uint32_t(sh.piv[0]) << shift;
+    rem = sh.piv[1];
+    if (shift == 0) *eq = sh.piv[2];
+    top = shift;
+    cur ^= 1;
+  }
+  __syncthreads();  // every thread has read the last pivot before sh.piv is reused
+  *need = rem;
+  return prefix;
+}
+
+// Index of the need-th (1-based) candidate, in index order, among the eq
+// candidates whose key is T (eq <= kSpTieMax; the indices lie in [0, n)).
+// They are gathered in LDS; up to kSpTieList of them rank themselves by a
+// direct count, more are selected by radix levels over the gathered indices.
+constexpr int kSpTieMax = 2 * kSpCandBins;
+
+template <class Reload>
+__device__ int32_t sp_tie_cut(const Reload& reload, const uint2 (&v)[kSpPerThread], int32_t count, bool one,
+                              uint32_t T, int32_t need, int32_t eq, int32_t n, SpResolveShared& sh) {
+  uint32_t* list = sh.hist2[0];  // both sets: kSpTieMax entries
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x == 0) sh.found[0] = 0;
+  __syncthreads();
+  for (int32_t i0 = 0; i0 < count; i0 += kSpBatch) {
+    if (!one) reload(i0);
+#pragma unroll
+    for (int e = 0; e < kSpPerThread; ++e) {
+      const uint64_t m = __ballot(v[e].x == T);
+      if (m) {  // the wave's tied entries appended at once
+        int32_t b = 0;
+        if (lane == 0) b = atomicAdd(&sh.found[0], __popcll(m));
+        b = __builtin_amdgcn_readfirstlane(b);
+        const uint32_t rank =
+            __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+        if (v[e].x == T) list[b + int32_t(rank)] = v[e].y;
+      }
+    }
+  }
+  __syncthreads();
+  const int32_t m = sh.found[0];  // == eq
+  if (m <= kSpTieList) {
+    if (int32_t(threadIdx.x) < m) {
+      const uint32_t mine = list[threadIdx.x];
+      int32_t rank = 1;
+      for (int32_t j = 0; j < m; ++j) rank += list[j] < mine ? 1 : 0;
+      if (rank == need) sh.cut = int32_t(mine);
+    }
+    __syncthreads();
+    return sh.cut;
+  }
+  int top = n > 1 ? 32 - __clz(n - 1) : 1;  // index bits [0, top) vary
+  uint32_t prefix = 0u;
+  int32_t rem = need;
 #pragma unroll 1
   while (top > 0) {
     const int shift = max(top - 11, 0);
     const uint32_t mask = (1u << (top - shift)) - 1u;
     for (int b = threadIdx.x; b < 2048; b += kSpThreads) sh.hist[b] = 0u;
     __syncthreads();
-    for (int32_t i0 = 0; i0 < count; i0 += kSpBatch) {
-      if (!one) reload(i0);
-#pragma unroll
-      for (int e = 0; e < kSpPerThread; ++e) {
-        const uint32_t key = kf(v[e]);
-        if (key != kSelNever && (top >= 32 || (key >> top) == (prefix >> top)))
-          atomicAdd(&sh.hist[(key >> shift) & mask], 1u);
-      }
+    for (int32_t j = threadIdx.x; j < m; j += kSpThreads) {
+      const uint32_t x = list[j];
+      if ((x >> top) == (prefix >> top)) atomicAdd(&sh.hist[(x >> shift) & mask], 1u);
     }
     __syncthreads();
     sp_pivot(sh.hist, rem, sh.wtot, sh.piv);
-    const int32_t bin = sh.piv[0];
+    prefix |= uint32_t(sh.piv[0]) << shift;
     rem = sh.piv[1];
-    prefix |= uint32_t(bin) << shift;
-    if (shift == 0) *eq = int32_t(sh.hist[bin]);
-    __syncthreads();  // every thread has read the pivot and the bin count
     top = shift;
   }
-  *need = rem;
-  return prefix;
+  return int32_t(prefix);
 }
 
 // Exact selection by streaming the segment's own inputs (the splitters missed
@@ -811,24 +1058,36 @@ __device__ uint32_t split_resolve(const Prod& pe, SpResolveShared& sh, const Sel
   };
   const bool one = nlist <= kSpBatch;
   reload(0);
-  // totals of the four codes
-  int32_t a[4] = {0, 0, 0, 0};
-  for (int32_t t = threadIdx.x; t < ntile; t += kSpThreads) {
-    const int4 x = *reinterpret_cast<const int4*>(tiles + size_t(t) * kTileWords);
-    a[0] += x.x;
-    a[1] += x.y;
-    a[2] += x.z;
-    a[3] += x.w;
-  }
-  if (threadIdx.x < 4) sh.sum[threadIdx.x] = 0;
-  __syncthreads();
+  // totals of the four codes: a direct output's from the state words, a
+  // ranked list's from its tile records
+  int32_t N0, N1, N2, N3;
+  if (Prod::kDirect) {
+    N1 = st[kSpEqLo];
+    N0 = st[kSpLe] - N1;
+    N2 = count;
+    N3 = st[kSpEqHi];
+  } else {
+    int32_t a[4] = {0, 0, 0, 0};
+    for (int32_t t = threadIdx.x; t < ntile; t += kSpThreads) {
+      const int4 x = *reinterpret_cast<const int4*>(tiles + size_t(t) * kTileWords);
+      a[0] += x.x;
+      a[1] += x.y;
+      a[2] += x.z;
+      a[3] += x.w;
+    }
+    if (threadIdx.x < 4) sh.sum[threadIdx.x] = 0;
+    __syncthreads();
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int32_t w = wave_sum(a[q]);
-    if (lane == 0 && w) atomicAdd(&sh.sum[q], w);
+    for (int q = 0; q < 4; ++q) {
+      const int32_t w = wave_sum(a[q]);
+      if (lane == 0 && w) atomicAdd(&sh.sum[q], w);
+    }
+    __syncthreads();
+    N0 = sh.sum[0];
+    N1 = sh.sum[1];
+    N2 = sh.sum[2];
+    N3 = sh.sum[3];
   }
-  __syncthreads();
-  const int32_t N0 = sh.sum[0], N1 = sh.sum[1], N2 = sh.sum[2], N3 = sh.sum[3];
   if (s.split_exact || k <= N0) mode = kModeExact;
   else if (k <= N0 + N1) mode = kModeTieLo;
   else if (k <= N0 + N1 + N2) mode = count <= cap ? kModeMid : kModeExact;
@@ -837,17 +1096,18 @@ __device__ uint32_t split_resolve(const Prod& pe, SpResolveShared& sh, const Sel
 
   uint32_t T = 0u;
   int32_t need = 0, cut = c.n, tstar = -1, tie_before = 0;
-  if (mode == kModeExact) {
-    T = split_exact(pe, sh, lay, c, k, tiles, codes);
-  } else if (mode == kModeMid) {
+  if (mode == kModeMid) {
     int32_t m_eq = 0;
     T = sp_cand_select([](const uint2& x) { return x.x; }, reload, v, count, one, k - N0 - N1, lo + 1u, hi - 1u, sh,
                        &need, &m_eq);
     if (need < m_eq) {  // not every candidate equal to T is taken: cut at the need-th one in index order
-      int32_t r2, e2;
-      cut = int32_t(sp_cand_select([T](const uint2& x) { return x.x == T ? x.y : kSelNever; }, reload, v, count, one,
-                                   need, 0u, uint32_t(c.n - 1), sh, &r2, &e2));
+      if (m_eq <= kSpTieMax) cut = sp_tie_cut(reload, v, count, one, T, need, m_eq, c.n, sh);
+      else mode = kModeExact;  // (streamed below)
     }
+  }
+  if (mode == kModeExact) {
+    T = split_exact(pe, sh, lay, c, k, tiles, codes);
+  } else if (mode == kModeMid) {
     if (OFFSETS && lds_tiles) {
       for (int32_t t = threadIdx.x; t < ntile; t += kSpThreads) sh.tcount[t] = 0;
       __syncthreads();

@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kSelThreads) void select_emit_kernel(SelectArgs a) 
 
 // The top-B of one segment held by one work-group (segsel_resident.h).
 struct SelectRes {
-  static constexpr int kGroup = 2;        // tiles a classifying wave loads at once (segsel_split.h)
+  static constexpr int kGroup = 1;        // tiles a classifying wave loads at once (segsel_split.h)
   static constexpr bool kDirect = false;  // a ranked list: the splitter path emits it from codes
   static constexpr bool aligned = false;
   __amdgpu_buffer_rsrc_t a_base;  // the segment's A, Phi and gate (out-of-range lanes read 0)
@@ -192,10 +192,19 @@ struct SelectRes {
     uint32_t g;
   };
 
+  // The gate byte first; A and Phi only where S depends on them (a text
+  // token, or a visual one whose gate is not zero).
   __device__ void load1(int32_t i, Raw1& r) const {
-    r.A = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
-    r.ph = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
     r.g = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+  }
+
+  __device__ void load1_rest(int32_t i, int cls, Raw1& r) const {
+    r.A = 0.0f;
+    r.ph = 0.0f;
+    if (cls == kText || r.g != 0u) {
+      r.A = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
+      if (has_phi) r.ph = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0));
+    }
   }
 
   __device__ uint32_t key1(const Raw1& r, int cls) const {
@@ -264,9 +273,12 @@ __global__ __launch_bounds__(kSpThreads) void select_split_sample_kernel(SelectA
   __shared__ SpSampleShared sh;
   SelCtx c = sel_ctx(a.lay);
   c.k = a.lay.cu_budget[c.seq + 1] - a.lay.cu_budget[c.seq];
+  const SelectRes p = select_res(a, c, blockIdx.z, false);
+  SpGather<SelectRes> g;
+  sp_gather(p, a.lay, c, g);  // the sample's loads first: the frame table's overlap them
   const SeqFrames<LDS> fr = sp_frames<LDS>(sh.fstart, sh.fend, a.lay, c.seq);
   __syncthreads();
-  split_sample(select_res(a, c, blockIdx.z, false), sh, fr, a.sel, a.lay, c, c.n);
+  split_sample(p, sh, fr, a.sel, a.lay, c, c.n, g);
 }
 
 __global__ __launch_bounds__(kSpPassThreads) void select_split_classify_kernel(SelectArgs a) {

@@ -188,13 +188,14 @@ STAGE_CASES = [("short", None), ("long", None), ("long", "four_pass"), ("long", 
 
 
 @pytest.mark.parametrize("layout,path", STAGE_CASES)
-@pytest.mark.parametrize("values", ["few", "many"])
+@pytest.mark.parametrize("values", ["few", "many", "spread"])
 def test_stage_exact_many_parts_and_ties(torch_cuda, monkeypatch, layout, path, values):
     """Stage-isolated on long sequences, with inputs drawn from a few values
     (long runs of equal keys straddling wave, tile and part boundaries; the
-    splitters land on tied keys) or from a few hundred (the k-th key among the
-    splitter candidates, with ties there): gate, tau, S and kept lists must
-    equal the oracle's exactly, on every selection path."""
+    splitters land on tied keys), from a few hundred (the k-th key among the
+    splitter candidates, with hundreds of ties there) or from a few thousand
+    (tens of ties at the k-th key): gate, tau, S and kept lists must equal the
+    oracle's exactly, on every selection path."""
     import torch
     from oracle import stlite_oracle as O
     from paper_2603_00188_amd import stlite as S
@@ -222,6 +223,10 @@ def test_stage_exact_many_parts_and_ties(torch_cuda, monkeypatch, layout, path, 
             rho = rng.choice(np.float32([0.1, 0.25, 0.5, 0.75, 1.0]), size=(U, L)).astype(np.float32)
             A = rng.choice(np.float32([1e-4, 2e-4, 5e-4]), size=(U, L)).astype(np.float32)
             phi = rng.choice(np.float32([0.9, 1.0, 1.1]), size=(U, L)).astype(np.float32)
+        elif values == "spread":
+            rho = rng.choice(np.linspace(0.2, 0.4, 2000, dtype=np.float32), size=(U, L)).astype(np.float32)
+            A = rng.choice(np.linspace(1e-4, 5e-4, 1500, dtype=np.float32), size=(U, L)).astype(np.float32)
+            phi = rng.choice(np.linspace(0.9, 1.1, 1700, dtype=np.float32), size=(U, L)).astype(np.float32)
         else:
             rho = rng.choice(np.linspace(0.2, 0.4, 300, dtype=np.float32), size=(U, L)).astype(np.float32)
             A = rng.choice(np.linspace(1e-4, 5e-4, 200, dtype=np.float32), size=(U, L)).astype(np.float32)
