@@ -598,11 +598,19 @@ def main():
     model = work_model(w, lay, cu_budget)
     stages = {n: roofline_entry(model[n], per_call[n]) for n in names}
     dom = max(names, key=lambda n: per_call[n])
+    # Selections: one resident launch when every sequence has at most 32,768
+    # tokens (and 1,024 frames), the splitter launches otherwise.
+    seqlens = np.diff(np.asarray(lay.cu_seqlens))
+    frames = np.diff(np.asarray(lay.cu_frames))
+    resident = int(seqlens.max()) <= 32768 and int(frames.max(initial=0)) <= 1024
     kernel_of = {"score_window": "score_pass_kernel<1> + score_pass_kernel<2>",
                  "tsg_rho": "rho_kernel",
-                 "tsg_threshold": "gate_produce_kernel + sel_level1_kernel + sel_level2_kernel + gate_emit_kernel",
+                 "tsg_threshold": "gate_resident_kernel" if resident else
+                                  "gate_split_sample_kernel + gate_split_classify_kernel + gate_split_resolve_kernel",
                  "css_saliency": "css_kernel<true>",
-                 "select_topk": "select_produce_kernel + sel_level1_kernel + sel_level2_kernel + select_emit_kernel",
+                 "select_topk": "select_resident_kernel" if resident else
+                                "select_split_sample_kernel + select_split_classify_kernel + "
+                                "select_split_resolve_kernel + select_split_emit_kernel",
                  "compact_kv": "compact_kernel"}
     roof = dict(stages[dom])
     roof.pop("ms")
