@@ -29,12 +29,15 @@ namespace {
 constexpr float kNegBig = -1.0e30f;
 constexpr float kScale2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
-// Minimum work-groups per CU in the launch bound (what the register allocator
-// budgets for): ceil(8 / NW), about two waves per SIMD, for groups of three or
-// more waves; one for the one- and two-wave groups of the smallest windows,
-// whose resident queries need more registers than a higher target leaves.
+// Second launch-bound argument: the minimum number of waves per SIMD the
+// register allocator budgets for (HIP's meaning of it).  Two (256 registers
+// each) for groups of three or more waves: their resident queries fill the
+// register file at two waves per SIMD, and an 8-wave group needs two waves on
+// every SIMD at once.  One for the one- and two-wave groups of the smallest
+// windows, whose resident queries need more registers than a higher target
+// leaves.
 template <int NW>
-constexpr int kScoreMinGroups = NW <= 2 ? 1 : (8 + NW - 1) / NW;
+constexpr int kScoreMinGroups = NW <= 2 ? 1 : 2;
 
 struct ChunkPos {
   int32_t seq, seq_start, seq_len, c0, c1, gchunk;
@@ -63,13 +66,36 @@ __device__ inline ChunkPos locate_chunk(const Layout& lay, int32_t chunk, int32_
 
 __device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// 32-row blocks are dealt to waves round-robin: wave w owns blocks w, w + NW.
-template <int NW>
-__device__ inline int block_of(int j) { return wave_id() + j * NW; }
+// Row-block layouts of the score passes (a unit is one 32-row block against
+// one 32-key block of a tile: eight MFMAs and 16 logits per lane).
+//   kPlain:    wave w owns blocks w + j NW (j < RB), both key blocks.
+//   kBalanced: 14 blocks on 8 waves.  Waves w and w + 4 of an 8-wave group
+//              run on the same SIMD, and the passes are bound by each SIMD's
+//              vector work, so a tile's 28 units are spread 7 per SIMD (the
+//              plain layouts leave 8 on some SIMDs: 7 waves put 8, 8, 8 and 4
+//              there): waves 0-3 own blocks 2w and 2w + 1 (4 units), waves 4-7
+//              own block w + 4 (2 units) and one key block, w & 1, of block
+//              10 + w / 2, i.e. 12 or 13 (1 unit).  The two waves sharing a
+//              block add their row sums (pass 1) and each give the column
+//              sums of their own key block (pass 2).
+constexpr int kPlain = 0, kBalanced = 1;
+
+template <int NW, int MODE = kPlain>
+__device__ inline int block_of(int j) {
+  const int w = wave_id();
+  if constexpr (MODE == kBalanced) return w < 4 ? 2 * w + j : (j == 0 ? w + 4 : 10 + (w >> 1));
+  else return w + j * NW;
+}
+
+// Units a wave of kind KIND owns: kind 0 every (row block, key block); kinds
+// 1 and 2 (balanced waves 4-7 with w & 1 = KIND - 1) only key block KIND - 1
+// of their second block.
+template <int KIND>
+constexpr bool owns(int rb, int kb) { return KIND == 0 || rb == 0 || kb == KIND - 1; }
 
 // Window queries as the A operand: lane l holds row l & 31 of each block;
 // k-step kk takes dims 16 kk + 8 (l >> 5) .. +7.
-template <int RB, int NW>
+template <int RB, int NW, int MODE = kPlain>
 __device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int unit, bf16x8_t (&qa)[RB][8]) {
   const int lane = threadIdx.x & 63;
   const int layer = unit / a.lay.n_kv_heads, kv = unit % a.lay.n_kv_heads;
@@ -77,7 +103,7 @@ __device__ inline void load_queries(const ScoreArgs& a, const ChunkPos& cp, int 
       a.q + ((size_t(layer) * a.lay.n_seqs + cp.seq) * a.n_q_heads + size_t(kv) * a.group) * a.window * kHeadDim;
 #pragma unroll
   for (int b = 0; b < RB; ++b) {
-    const int row = block_of<NW>(b) * 32 + (lane & 31);
+    const int row = block_of<NW, MODE>(b) * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -97,11 +123,11 @@ __device__ inline void fill_row_limits(const ScoreArgs& a, const ChunkPos& cp, i
 
 // Accumulator start of a masked tile: -inf where the row may not see the key
 // (past its causal limit or past the chunk), 0 elsewhere.
-template <int NW>
+template <int NW, int MODE = kPlain>
 __device__ inline f32x16_t mask_init(int32_t t0, int kb, int rb, const int32_t* lim_s) {
   const int lane = threadIdx.x & 63;
   const int32_t key = t0 + kb * 32 + (lane & 31);
-  const int base = block_of<NW>(rb) * 32;
+  const int base = block_of<NW, MODE>(rb) * 32;
   f32x16_t m;
 #pragma unroll
   for (int i = 0; i < 16; ++i) m[i] = key > lim_s[base + acc32_row(i, lane)] ? -INFINITY : 0.0f;
@@ -140,27 +166,35 @@ __device__ inline int scatter_reg(int lane) {
   return 8 * ((lane >> 4) & 1) + 4 * ((lane >> 3) & 1) + 2 * ((lane >> 2) & 1) + ((lane >> 1) & 1);
 }
 
+// Shared memory of a score-pass work-group.
+template <int RB, int NW>
+struct ScoreShared {
+  uint16_t ks0[kTileElems] __attribute__((aligned(16)));
+  uint16_t ks1[kTileElems] __attribute__((aligned(16)));
+  uint16_t ks2[kTileElems] __attribute__((aligned(16)));
+  int32_t lim_s[NW * RB * 32];
+  float red_s[2][NW][kTileKeys];
+  float xch[2][32];  // balanced pass 1: the second sharing wave's row sums of blocks 12 and 13
+  int32_t risky;
+};
+
 // One pass over a chunk of keys.  PASS 1 writes per-row (offset, sum) for the
 // chunk (and flags the chunk if a sum overflowed); PASS 2 writes A for the
-// chunk's keys.
-template <int PASS, int RB, int NW>
-__global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t ks0[kTileElems], ks1[kTileElems], ks2[kTileElems];
-  __shared__ int32_t lim_s[NW * RB * 32];
-  __shared__ float red_s[2][NW][kTileKeys];
-  __shared__ int32_t risky;
-  const int unit = blockIdx.y;
-  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
-  if (cp.seq < 0) return;
+// chunk's keys.  KIND: which units of its blocks the wave owns (owns<KIND>).
+template <int PASS, int RB, int NW, int MODE, int KIND>
+__device__ __forceinline__ void score_pass_body(const ScoreArgs& a, ScoreShared<RB, NW>& sh, const ChunkPos& cp,
+                                                int unit) {
+  uint16_t* const ks0 = sh.ks0;
+  uint16_t* const ks1 = sh.ks1;
+  uint16_t* const ks2 = sh.ks2;
+  int32_t* const lim_s = sh.lim_s;
   const int lane = threadIdx.x & 63;
   const int wave = wave_id();
-  if (PASS == 1 && threadIdx.x == 0) risky = 0;
-  fill_row_limits(a, cp, lim_s);
-  // The wave's last block may lie past the real rows (uniform).
-  const bool last_real = block_of<NW>(RB - 1) < a.blocks;
+  // The wave's last block may lie past the real rows (uniform; plain layout).
+  const bool last_real = block_of<NW, MODE>(RB - 1) < a.blocks;
 
   bf16x8_t qa[RB][8];
-  load_queries<RB, NW>(a, cp, unit, qa);
+  load_queries<RB, NW, MODE>(a, cp, unit, qa);
   // Pass 1: offsets o of the row groups g = i >> 2 (rows 8 g .. 8 g + 7 of a
   // block); pass 2: row log-normalisers lse.  Both in log2 units.
   float ofs[RB][4];
@@ -170,7 +204,7 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) lse[rb][i] = lrow[block_of<NW>(rb) * 32 + acc32_row(i, lane)];
+      for (int i = 0; i < 16; ++i) lse[rb][i] = lrow[block_of<NW, MODE>(rb) * 32 + acc32_row(i, lane)];
   }
 
   const uint16_t* kseq = a.k + (size_t(unit) * a.lay.total_tokens + cp.seq_start) * kHeadDim;
@@ -203,7 +237,9 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
     // Offsets: each row group's maximum over the first tile (masked keys
     // excluded; a group that sees none of them sees none of the chunk and
     // gets kNegBig).  A row far below its group's offset can underflow its
-    // sum; the chunk is then flagged for the exact pass.
+    // sum; the chunk is then flagged for the exact pass.  Every unit of the
+    // wave's blocks is formed here, owned or not, so that the two waves
+    // sharing a block take the same offsets.
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -212,8 +248,8 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
           acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              qa[rb][kk], kbuf[(8 * kb + kk) % 4], kk == 0 ? mask_init<NW>(cp.c0, kb, rb, lim_s) : acc[kb][rb], 0, 0,
-              0);
+              qa[rb][kk], kbuf[(8 * kb + kk) % 4],
+              kk == 0 ? mask_init<NW, MODE>(cp.c0, kb, rb, lim_s) : acc[kb][rb], 0, 0, 0);
       }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
@@ -261,22 +297,23 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
   auto put_cols = [&](int32_t n, int kb) {
     float c = col[0] + col[1];
     c += __shfl_xor(c, 32);
-    if (lane < 32) red_s[n & 1][wave][kb * 32 + lane] = c;
+    if (lane < 32) sh.red_s[n & 1][wave][kb * 32 + lane] = c;
   };
   // Pass 2: A of tile n's keys, once every wave's column sums are in LDS.
   auto reduce = [&](int32_t n) {
     if (threadIdx.x < kTileKeys) {
       float s = 0.0f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) s += red_s[n & 1][w][threadIdx.x];
+      for (int w = 0; w < NW; ++w) s += sh.red_s[n & 1][w][threadIdx.x];
       const int32_t j = cp.c0 + n * kTileKeys + threadIdx.x;
       if (j < cp.c1) aout[j] = s * inv_g;
     }
   };
   // Section kb of a clean tile: the MFMAs of key block kb, each MFMA followed
   // by the vector work on two elements of key block kb ^ 1 (i and i + 1 of
-  // the same row group, i even), in that order.
-  // B fragments past the tile's sixteen are the next tile's first three.
+  // the same row group, i even), in that order; units the wave does not own
+  // are left out.  B fragments past the tile's sixteen are the next tile's
+  // first three.
   auto section = [&](int kb, const uint16_t* tile, const uint16_t* next) {
     col[0] = 0.0f;
     col[1] = 0.0f;
@@ -289,9 +326,10 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
         read_b(next, g + 3 - 16);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[rb][kk], kbuf[g % 4],
-                                                              kk == 0 ? f32x16_t{} : acc[kb][rb], 0, 0, 0);
-        elem_pinned(kb ^ 1, rb, 2 * kk);
+        if (owns<KIND>(rb, kb))
+          acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[rb][kk], kbuf[g % 4],
+                                                                kk == 0 ? f32x16_t{} : acc[kb][rb], 0, 0, 0);
+        if (owns<KIND>(rb, kb ^ 1)) elem_pinned(kb ^ 1, rb, 2 * kk);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -330,8 +368,9 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
     col[1] = 0.0f;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
+      if (owns<KIND>(rb, 1))
 #pragma unroll
-      for (int i = 0; i < 16; ++i) elem(1, rb, i);
+        for (int i = 0; i < 16; ++i) elem(1, rb, i);
     if (PASS == 2) {
       put_cols(n_clean - 1, 1);
       barrier_lds();
@@ -354,16 +393,18 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
         read_b(tile, 8 * kb + kk);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
-          acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              qa[rb][kk], kbuf[(8 * kb + kk) % 4], kk == 0 ? mask_init<NW>(t0, kb, rb, lim_s) : acc[kb][rb], 0, 0,
-              0);
+          if (owns<KIND>(rb, kb))
+            acc[kb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                qa[rb][kk], kbuf[(8 * kb + kk) % 4],
+                kk == 0 ? mask_init<NW, MODE>(t0, kb, rb, lim_s) : acc[kb][rb], 0, 0, 0);
       }
       col[0] = 0.0f;
       col[1] = 0.0f;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
+        if (owns<KIND>(rb, kb))
 #pragma unroll
-        for (int i = 0; i < 16; ++i) elem(kb, rb, i);
+          for (int i = 0; i < 16; ++i) elem(kb, rb, i);
       if (PASS == 2) put_cols(n, kb);
     }
     if (PASS == 2) {
@@ -377,12 +418,22 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
     // the chunk's sum is a plain sum over them.  A row that sees a key of the
     // chunk but whose sum overflowed, or underflowed below 2^-60 (its logits
     // far under its group's offset), sends the chunk to the exact pass.
+    float srow[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) srow[rb] = sum32_scatter(sum[rb]);
+    const int i = scatter_reg(lane);
+    if constexpr (MODE == kBalanced) {
+      // A shared block's second wave hands its half of the row sums over.
+      if (KIND == 2 && (lane & 1) == 0) sh.xch[(wave - 4) >> 1][acc32_row(i, lane)] = srow[1];
+      __syncthreads();
+      if (KIND == 1) srow[1] += sh.xch[(wave - 4) >> 1][acc32_row(i, lane)];
+    }
     bool bad = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const float s = sum32_scatter(sum[rb]);
-      const int i = scatter_reg(lane);
-      const int r = block_of<NW>(rb) * 32 + acc32_row(i, lane);
+      if (MODE == kBalanced && KIND == 2 && rb == 1) continue;  // written by the first sharing wave
+      const float s = srow[rb];
+      const int r = block_of<NW, MODE>(rb) * 32 + acc32_row(i, lane);
       float o = ofs[rb][0];
 #pragma unroll
       for (int g = 1; g < 4; ++g) o = (i >> 2) == g ? ofs[rb][g] : o;
@@ -391,9 +442,31 @@ __global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kerne
         bad |= r < a.rows && lim_s[r] >= cp.c0 && !(s >= 0x1.0p-60f && s < INFINITY);
       }
     }
-    if (__ballot(bad) != 0 && lane == 0) atomicOr(&risky, 1);
+    if (__ballot(bad) != 0 && lane == 0) atomicOr(&sh.risky, 1);
     __syncthreads();
-    if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = risky;
+    if (threadIdx.x == 0) a.redo[size_t(unit) * a.total_chunks + cp.gchunk] = sh.risky;
+  }
+}
+
+template <int PASS, int RB, int NW, int MODE>
+__global__ __launch_bounds__(NW * 64, kScoreMinGroups<NW>) void score_pass_kernel(ScoreArgs a) {
+  __shared__ ScoreShared<RB, NW> sh;
+  const int unit = blockIdx.y;
+  const ChunkPos cp = locate_chunk(a.lay, a.chunk, blockIdx.x);
+  if (cp.seq < 0) return;
+  if (PASS == 1 && threadIdx.x == 0) sh.risky = 0;
+  fill_row_limits(a, cp, sh.lim_s);
+  if constexpr (MODE == kBalanced) {
+    static_assert(NW == 8 && RB == 2, "the balanced layout is 14 blocks on 8 waves");
+    const int w = wave_id();
+    if (w < 4)
+      score_pass_body<PASS, RB, NW, MODE, 0>(a, sh, cp, unit);
+    else if (w & 1)
+      score_pass_body<PASS, RB, NW, MODE, 2>(a, sh, cp, unit);
+    else
+      score_pass_body<PASS, RB, NW, MODE, 1>(a, sh, cp, unit);
+  } else {
+    score_pass_body<PASS, RB, NW, MODE, 0>(a, sh, cp, unit);
   }
 }
 
@@ -509,11 +582,11 @@ __global__ __launch_bounds__(64) void score_combine_kernel(ScoreArgs a) {
   a.lse2[(size_t(unit) * a.lay.n_seqs + s) * a.rows_pad + r] = out;
 }
 
-template <int RB, int NW>
+template <int RB, int NW, int MODE = kPlain>
 hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
   const dim3 grid(a.total_chunks, a.lay.n_units);
   const dim3 block(64 * NW);
-  hipLaunchKernelGGL((score_pass_kernel<1, RB, NW>), grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_pass_kernel<1, RB, NW, MODE>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((score_rowstats_exact_kernel<RB, NW>), dim3(std::min(a.total_chunks, 4), a.lay.n_units), block, 0,
@@ -524,7 +597,7 @@ hipError_t launch_rb(const ScoreArgs& a, hipStream_t stream) {
                      stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((score_pass_kernel<2, RB, NW>), grid, block, 0, stream, a);
+  hipLaunchKernelGGL((score_pass_kernel<2, RB, NW, MODE>), grid, block, 0, stream, a);
   return hipGetLastError();
 }
 
@@ -540,6 +613,10 @@ hipError_t launch_nw(const ScoreArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_score_window(const ScoreArgs& a, hipStream_t stream) {
+  // The exact pass 1 keeps the plain 8-wave layout (blocks w and w + 8): it
+  // writes whole rows, whichever waves hold them.
+  if (a.balanced) return a.waves == 8 && a.row_blocks == 2 && a.blocks == 14 ? launch_rb<2, 8, kBalanced>(a, stream)
+                                                                            : hipErrorInvalidValue;
   switch (a.waves) {
     case 1: return launch_nw<1>(a, stream);
     case 2: return launch_nw<2>(a, stream);

@@ -40,7 +40,7 @@ struct Facts {
   int64_t max_seq;
   int64_t total_hist_blocks;
   int64_t max_cur;
-  int32_t rows, rows_pad, blocks, waves, row_blocks, chunk;
+  int32_t rows, rows_pad, blocks, waves, row_blocks, balanced, chunk;
   int64_t total_chunks;
   int32_t sel_parts;    // parts per segment of the gate and top-B selections
   int32_t max_seq_frames;
@@ -57,6 +57,11 @@ Facts derive(const stlite_problem* p) {
   f.blocks = nb;
   f.row_blocks = nb >= 2 ? 2 : 1;
   f.waves = (nb + f.row_blocks - 1) / f.row_blocks;
+  // 14 blocks (e.g. G = 7 query heads per KV head, window 64) run on 8 waves
+  // instead of 7, two of the blocks split by key block between two waves, so
+  // that each of the four SIMDs of a CU carries the same vector work.
+  f.balanced = nb == 14 ? 1 : 0;
+  if (f.balanced) f.waves = 8;
   f.rows_pad = f.waves * f.row_blocks * 32;
   // Key chunk per work-group of the score passes.  Their window queries fill
   // the register file (two waves per SIMD), so a CU holds 8 / waves of their
@@ -462,6 +467,7 @@ stlite_status stlite_score_window(const stlite_problem* p, const uint16_t* q_win
   a.blocks = f.blocks;
   a.waves = f.waves;
   a.row_blocks = f.row_blocks;
+  a.balanced = f.balanced;
   a.chunk = f.chunk;
   a.total_chunks = int32_t(f.total_chunks);
   return hip_status(launch_score_window(a, static_cast<hipStream_t>(stream)), "score_window launch");

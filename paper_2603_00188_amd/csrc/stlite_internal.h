@@ -43,6 +43,7 @@ struct ScoreArgs {
   int32_t blocks;        // ceil(rows / 32) real 32-row blocks
   int32_t waves;         // 1 .. 8
   int32_t row_blocks;    // 32-row MFMA blocks per wave (1 or 2)
+  int32_t balanced;      // 1: 14 blocks on 8 waves, 7 units per SIMD (score_window.hip)
   int32_t chunk;         // keys per work-group (multiple of 64)
   int32_t total_chunks;  // sum over sequences of ceil(L_s / chunk)
 };

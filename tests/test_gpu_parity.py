@@ -84,6 +84,10 @@ SMALL = {
     "g3w60": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=3, Hkv=2, window=60, layers=1),
     "g5w60": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=5, Hkv=1, window=60, layers=1),
     "g6w64": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=6, Hkv=1, window=64, layers=1),
+    # 14 row blocks (the balanced 8-wave layout, two blocks split by key block between two waves):
+    # several key chunks per sequence, a short second sequence, and 28 padding rows in a split block
+    "g7w64": _small([[(F, 20, 30), (T, 100)] * 4, [(T, 50), (F, 9, 10), (T, 77)]], G=7, Hkv=1, window=64, layers=1),
+    "g7w60": _small([[(F, 20, 30), (T, 100)] * 3, [(F, 5, 6), (T, 300)]], G=7, Hkv=2, window=60, layers=1),
     # more frames in one sequence than the selection kernels keep in LDS (1024)
     "many_frames": _small([[(F, 2, 3), (T, 1)] * 1100 + [(T, 20)]], G=2, Hkv=1, layers=1, beta=(1, 3)),
 }
