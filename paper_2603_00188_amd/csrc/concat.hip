@@ -382,17 +382,13 @@ __global__ __launch_bounds__(256) void css_cat_kernel(CssArgs a) {
 }
 
 // Phi = 0 on the text tokens of every layer (the frames are written by css_cat_kernel).
+// Work-group (g, layer) writes text run g (token_run).
 __global__ __launch_bounds__(256) void cat_text_kernel(CssArgs a) {
   const Layout& lay = a.lay;
-  const int s = blockIdx.x, layer = blockIdx.y;
-  float* out = a.phi + size_t(layer) * lay.total_tokens;
-  const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
-  int32_t prev = lay.cu_seqlens[s];
-  for (int32_t f = f0; f <= f1; ++f) {
-    const int32_t off = f < f1 ? lay.frame_meta[3 * f] : lay.cu_seqlens[s + 1];
-    for (int32_t j = prev + threadIdx.x; j < off; j += blockDim.x) out[j] = 0.0f;
-    if (f < f1) prev = off + frame_size(lay, f);
-  }
+  float* out = a.phi + size_t(blockIdx.y) * lay.total_tokens;
+  int32_t b, e;
+  token_run(lay, int32_t(blockIdx.x), false, &b, &e);
+  for (int32_t j = b + int32_t(threadIdx.x); j < e; j += blockDim.x) out[j] = 0.0f;
 }
 
 }  // namespace
@@ -426,7 +422,7 @@ hipError_t launch_tsg_rho_concat(const RhoArgs& r, const GateArgs& g, hipStream_
 
 hipError_t launch_css_concat(const CssArgs& a, hipStream_t stream) {
   const int32_t H = a.lay.n_kv_heads, n_layers = a.lay.n_units / H;
-  hipLaunchKernelGGL(cat_text_kernel, dim3(a.lay.n_seqs, n_layers), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(cat_text_kernel, dim3(a.lay.n_frames + a.lay.n_seqs, n_layers), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.lay.n_frames == 0) return e;
   const int64_t logical = int64_t(a.lay.n_frames) * a.strips;

@@ -399,23 +399,20 @@ __global__ __launch_bounds__(256) void css_wide_kernel(CssArgs a) {
     }
 }
 
+// Phi = 0 on text tokens: work-group (g, unit) writes text run g (token_run),
+// all runs at once.
 __global__ __launch_bounds__(256) void css_text_kernel(CssArgs a) {
   const Layout& lay = a.lay;
-  const int s = blockIdx.x, unit = blockIdx.y;
-  float* out = a.phi + size_t(unit) * lay.total_tokens;
-  const int32_t f0 = lay.cu_frames[s], f1 = lay.cu_frames[s + 1];
-  int32_t prev = lay.cu_seqlens[s];
-  for (int32_t f = f0; f <= f1; ++f) {
-    const int32_t off = f < f1 ? lay.frame_meta[3 * f] : lay.cu_seqlens[s + 1];
-    for (int32_t j = prev + threadIdx.x; j < off; j += blockDim.x) out[j] = 0.0f;
-    if (f < f1) prev = off + lay.frame_meta[3 * f + 1] * lay.frame_meta[3 * f + 2];
-  }
+  float* out = a.phi + size_t(blockIdx.y) * lay.total_tokens;
+  int32_t b, e;
+  token_run(lay, int32_t(blockIdx.x), false, &b, &e);
+  for (int32_t j = b + int32_t(threadIdx.x); j < e; j += blockDim.x) out[j] = 0.0f;
 }
 
 }  // namespace
 
 hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream) {
-  hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_frames + a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.lay.n_frames == 0) return e;
   const int64_t logical = int64_t(a.lay.n_frames) * a.strips;  // a.strips: max over frames of 4 x 16 tiles
@@ -431,7 +428,7 @@ hipError_t launch_css_wide(const CssArgs& a, int32_t nbhd, hipStream_t stream) {
 }
 
 hipError_t launch_css(const CssArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(css_text_kernel, dim3(a.lay.n_frames + a.lay.n_seqs, a.lay.n_units), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.lay.n_frames == 0) return e;
   const int64_t logical = int64_t(a.lay.n_frames) * a.strips;  // a.strips: max over frames of ceil(C / 14)

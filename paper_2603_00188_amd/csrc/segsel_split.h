@@ -46,7 +46,9 @@ constexpr int kSpWaves = kSpThreads / 64;
 constexpr int kSpPerThread = 24;             // candidate entries per resolving thread and batch
 constexpr int kSpBatch = kSpPerThread * kSpThreads;  // 24576
 constexpr int kSpSampleEach = 2;             // sample keys per sampling thread
+constexpr int kSpSampleLog = 11;
 constexpr int kSpSample = kSpThreads * kSpSampleEach;  // 2048 sample keys
+static_assert(kSpSample == 1 << kSpSampleLog, "the strata are found by a shift");
 constexpr int kSpPassThreads = 256;          // classify and emit: 4 waves per work-group
 constexpr int kSpPassWaves = kSpPassThreads / 64;
 constexpr int kSpStage = 512;                // candidates staged per wave before a flush
@@ -68,8 +70,8 @@ enum : int32_t {
 };
 // Segment state words.
 enum : int { kSpLo = 0, kSpHi, kSpK, kSpCount, kSpMode, kSpT, kSpCut, kSpNeed, kSpLe, kSpEqLo, kSpEqHi };
-// (kSpLe, kSpEqLo, kSpEqHi: a direct output's totals of keys <= lo, == lo and
-// == hi, summed by classify; a ranked list's come from its tile records.)
+// (kSpLe, kSpEqLo, kSpEqHi: the segment's totals of keys <= lo, == lo and
+// == hi, summed by classify.)
 // Tile record words: counts of codes 0..3, taken candidates, output offset,
 // and (kModeAll) the largest selectable key plus one (0: none).
 enum : int { kTileLess = 0, kTileEqLo, kTileMid, kTileEqHi, kTileTaken, kTileOut, kTileMax, kTileWords = 8 };
@@ -402,7 +404,7 @@ struct SpSampleShared {
 
 // The sample positions of one segment and the first step of their loads,
 // issued before anything else of the sample kernel: the n tokens fall in S =
-// min(2048, n) strata [floor(j n / S), floor((j + 1) n / S)), and stratum j
+// S = min(2048, n) strata [floor(j n / S), floor((j + 1) n / S)), and stratum j
 // (thread j mod kSpThreads, slot j / kSpThreads) gives one hashed position.
 // Prod provides Raw1, void load1(int32_t i, Raw1&), void load1_rest(int32_t
 // i, int cls, Raw1&) and uint32_t key1(const Raw1&, int cls): the inputs of
@@ -425,8 +427,8 @@ __device__ __forceinline__ void sp_gather(const Prod& p, const Layout& lay, cons
     const int32_t j = int32_t(threadIdx.x) + kSpThreads * e;
     g.pos[e] = 0;
     if (j < S) {
-      const int32_t a = S == n ? j : int32_t((int64_t(j) * n) >> 11);
-      const int32_t b = S == n ? j + 1 : int32_t((int64_t(j + 1) * n) >> 11);
+      const int32_t a = S == n ? j : int32_t((int64_t(j) * n) >> kSpSampleLog);
+      const int32_t b = S == n ? j + 1 : int32_t((int64_t(j + 1) * n) >> kSpSampleLog);
       g.pos[e] = a + int32_t(__umulhi(sp_hash(uint32_t(j) ^ salt), uint32_t(b - a)));
       g.valid |= 1u << e;
     }
@@ -531,8 +533,17 @@ __device__ void split_sample(const Prod& p, SpSampleShared& sh, const SeqFrames<
     }
   }
   if (threadIdx.x == 0) {
-    st[kSpLo] = int32_t(has_lo ? min(plo, kSelKeyMax) : 0u);
-    st[kSpHi] = int32_t(has_hi ? min(phi, kSelKeyMax) : kSelKeyMax);
+    // The two splitters are kept distinct: a key equal to both would take the
+    // code of a key strictly between them while counting as a tie at both
+    // (a tie group covering the whole sample band, e.g. the gated-out S = 0).
+    uint32_t lo = has_lo ? min(plo, kSelKeyMax) : 0u;
+    uint32_t hi = has_hi ? min(phi, kSelKeyMax) : kSelKeyMax;
+    if (lo == hi) {
+      if (hi < kSelKeyMax) hi = lo + 1u;
+      else lo = hi - 1u;
+    }
+    st[kSpLo] = int32_t(lo);
+    st[kSpHi] = int32_t(hi);
     st[kSpK] = k;
     st[kSpCount] = 0;
     st[kSpMode] = kModeOpen;
@@ -639,8 +650,8 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
       if (j0 + i < nt && !(((g.uni >> i) & 1u) && !p.selectable(int((g.ucls >> (2 * i)) & 3u))))
         p.load((tw + kSpPassWaves * (j0 + i)) * kSpTile, raw[i]);
   };
-  // a direct output's totals (keys <= lo: a per-lane count in the fast path
-  // and a wave count elsewhere; ties at lo and at hi)
+  // the segment's totals (keys <= lo: for a direct output a per-lane count in
+  // the fast path and a wave count elsewhere; ties at lo and at hi)
   uint32_t le_lane = 0u;
   int32_t le_w = 0, eqlo_w = 0, eqhi_w = 0;
   // cnt: keys <= lo, == lo, strictly between, == hi.  A ranked list records
@@ -649,11 +660,9 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
   auto finish_tile = [&](int32_t t, int32_t base, uint32_t packed, const int32_t (&cnt)[4], uint32_t kmax) {
     if (Prod::kDirect) put(base, packed);
     else __builtin_amdgcn_raw_buffer_store_b32(packed, codes, base + 4 * lane, 0, 0);
-    if (Prod::kDirect) {
-      le_w += cnt[0];
-      eqlo_w += cnt[1];
-      eqhi_w += cnt[3];
-    }
+    le_w += cnt[0];
+    eqlo_w += cnt[1];
+    eqhi_w += cnt[3];
     if (!Prod::kDirect || cnt[1] + cnt[3] > 0 || mode == kModeAll) {
       if (lane == 0) {
         int4* rec = reinterpret_cast<int4*>(tiles + size_t(t) * kTileWords);
@@ -775,7 +784,7 @@ __device__ void split_classify(const Prod& p, SpPassShared& sh, const SelPlan& s
     process(rb, j + G, gb);
   }
   if (staged) flush();
-  if (Prod::kDirect) {  // the wave's totals
+  {  // the wave's totals
     const int32_t le = __builtin_amdgcn_readlane(sp_wave_inscan(int32_t(le_lane)), 63) + le_w;
     if (lane == 0) {
       if (le) atomicAdd(&st[kSpLe], le);
@@ -1058,36 +1067,12 @@ __device__ uint32_t split_resolve(const Prod& pe, SpResolveShared& sh, const Sel
   };
   const bool one = nlist <= kSpBatch;
   reload(0);
-  // totals of the four codes: a direct output's from the state words, a
-  // ranked list's from its tile records
-  int32_t N0, N1, N2, N3;
-  if (Prod::kDirect) {
-    N1 = st[kSpEqLo];
-    N0 = st[kSpLe] - N1;
-    N2 = count;
-    N3 = st[kSpEqHi];
-  } else {
-    int32_t a[4] = {0, 0, 0, 0};
-    for (int32_t t = threadIdx.x; t < ntile; t += kSpThreads) {
-      const int4 x = *reinterpret_cast<const int4*>(tiles + size_t(t) * kTileWords);
-      a[0] += x.x;
-      a[1] += x.y;
-      a[2] += x.z;
-      a[3] += x.w;
-    }
-    if (threadIdx.x < 4) sh.sum[threadIdx.x] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int32_t w = wave_sum(a[q]);
-      if (lane == 0 && w) atomicAdd(&sh.sum[q], w);
-    }
-    __syncthreads();
-    N0 = sh.sum[0];
-    N1 = sh.sum[1];
-    N2 = sh.sum[2];
-    N3 = sh.sum[3];
-  }
+  // totals of the four codes (keys below lo, equal to lo, strictly between,
+  // equal to hi), summed by classify into the state words
+  const int32_t N1 = st[kSpEqLo];
+  const int32_t N0 = st[kSpLe] - N1;
+  const int32_t N2 = count;
+  const int32_t N3 = st[kSpEqHi];
   if (s.split_exact || k <= N0) mode = kModeExact;
   else if (k <= N0 + N1) mode = kModeTieLo;
   else if (k <= N0 + N1 + N2) mode = count <= cap ? kModeMid : kModeExact;

@@ -27,6 +27,31 @@ struct Layout {
   int64_t total_budget;
 };
 
+// Token run g of a layout's non-frame tokens, [*b, *e): for g < n_frames the
+// text after frame g, up to the next frame of its sequence or the sequence's
+// end, preceded by frame g itself when with_current and frame g is its
+// sequence's last (current) frame; for n_frames <= g < n_frames + n_seqs the
+// text before sequence g - n_frames's first frame (all of it when it has no
+// frame).  Runs of all g cover exactly the text (and current) tokens.
+__device__ inline void token_run(const Layout& lay, int32_t g, bool with_current, int32_t* b, int32_t* e) {
+  if (g < lay.n_frames) {
+    int32_t lo = 0, hi = lay.n_seqs - 1;  // the sequence of frame g: last s with cu_frames[s] <= g
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (lay.cu_frames[mid] <= g) lo = mid;
+      else hi = mid - 1;
+    }
+    const bool last = g + 1 == lay.cu_frames[lo + 1];
+    const int32_t start = lay.frame_meta[3 * g];
+    *b = with_current && last ? start : start + lay.frame_meta[3 * g + 1] * lay.frame_meta[3 * g + 2];
+    *e = last ? lay.cu_seqlens[lo + 1] : lay.frame_meta[3 * (g + 1)];
+  } else {
+    const int32_t s = g - lay.n_frames;
+    *b = lay.cu_seqlens[s];
+    *e = lay.cu_frames[s] < lay.cu_frames[s + 1] ? lay.frame_meta[3 * lay.cu_frames[s]] : lay.cu_seqlens[s + 1];
+  }
+}
+
 struct ScoreArgs {
   Layout lay;
   const uint16_t* q;     // [layers][seqs][Hq][window][d]
@@ -137,7 +162,7 @@ __host__ __device__ inline int64_t sel_key_base(int32_t s0, int32_t seq) { retur
 struct GateArgs {
   Layout lay;
   const float* rho;      // [units][L] (historical entries read)
-  float* rho_zero_fill;  // nullable: every entry of this array is zeroed before rho is written
+  float* rho_zero_fill;  // nullable: its entries of non-historical tokens are zeroed (the rho pass writes the rest)
   uint8_t* gate;         // nullable for the rho-only call; [units][L]
   int32_t* hist_tok;     // workspace [sum N_hist]: absolute token of every historical row
   HistBlock* blocks;     // workspace [total_hist_blocks]
@@ -209,7 +234,8 @@ hipError_t launch_tsg_fixed_gate(const GateArgs& g, float tau, hipStream_t strea
 // Rank gate and tau_red from g.rho (the exact selection of segsel.h).
 hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream);
 // TSG plan tables (historical-token table, rho blocks) and the
-// fill of g.gate with 1 / g.rho_zero_fill with 0 over g.lay.n_units units.
+// fill of g.gate with 1 (every token) and of g.rho_zero_fill with 0 (the
+// tokens that are not historical) over g.lay.n_units units.
 hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream);
 // Concatenated key space (D = n_kv_heads * 128; outputs [n_layers][total_tokens]).
 hipError_t launch_layer_mean(const float* a_base, float* a_layer, const Layout& lay, hipStream_t stream);

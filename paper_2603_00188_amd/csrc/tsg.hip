@@ -74,9 +74,9 @@ __global__ __launch_bounds__(256) void tsg_plan_kernel(GateArgs a) {
   for (int32_t j = threadIdx.x; j < n; j += blockDim.x) a.hist_tok[h + j] = off + j;
 }
 
-// gate = 1 on every token (the emit pass then decides the historical ones) and
-// rho = 0 everywhere (the rho pass then writes the historical ones); either
-// pointer may be null.
+// gate = 1 on every token (the selection then decides the historical ones)
+// and rho = 0 everywhere; either pointer may be null.  (The rho call zeroes
+// only the tokens that are not historical, with rho_zero_kernel.)
 __global__ __launch_bounds__(256) void gate_fill_kernel(GateArgs a, size_t n) {
   const size_t stride = size_t(gridDim.x) * blockDim.x;
   const size_t i0 = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -96,6 +96,17 @@ __global__ __launch_bounds__(256) void gate_fill_kernel(GateArgs a, size_t n) {
     if (gate) gate[i] = 1;
     if (rho) rho[i] = 0.0f;
   }
+}
+
+// rho = 0 on the tokens that are not historical (text and each sequence's
+// current frame); the rho pass writes every historical token.  Work-group
+// (g, unit) covers token run g (token_run, current frames included).
+__global__ __launch_bounds__(256) void rho_zero_kernel(GateArgs a) {
+  const Layout& lay = a.lay;
+  float* rho = a.rho_zero_fill + size_t(blockIdx.y) * lay.total_tokens;
+  int32_t b, e;
+  token_run(lay, int32_t(blockIdx.x), true, &b, &e);
+  for (int32_t j = b + int32_t(threadIdx.x); j < e; j += blockDim.x) rho[j] = 0.0f;
 }
 
 __device__ inline float sumsq8(uint4 v) {
@@ -124,13 +135,22 @@ __global__ __launch_bounds__(256) void cur_norms_kernel(RhoArgs a) {
   const int32_t n = min(frame_size(lay, f1 - 1), int32_t(blockIdx.x + 1) * 64);
   const uint16_t* kunit = a.k + size_t(unit) * lay.total_tokens * kHeadDim;
   float* rn = a.rn_cur + size_t(unit) * lay.total_tokens;
+  // 16 groups of 16 lanes, four keys per group: all four loads first.
   const int group = threadIdx.x >> 4, gl = threadIdx.x & 15;
-  for (int32_t j = int32_t(blockIdx.x) * 64 + group; j < n; j += blockDim.x >> 4) {
-    const uint4 v = *reinterpret_cast<const uint4*>(kunit + size_t(off + j) * kHeadDim + gl * 8);
-    float ss = sumsq8(v);
+  const int32_t j0 = int32_t(blockIdx.x) * 64 + group;
+  uint4 v[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int32_t j = j0 + 16 * q;
+    v[q] = j < n ? *reinterpret_cast<const uint4*>(kunit + size_t(off + j) * kHeadDim + gl * 8) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int32_t j = j0 + 16 * q;
+    float ss = sumsq8(v[q]);
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
-    if (gl == 0) rn[off + j] = SIM == kSimNegL2 ? -ss : (ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f);
+    if (gl == 0 && j < n) rn[off + j] = SIM == kSimNegL2 ? -ss : (ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f);
   }
 }
 
@@ -363,9 +383,17 @@ hipError_t launch_gate_prologue(const GateArgs& g, hipStream_t stream) {
   hipLaunchKernelGGL(tsg_plan_kernel, dim3(g.lay.n_seqs + g.lay.n_frames), dim3(256), 0, stream, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t n = size_t(g.lay.n_units) * g.lay.total_tokens;
-  const unsigned blocks = unsigned(std::min<size_t>((n / 4 + 255) / 256 + 1, 8192));
-  hipLaunchKernelGGL(gate_fill_kernel, dim3(blocks), dim3(256), 0, stream, g, n);
+  if (g.gate) {
+    GateArgs fill = g;
+    fill.rho_zero_fill = nullptr;
+    const size_t n = size_t(g.lay.n_units) * g.lay.total_tokens;
+    const unsigned blocks = unsigned(std::min<size_t>((n / 4 + 255) / 256 + 1, 8192));
+    hipLaunchKernelGGL(gate_fill_kernel, dim3(blocks), dim3(256), 0, stream, fill, n);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (g.rho_zero_fill && g.lay.n_units > 0)
+    hipLaunchKernelGGL(rho_zero_kernel, dim3(g.lay.n_frames + g.lay.n_seqs, g.lay.n_units), dim3(256), 0, stream, g);
   return hipGetLastError();
 }
 

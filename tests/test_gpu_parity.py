@@ -260,6 +260,60 @@ def test_stage_exact_many_parts_and_ties(torch_cuda, monkeypatch, layout, path, 
                 assert (kept[u, cu_budget[s]:cu_budget[s + 1]] == want).all(), (beta, u, s)
 
 
+@pytest.mark.parametrize("path", [None, "split", "split_exact", "four_pass"])
+def test_stage_tie_group_covers_sample_band(torch_cuda, monkeypatch, path):
+    """A tie group holding most of a long segment and the k-th key: the
+    gate's rho equal to 0.5 on 95 % of the history, and the top-B's S = 0 on
+    every historical token (the gate passed in is all zeros there), with B
+    above the count of positive scores.  The splitters drawn from such a
+    sample fall on the same key; gate, tau and kept lists must still equal
+    the oracle's exactly."""
+    import torch
+    from oracle import stlite_oracle as O
+    from paper_2603_00188_amd import stlite as S
+    if path:
+        monkeypatch.setenv("STLITE_SELECT_PATH", path)
+    nf, (r, c), nt = 80, (40, 50), 100
+    fm, off = [], 0
+    for _ in range(nf):
+        fm.append((off, r, c))
+        off += r * c + nt
+    cu_seqlens = np.array([0, off], np.int32)
+    cu_frames = np.array([0, nf], np.int32)
+    frame_meta = np.array(fm, np.int32)
+    cu_budget = S.budgets(cu_seqlens, 1, 5)
+    prob = S.Problem(1, 2, 2, 8, cu_seqlens, cu_frames, frame_meta, cu_budget)
+    U, L = prob.units, prob.total_tokens
+    B = int(cu_budget[1])
+    vis = np.zeros(L, bool)
+    for o, rr, cc in fm:
+        vis[o:o + rr * cc] = True
+    hist = np.concatenate([np.arange(o, o + rr * cc) for o, rr, cc in fm[:-1]])
+    rng = np.random.default_rng(9)
+    rho = np.zeros((U, L), np.float32)
+    rho[:, hist] = np.where(rng.random((U, len(hist))) < 0.95, np.float32(0.5),
+                            rng.uniform(0.0, 1.0, (U, len(hist))).astype(np.float32))
+    A = rng.uniform(1e-5, 1e-3, (U, L)).astype(np.float32)
+    phi = rng.uniform(0.5, 1.5, (U, L)).astype(np.float32)
+    gate_in = np.ones((U, L), np.uint8)
+    gate_in[:, hist] = 0
+    out = S.Buffers(prob)
+    dev = lambda x: torch.from_numpy(x).cuda()
+    S.stlite_tsg_threshold(prob, dev(rho), out.tau, out.gate, out.ws_tsg)
+    S.stlite_select_topk(prob, dev(A), dev(phi), dev(gate_in), 1.0, out.kept, out.score, out.ws)
+    torch.cuda.synchronize()
+    gate, tau, kept = out.gate.cpu().numpy(), out.tau.cpu().numpy(), out.kept.cpu().numpy()
+    n_pos = int(np.count_nonzero(~vis)) + int(fm[-1][1] * fm[-1][2])
+    assert B > n_pos  # the k-th largest S is one of the zeros
+    for u in range(U):
+        g_ref, tau_ref = O.tsg_gate(rho[u][hist].astype(np.float64), hist, L, B)
+        assert (gate[u] == g_ref).all(), u
+        assert np.float32(tau[u, 0]) == np.float32(tau_ref), u
+        s32 = np.where(vis, np.where(gate_in[u] > 0, A[u] + phi[u], np.float32(0)), A[u])
+        want = O.select_topk(s32.astype(np.float64), B)
+        assert (kept[u, :B] == want).all(), u
+
+
 @pytest.mark.parametrize("path", ["four_pass", "split", "split_exact"])
 def test_selection_paths_agree(torch_cuda, monkeypatch, path):
     """The whole pass on the small cases (ragged batches, sequences shorter
