@@ -269,7 +269,7 @@ hipError_t launch_gate_select(const GateArgs& g, hipStream_t stream) {
     case kSelPathSplit:
       return launch_split(g.sel.lds_frames ? gate_split_sample_kernel<true> : gate_split_sample_kernel<false>,
                           gate_split_classify_kernel, gate_split_resolve_kernel,
-                          static_cast<void (*)(GateArgs)>(nullptr), g, g.sel, g.lay, stream);
+                          static_cast<void (*)(GateArgs)>(nullptr), g, g.lay, stream);
     default:
       return launch_sel_passes(g.sel.lds_frames ? gate_produce_kernel<true> : gate_produce_kernel<false>,
                                gate_emit_kernel, g, g.sel, g.lay, stream);

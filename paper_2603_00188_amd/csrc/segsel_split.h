@@ -1299,10 +1299,32 @@ __device__ inline SeqFrames<LDS> sp_frames(int32_t* fs, int32_t* fe, const Layou
 // The launches: sample and resolve over (1, sequences, units), classify and
 // (with an emit kernel: ranked lists) emit over (split_parts, sequences,
 // units).
+//
+// The classify and emit grids are sized to whole rounds of the work-groups
+// the GPU holds at once (the classify kernel's occupancy on 256 CUs), so that
+// no last round runs on a fraction of the chip: the parts per segment are a
+// round's work-groups over the segments, in as many rounds as keep a
+// work-group to at most 64 tiles.  Without an occupancy figure the plan's
+// part count (32 tiles per work-group) stays.
 template <class Args>
 hipError_t launch_split(void (*sample)(Args), void (*classify)(Args), void (*resolve)(Args), void (*emit)(Args),
-                        const Args& a, const SelPlan& s, const Layout& lay, hipStream_t stream) {
+                        const Args& a_in, const Layout& lay, hipStream_t stream) {
   if (lay.n_units == 0 || lay.n_seqs == 0) return hipSuccess;
+  static int occupancy = 0;  // work-groups of the classify kernel per CU (-1: unknown)
+  if (occupancy == 0) {
+    int b = 0;
+    occupancy = hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, classify, kSpPassThreads, 0) == hipSuccess && b > 0
+                    ? b : -1;
+  }
+  Args a = a_in;
+  SelPlan& s = a.sel;
+  if (occupancy > 0) {
+    const int64_t segs = int64_t(lay.n_units) * lay.n_seqs;
+    const int64_t per_round = std::max<int64_t>(1, int64_t(256) * occupancy / segs);
+    const int64_t tiles = std::max<int64_t>(1, s.split_tiles);
+    const int64_t rounds = std::max<int64_t>(1, (tiles + 64 * per_round - 1) / (64 * per_round));
+    s.split_parts = int32_t(std::min<int64_t>(rounds * per_round, tiles));
+  }
   const dim3 seg_grid(1, lay.n_seqs, lay.n_units), pass_grid(s.split_parts, lay.n_seqs, lay.n_units);
   hipLaunchKernelGGL(sample, seg_grid, dim3(kSpThreads), 0, stream, a);
   hipError_t e = hipGetLastError();

@@ -313,7 +313,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     case kSelPathSplit:
       return launch_split(a.sel.lds_frames ? select_split_sample_kernel<true> : select_split_sample_kernel<false>,
                           select_split_classify_kernel, select_split_resolve_kernel, select_split_emit_kernel, a,
-                          a.sel, a.lay, stream);
+                          a.lay, stream);
     default:
       return launch_sel_passes(a.sel.lds_frames ? select_produce_kernel<true> : select_produce_kernel<false>,
                                select_emit_kernel, a, a.sel, a.lay, stream);

@@ -184,6 +184,7 @@ SelPlan sel_carve(const stlite_problem* p, const Facts& f, char* w) {
   s.lds_frames = f.max_seq_frames <= kSelFrames ? 1 : 0;
   sel_path(f, s);
   s.split_parts = split_parts(p, f);
+  s.split_tiles = int32_t(std::max<int64_t>(ceil_div(f.max_seq, 256), 1));
   {  // the splitter path's arrays, over the same bytes as the four passes' ones
     const size_t U = size_t(f.units);
     char* x = w;

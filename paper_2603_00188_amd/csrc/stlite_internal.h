@@ -124,7 +124,8 @@ struct SelPlan {
   int32_t* tiles;        // [units][sp_tile_stride][8]: per 256-token tile counts and output offset
   uint2* cands;          // [units][sp_cand_stride]: (key, token) of the tokens between the splitters
   int32_t* sstate;       // [units][seqs][kSpWords]: splitters, counts, mode, T, tie cut
-  int32_t split_parts;   // work-groups per segment of the classify and emit passes
+  int32_t split_parts;   // work-groups per segment of the classify and emit passes (launch_split refines it)
+  int32_t split_tiles;   // 256-token tiles of the longest segment
   int32_t split_exact;   // 1: resolve every segment by the exact streaming selection (diagnostic)
   int32_t lds_frames;    // 1: no sequence has more than kSelFrames frames
   int32_t path;          // SelPath
