@@ -62,6 +62,16 @@ class Case:
 
     def run(self, alpha=None, css=True, tsg=True, overlap=False, mean_width=0):
         import torch
+        # Every output element the comparisons read must be written by the
+        # pass: poison them first (NaN, a gate byte of 0xAB, kept index -1).
+        o = self.out
+        o.a_base.fill_(float("nan"))
+        o.kept.fill_(-1)
+        if css:
+            o.phi.fill_(float("nan"))
+        if tsg:
+            o.rho.fill_(float("nan"))
+            o.gate.fill_(0xAB)
         S.compress(self.prob, self.dq, self.dk, self.dv, self.out,
                    alpha=self.w.alpha if alpha is None else alpha, css=css, tsg=tsg, overlap=overlap,
                    mean_width=mean_width)
