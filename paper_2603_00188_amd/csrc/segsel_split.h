@@ -403,7 +403,7 @@ struct SpSampleShared {
 };
 
 // The sample positions of one segment and the first step of their loads,
-// issued before anything else of the sample kernel: the n tokens fall in S =
+// issued before anything else of the sample kernel: the n tokens fall in
 // S = min(2048, n) strata [floor(j n / S), floor((j + 1) n / S)), and stratum j
 // (thread j mod kSpThreads, slot j / kSpThreads) gives one hashed position.
 // Prod provides Raw1, void load1(int32_t i, Raw1&), void load1_rest(int32_t
