@@ -329,9 +329,9 @@ def measured_peaks(stream):
 def chr_harness(prob, q, dk, a_base, out, stream):
     """Cache hit rate (Eq. chr) of the pass's kept sets and of SnapKV mode (the
     same window score, flat top-B, no CSS or gate) against I*, the top-B of the
-    first decode query's attention over the full cache.  On this generator the
-    decode query is the last window query, so window voting is close to I* by
-    construction: these values describe the generator, not GUI traces."""
+    first decode query's attention over the full cache.  Here the decode query
+    is the last window query, so window voting is close to I* by construction:
+    these values describe the synthetic inputs, not GUI traces."""
     import torch
     from paper_2603_00188_amd import stlite as S
     from paper_2603_00188_amd import workload as W
@@ -489,6 +489,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--beta", default=None, metavar="NUM/DEN",
                     help="budget ratio as a fraction (default: the workload's own)")
+    ap.add_argument("--screen", default="iid", choices=("iid", "gui"),
+                    help="screen model of the synthetic frames: independent patches (default) or flat "
+                         "textured panels with UI elements")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-baseline-only", action="store_true",
                     help="only time the fp64 oracle on the host for --config (no GPU work) and print it")
@@ -508,7 +511,7 @@ def main():
     from paper_2603_00188_amd import workload as W
     beta = tuple(int(x) for x in args.beta.split("/")) if args.beta else None
     if args.cpu_baseline_only:
-        w = W.config(args.config, beta)
+        w = W.config(args.config, beta).with_screen(args.screen)
         log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
         base = cpu_baseline(w, W.make_inputs(w, workers=16))
         print(json.dumps({"config": w.name, "tokens": w.total_tokens, "cpu_baseline": base}), flush=True)
@@ -522,7 +525,7 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
-    w = W.config(args.config, beta)
+    w = W.config(args.config, beta).with_screen(args.screen)
     log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
     inputs = W.make_inputs(w, workers=16)
     scene, k, v, q = inputs
@@ -643,7 +646,7 @@ def main():
                         f"beta {w.beta[0]}/{w.beta[1]}, alpha {w.alpha}",
             "tokens": lay.total_tokens, "layers": w.n_layers, "kv_heads": w.n_kv_heads,
             "q_heads": w.n_q_heads, "window": w.window, "beta": f"{w.beta[0]}/{w.beta[1]}",
-            "budget_per_unit": int(cu_budget[-1]),
+            "budget_per_unit": int(cu_budget[-1]), "screen": w.screen,
             "streams": "score | tsg_rho+tsg_threshold+css, then select, compact" if overlap else "one stream",
         },
         "roofline": roof,

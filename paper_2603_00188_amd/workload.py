@@ -29,6 +29,18 @@ Recipe (all draws in float32, rounded once to bf16 with round-to-nearest-even):
   keys of kv head g//G over the sequence's element rectangle, plus N(0, 0.1^2)
   noise per component.
 
+Two screen models (``Workload.screen``):
+
+* ``"iid"`` (every named workload): each freshly drawn patch embedding is
+  independent of its neighbours;
+* ``"gui"``: a screen is a few flat panels (a top bar, a side bar and the main
+  area, one colour embedding each, drawn once per trajectory) with UI elements
+  drawn over about a quarter of the area.  A background patch is its panel's
+  colour plus a texture of 1/3 of its scale (neighbouring background patches
+  have cosine about 0.9); an element patch is an independent embedding.  A
+  frame transition repaints each resampled rectangle the same way.  The
+  element rectangle the queries aim at is centred on an element patch.
+
 Random streams: ``numpy.random.SeedSequence(seed).spawn(n_layers + 1)``; stream 0
 draws the layout, the frame evolution and the element rectangles, stream l+1
 draws everything that belongs to layer l, so any single layer can be
@@ -47,6 +59,11 @@ HEAD_DIM = 128
 # Segment kinds in a trajectory description.
 FRAME = "frame"
 TEXT = "text"
+
+# Screen models (module docstring).
+SCREENS = ("iid", "gui")
+GUI_TEXTURE = 1.0 / 3.0   # background texture scale, relative to a panel colour's
+GUI_COVER = 0.25          # element area drawn per painted region, as a fraction of it
 
 
 @dataclasses.dataclass(frozen=True)
@@ -82,6 +99,7 @@ class Workload:
     seed: int = 0
     alpha: float = 1.0
     head_dim: int = HEAD_DIM
+    screen: str = "iid"                   # "iid" | "gui" (module docstring)
 
     @property
     def group(self) -> int:
@@ -105,6 +123,12 @@ class Workload:
 
     def with_layers(self, n_layers: int) -> "Workload":
         return dataclasses.replace(self, n_layers=n_layers)
+
+    def with_screen(self, screen: str) -> "Workload":
+        if screen not in SCREENS:
+            raise ValueError(f"screen must be one of {SCREENS}")
+        name = self.name if screen == "iid" else f"{self.name}_{screen}"
+        return dataclasses.replace(self, screen=screen, name=name)
 
 
 def _interleaved(n_frames: int, rows: int, cols: int, text) -> Tuple[Tuple, ...]:
@@ -259,6 +283,47 @@ class Scene:
     frame_emb: List[np.ndarray]            # per frame: [rows*cols, d] float32
     element: List[Tuple[int, int, int, int]]  # per sequence: (u0, v0, h, w) in its current frame
     duplicate: List[bool]                  # per frame: exact copy of its predecessor
+    content: Optional[List[np.ndarray]] = None  # gui screens, per frame: [rows*cols] bool, element patch
+
+
+def gui_panels(rows: int, cols: int) -> np.ndarray:
+    """Panel of every cell of a rows x cols gui screen: 0 top bar (the first
+    ~rows/12 rows), 1 side bar (the first ~cols/6 columns below it), 2 main area."""
+    tb = max(1, round(rows / 12))
+    sb = max(1, round(cols / 6))
+    p = np.full((rows, cols), 2, np.int8)
+    p[:tb, :] = 0
+    p[tb:, :sb] = 1
+    return p
+
+
+def _gui_paint(rng, e, content, panels, colours, rect, element, d):
+    """Repaint rect = (u0, v0, h, w) of a gui screen e [rows, cols, d]: textured
+    panel background, then elements over about GUI_COVER of its area (at least
+    one), each of a size drawn from ``element`` and clipped to the rectangle."""
+    u0, v0, h, ww = rect
+    inv = np.float32(1.0 / math.sqrt(d))
+    e[u0:u0 + h, v0:v0 + ww] = (colours[panels[u0:u0 + h, v0:v0 + ww]]
+                                + np.float32(GUI_TEXTURE) * inv * rng.standard_normal((h, ww, d), dtype=np.float32))
+    content[u0:u0 + h, v0:v0 + ww] = False
+    (hlo, hhi), (wlo, whi) = element
+    mean_area = 0.25 * (hlo + hhi) * (wlo + whi)
+    for _ in range(max(1, int(math.ceil(GUI_COVER * h * ww / mean_area)))):
+        eh = min(int(rng.integers(hlo, hhi + 1)), h)
+        ew = min(int(rng.integers(wlo, whi + 1)), ww)
+        a = u0 + int(rng.integers(0, h - eh + 1))
+        b = v0 + int(rng.integers(0, ww - ew + 1))
+        e[a:a + eh, b:b + ew] = rng.standard_normal((eh, ew, d), dtype=np.float32) * inv
+        content[a:a + eh, b:b + ew] = True
+
+
+def _centred_rect(p, rows, cols, h, ww):
+    """Rectangle of size h x w (clipped to the grid) centred on cell p."""
+    h = min(h, rows)
+    ww = min(ww, cols)
+    u0 = min(max(p // cols - h // 2, 0), rows - h)
+    v0 = min(max(p % cols - ww // 2, 0), cols - ww)
+    return u0, v0, h, ww
 
 
 def make_scene(w: Workload) -> Scene:
@@ -266,8 +331,12 @@ def make_scene(w: Workload) -> Scene:
     d = w.head_dim
     rng = _rng(_streams(w)[0])
     red = w.redundancy
+    gui = w.screen == "gui"
+    if w.screen not in SCREENS:
+        raise ValueError(f"unknown screen model {w.screen!r}")
     embs: List[np.ndarray] = []
     dups: List[bool] = []
+    conts: List[np.ndarray] = []
     elems = []
     for s in range(lay.n_seqs):
         fm = lay.seq_frames(s)
@@ -278,10 +347,20 @@ def make_scene(w: Workload) -> Scene:
             n_dup = min(n_dup, nf - 1)
             dup_set = set(int(x) for x in rng.choice(np.arange(1, nf), size=n_dup, replace=False))
         prev = None
+        cont = None
+        colours = None
         for f in range(nf):
             r, c = int(fm[f, 1]), int(fm[f, 2])
             fresh = prev is None or prev.shape[0] != r * c
-            if fresh:
+            if fresh and gui:
+                if colours is None:
+                    colours = rng.standard_normal((3, d), dtype=np.float32) / np.float32(math.sqrt(d))
+                e = np.empty((r, c, d), np.float32)
+                cont = np.zeros((r, c), bool)
+                _gui_paint(rng, e, cont, gui_panels(r, c), colours, (0, 0, r, c), w.element, d)
+                e = e.reshape(r * c, d)
+                dups.append(False)
+            elif fresh:
                 e = (rng.standard_normal((r * c, d), dtype=np.float32) / np.float32(math.sqrt(d)))
                 dups.append(False)
             elif f in dup_set:
@@ -301,22 +380,33 @@ def make_scene(w: Workload) -> Scene:
                         h = int(np.clip(round(math.sqrt(area * aspect)), 1, r))
                         ww = int(np.clip(round(area / h), 1, c))
                         rects.append(_random_rect(rng, r, c, h, ww))
-                for (u0, v0, h, ww) in rects:
-                    e[u0:u0 + h, v0:v0 + ww] = (
-                        rng.standard_normal((h, ww, d), dtype=np.float32) / np.float32(math.sqrt(d)))
+                if gui:
+                    cont = cont.copy()
+                    for rect in rects:
+                        _gui_paint(rng, e, cont, gui_panels(r, c), colours, rect, w.element, d)
+                else:
+                    for (u0, v0, h, ww) in rects:
+                        e[u0:u0 + h, v0:v0 + ww] = (
+                            rng.standard_normal((h, ww, d), dtype=np.float32) / np.float32(math.sqrt(d)))
                 e = e.reshape(r * c, d)
                 dups.append(False)
             embs.append(e)
+            if gui:
+                conts.append(cont.reshape(-1))
             prev = e
         if nf:
             r, c = int(fm[-1, 1]), int(fm[-1, 2])
             (hlo, hhi), (wlo, whi) = w.element
             h = int(rng.integers(hlo, hhi + 1))
             ww = int(rng.integers(wlo, whi + 1))
-            elems.append(_random_rect(rng, r, c, h, ww))
+            if gui:  # centred on an element patch of the current frame
+                cells = np.flatnonzero(conts[-1])
+                elems.append(_centred_rect(int(cells[int(rng.integers(0, len(cells)))]), r, c, h, ww))
+            else:
+                elems.append(_random_rect(rng, r, c, h, ww))
         else:
             elems.append((0, 0, 0, 0))
-    return Scene(lay, embs, elems, dups)
+    return Scene(lay, embs, elems, dups, conts if gui else None)
 
 
 def text_positions(lay: Layout) -> np.ndarray:
@@ -485,26 +575,32 @@ def make_step_inputs(w: Workload, steps: Optional[Sequence[int]] = None,
     # alone whatever other steps are listed
     (hlo, hhi), (wlo, whi) = w.element
     elems, anchors = [], []
+    gui = scene.content is not None
     for t in steps:
         rng = _rng(np.random.SeedSequence([w.seed, STEP_STREAM, t]))
         r, c = int(fm[t, 1]), int(fm[t, 2])
         h = int(rng.integers(hlo, hhi + 1))
         ww = int(rng.integers(wlo, whi + 1))
-        elems.append(_random_rect(rng, r, c, h, ww))
+        if gui:  # centred on an element patch of frame t
+            cells = np.flatnonzero(scene.content[t])
+            elems.append(_centred_rect(int(cells[int(rng.integers(0, len(cells)))]), r, c, h, ww))
+        else:
+            elems.append(_random_rect(rng, r, c, h, ww))
         anchor = None
         if t > 0:
             f = int(rng.integers(0, t))
             ef, et = scene.frame_emb[f], scene.frame_emb[t]
             if ef.shape == et.shape:
-                changed = np.flatnonzero((ef != et).any(axis=1))
+                changed = (ef != et).any(axis=1)
+                if gui and (changed & scene.content[f]).any():  # a changed element patch
+                    changed &= scene.content[f]
+                changed = np.flatnonzero(changed)
                 rf, cf = int(fm[f, 1]), int(fm[f, 2])
                 if len(changed):
                     p = int(changed[int(rng.integers(0, len(changed)))])
-                    h = min(int(rng.integers(hlo, hhi + 1)), rf)
-                    ww = min(int(rng.integers(wlo, whi + 1)), cf)
-                    u0 = min(max(p // cf - h // 2, 0), rf - h)
-                    v0 = min(max(p % cf - ww // 2, 0), cf - ww)
-                    anchor = (f, u0, v0, h, ww)
+                    h = int(rng.integers(hlo, hhi + 1))
+                    ww = int(rng.integers(wlo, whi + 1))
+                    anchor = (f,) + _centred_rect(p, rf, cf, h, ww)
         anchors.append(anchor)
 
     def cells(frame, u0, v0, h, ww):

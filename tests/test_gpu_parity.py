@@ -90,6 +90,11 @@ SMALL = {
     "g7w60": _small([[(F, 20, 30), (T, 100)] * 3, [(F, 5, 6), (T, 300)]], G=7, Hkv=2, window=60, layers=1),
     # more frames in one sequence than the selection kernels keep in LDS (1024)
     "many_frames": _small([[(F, 2, 3), (T, 1)] * 1100 + [(T, 20)]], G=2, Hkv=1, layers=1, beta=(1, 3)),
+    # gui screens (flat textured panels and element patches): clusters of close Phi, rho and S values
+    # around the gate threshold and the top-B cut, with exact duplicate frames and a second trajectory
+    "gui": _small([[(F, 18, 32), (T, 40)] * 5, [(F, 12, 20), (T, 30)] * 3], G=7, Hkv=2, window=32,
+                  beta=(1, 4), red=W.Redundancy(frac=(0.05, 0.2), n_rects=(1, 4), dup_frac=0.3),
+                  element=((1, 3), (2, 4))).with_screen("gui"),
 }
 
 
@@ -373,9 +378,9 @@ def test_determinism(torch_cuda):
         assert np.array_equal(r1[k], r2[k], equal_nan=True), k
 
 
-def _full(idx, beta=None, samples=((0, 0, 0), (27, 3, 0))):
+def _full(idx, beta=None, samples=((0, 0, 0), (27, 3, 0)), screen="iid"):
     H = _H()
-    w = W.config(idx, beta)
+    w = W.config(idx, beta).with_screen(screen)
     H.log(f"config {idx} {w.name}: generate L={w.total_tokens} x {w.n_layers} layers")
     case = H.Case(w)
     H.log(f"config {idx}: run")
@@ -405,6 +410,13 @@ def test_config2_sampled(torch_cuda):
         for layer, kv in units:
             st = H.compare_unit(case2, res2, layer, kv, 0)
             H.log(f"config 2 beta {beta} unit ({layer},{kv},0): {st}")
+
+
+@pytest.mark.timeout(900)
+def test_config2_gui_sampled(torch_cuda):
+    """The long-horizon workload (62,720 tokens) on gui screens, in the
+    benchmark's launch configuration."""
+    _full(2, samples=((0, 0, 0), (13, 2, 0), (27, 3, 0)), screen="gui")
 
 
 @pytest.mark.timeout(900)

@@ -99,3 +99,68 @@ def test_step_inputs_are_prefixes_of_the_trajectory():
     sub = W.make_step_inputs(w, steps=[2, 0], base=base)
     assert np.array_equal(sub.q[:, 0], si.q[:, 2]) and np.array_equal(sub.q_dec[:, 1], si.q_dec[:, 0])
     assert list(np.diff(sub.layout.cu_seqlens)) == [ends[2], ends[0]]
+
+
+def _centre(rect):
+    u0, v0, h, ww = rect
+    return u0 + h // 2, v0 + ww // 2
+
+
+def test_gui_screen_structure():
+    """The gui screen model: the same layout as the named workload, flat
+    textured panels (neighbouring background patches of one panel have cosine
+    about 1 / (1 + (1/3)^2) = 0.9), independent element patches over about a
+    quarter of the screen, transitions that keep every other patch, a query
+    target centred on an element patch, and CSS saliency (the oracle's, Eq.
+    css_calc) that tells elements from background."""
+    from oracle import stlite_oracle as O
+    w = W.config(2).with_layers(1)
+    g = w.with_screen("gui")
+    assert w.screen == "iid" and g.name == "long_horizon_gui"
+    assert W.make_scene(w).content is None
+    sc, k, _, _ = W.make_inputs(g)
+    lay = sc.layout
+    assert np.array_equal(lay.frame_meta, W.make_layout(w).frame_meta)
+    assert len(sc.content) == len(lay.frame_meta)
+    for f, (off, r, c) in enumerate(lay.frame_meta):
+        ct = sc.content[f].reshape(r, c)
+        assert 0.12 < ct.mean() < 0.35
+        e = sc.frame_emb[f].reshape(r, c, -1)
+        cs = (e[:, :-1] * e[:, 1:]).sum(-1) / (np.linalg.norm(e[:, :-1], axis=-1) * np.linalg.norm(e[:, 1:], axis=-1))
+        pan = W.gui_panels(r, c)
+        bg = ~ct[:, :-1] & ~ct[:, 1:] & (pan[:, :-1] == pan[:, 1:])
+        el = ct[:, :-1] & ct[:, 1:]
+        assert 0.85 < cs[bg].mean() < 0.95
+        assert abs(cs[el].mean()) < 0.15
+        if f:
+            same = (sc.frame_emb[f] == sc.frame_emb[f - 1]).all(axis=1)
+            assert np.array_equal(sc.content[f][same], sc.content[f - 1][same])
+            assert 0.6 < same.mean() < 0.999
+    off, r, c = (int(x) for x in lay.frame_meta[-1])
+    u, v = _centre(sc.element[0])
+    assert sc.content[-1].reshape(r, c)[u, v]
+    phi = O.css_frame(O.bf16_to_f64(k[0, 0, off:off + r * c]), r, c)
+    ct = sc.content[-1]
+    assert phi[ct].mean() > 0.9 and phi[~ct].mean() < 0.45
+
+
+def test_gui_step_targets_and_anchors():
+    """Per-step inputs on gui screens: each step's element is centred on an
+    element patch of its current frame, and each anchor on an element patch of
+    the earlier frame that the current frame has changed."""
+    w = W.config(3).with_layers(1).with_screen("gui")
+    si = W.make_step_inputs(w, steps=[0, 3, 20, 47], pack=False)
+    scene = W.make_scene(w)
+    fm = scene.layout.seq_frames(0)
+    n_anchor = 0
+    for i, t in enumerate(si.steps):
+        r, c = int(fm[t, 1]), int(fm[t, 2])
+        u, v = _centre(si.element[i])
+        assert scene.content[t].reshape(r, c)[u, v]
+        if si.anchor[i] is not None:
+            f, u0, v0, h, ww = si.anchor[i]
+            p = (u0 + h // 2) * c + (v0 + ww // 2)
+            assert f < t and scene.content[f][p]
+            assert (scene.frame_emb[f][p] != scene.frame_emb[t][p]).any()
+            n_anchor += 1
+    assert n_anchor >= 2
