@@ -123,10 +123,14 @@ struct SelectRes {
   static constexpr int kGroup = 1;        // tiles a classifying wave loads at once (segsel_split.h)
   static constexpr bool kDirect = false;  // a ranked list: the splitter path emits it from codes
   static constexpr bool aligned = false;
-  __amdgpu_buffer_rsrc_t a_base;  // the segment's A, Phi and gate (out-of-range lanes read 0)
+  // The segment's A, Phi and gate (out-of-range lanes read 0).  A Phi or gate
+  // the call does not give is a buffer of no records: its loads return 0
+  // without touching memory, so every load is issued unconditionally.
+  __amdgpu_buffer_rsrc_t a_base;
   __amdgpu_buffer_rsrc_t phi;
   __amdgpu_buffer_rsrc_t gate;
   bool has_phi, has_gate;
+  uint32_t closed;   // the gate byte of a gated-out token: 0, or 256 (no byte) without a gate
   bool needs_class;  // Phi or the gate is given: visual tokens must be told from text
   float alpha;
   float* score;      // nullable: the segment's S
@@ -144,8 +148,8 @@ struct SelectRes {
     for (int e = 0; e < 4; ++e) {
       const int32_t i = base + 64 * e + lane;
       r.A[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
-      r.ph[e] = has_phi ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0)) : 0.0f;
-      r.g[e] = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+      r.ph[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0));
+      r.g[e] = __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0);
     }
   }
 
@@ -153,7 +157,7 @@ struct SelectRes {
   __device__ float score_of(float A, float ph, uint32_t g, bool visual) const {
     if (!visual) return A;
     const float x = has_phi ? fmaf(alpha, ph, A) : A;
-    return g == 0 ? 0.0f : x;
+    return g == closed ? 0.0f : x;
   }
 
   __device__ void keys(int32_t base, const int (&cls)[4], int32_t hi, const Raw& r, uint32_t (&key)[4]) const {
@@ -195,15 +199,15 @@ struct SelectRes {
   // The gate byte first; A and Phi only where S depends on them (a text
   // token, or a visual one whose gate is not zero).
   __device__ void load1(int32_t i, Raw1& r) const {
-    r.g = has_gate ? __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0) : 1u;
+    r.g = __builtin_amdgcn_raw_buffer_load_b8(gate, i, 0, 0);
   }
 
   __device__ void load1_rest(int32_t i, int cls, Raw1& r) const {
     r.A = 0.0f;
     r.ph = 0.0f;
-    if (cls == kText || r.g != 0u) {
+    if (cls == kText || r.g != closed) {
       r.A = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(a_base, i * 4, 0, 0));
-      if (has_phi) r.ph = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0));
+      r.ph = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(phi, i * 4, 0, 0));
     }
   }
 
@@ -226,10 +230,11 @@ __device__ inline SelectRes select_res(const SelectArgs& a, const SelCtx& c, int
   p.a_base = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.a_base) + seg0, 0, c.n * 4, kBufferFlags);
   p.has_phi = a.phi != nullptr;
   p.has_gate = a.gate != nullptr;
-  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0, c.n * 4,
-                                            kBufferFlags);
+  p.phi = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.has_phi ? a.phi + seg0 : a.a_base), 0,
+                                            p.has_phi ? c.n * 4 : 0, kBufferFlags);
   p.gate = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.has_gate ? a.gate + seg0 : nullptr), 0,
                                              p.has_gate ? c.n : 0, kBufferFlags);
+  p.closed = p.has_gate ? 0u : 256u;
   p.needs_class = p.has_phi || p.has_gate;
   p.alpha = a.alpha;
   p.score = (score && a.score) ? a.score + seg0 : nullptr;
