@@ -138,12 +138,15 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), flush=True)
 
 
-def cpu_baseline(w, case_inputs, budget_s=6.0, runs=3):
+def cpu_baseline(w, case_inputs, budget_s=6.0, runs=3, literal=False):
     """The fp64 oracle on the host, timed the way the baseline plan asks: one
     untimed unit, then the median of `runs` timed passes over a sample of whole
     (layer, kv head) units (every sequence) sized to ~budget_s per pass from
-    the untimed unit's time, scaled to all units."""
+    the untimed unit's time, scaled to all units.  literal: time the
+    pure-Python loop twin of the oracle instead of the NumPy one (meant for the
+    tiny workload)."""
     from oracle import stlite_oracle as O
+    from oracle import literal as O1
     scene, k, v, q = case_inputs
     lay = scene.layout
     try:
@@ -158,8 +161,15 @@ def cpu_baseline(w, case_inputs, budget_s=6.0, runs=3):
     def one(unit):
         l, h = unit
         for s in range(lay.n_seqs):
-            O.compress_sequence(q, k, v, lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s, l, h, w.group,
-                                w.beta, w.alpha)
+            if literal:
+                a, b = int(lay.cu_seqlens[s]), int(lay.cu_seqlens[s + 1])
+                Q = O.bf16_to_f64(q[l, s, h * w.group:(h + 1) * w.group]).tolist()
+                K = O.bf16_to_f64(k[l, h, a:b]).tolist()
+                frames = O.seq_frames_local(lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s)
+                O1.compress(Q, K, frames, O.budget(b - a, *w.beta), w.alpha)
+            else:
+                O.compress_sequence(q, k, v, lay.cu_seqlens, lay.cu_frames, lay.frame_meta, s, l, h, w.group,
+                                    w.beta, w.alpha)
 
     t0 = time.perf_counter()
     one(order[0])  # untimed
@@ -175,9 +185,11 @@ def cpu_baseline(w, case_inputs, budget_s=6.0, runs=3):
         log(f"cpu baseline: timed run {r + 1} of {runs}: {n} units in {times[-1]:.3g} s")
     med = float(np.median(times))
     rate = lay.total_tokens / (med / n * len(units_all))
-    return {"value": round(rate, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+    what = "pure-Python loop twin of the oracle (one thread)" if literal else "fp64 NumPy oracle"
+    return {"value": round(rate, 1), "unit": "tokens/s", "cores": 1 if literal else int(cores),
+            "kind": "oracle-literal" if literal else "oracle",
             "sample": f"{n} of {len(units_all)} (layer, kv head) units of the full workload, every sequence, "
-                      f"fp64 NumPy oracle; one untimed unit, then the median of {runs} timed passes "
+                      f"{what}; one untimed unit, then the median of {runs} timed passes "
                       f"({', '.join(f'{t:.3g}' for t in times)} s), rate scaled to all {len(units_all)} units"}
 
 
@@ -495,6 +507,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-baseline-only", action="store_true",
                     help="only time the fp64 oracle on the host for --config (no GPU work) and print it")
+    ap.add_argument("--literal", action="store_true",
+                    help="with --cpu-baseline-only: time the pure-Python loop twin of the oracle instead "
+                         "(the tiny workload, --config 0)")
     ap.add_argument("--pass-only", action="store_true",
                     help="time the pass only: no measured peaks, decode, variants, cache hit rate or "
                          "multi-step timings (for counter runs)")
@@ -513,7 +528,7 @@ def main():
     if args.cpu_baseline_only:
         w = W.config(args.config, beta).with_screen(args.screen)
         log(f"generating {w.name}: {w.total_tokens} tokens x {w.n_layers} layers")
-        base = cpu_baseline(w, W.make_inputs(w, workers=16))
+        base = cpu_baseline(w, W.make_inputs(w, workers=16), literal=args.literal)
         print(json.dumps({"config": w.name, "tokens": w.total_tokens, "cpu_baseline": base}), flush=True)
         return
 
