@@ -127,7 +127,8 @@ typedef enum stlite_similarity {
  *
  * Limits: head_dim == 128; n_q_heads % n_kv_heads == 0; 1 <= window <= L_s for
  * every sequence; G * window <= 512 (the window queries of one kv head stay
- * resident in registers); total_tokens < 2^31; L_s <= 2^28; n_seqs <= 65535;
+ * resident in registers); total_tokens < 2^31; L_s <= 2^28; rows * cols <= 2^22
+ * for every frame; n_seqs <= 65535;
  * n_layers * n_kv_heads <= 65535 (outside these, STLITE_ERR_UNSUPPORTED).
  * Budgets are per sequence
  * (the same for every layer and head: the paper's flat budget) and must satisfy

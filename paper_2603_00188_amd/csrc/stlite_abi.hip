@@ -333,6 +333,8 @@ int64_t stlite_budget(int64_t L, int64_t beta_num, int64_t beta_den) {
   return static_cast<int64_t>(prod / beta_den);
 }
 
+constexpr int64_t kMaxFramePatches = int64_t(1) << 22;  // rows * cols of one frame
+
 stlite_status stlite_validate(const stlite_problem* p) {
   if (!p) return fail(STLITE_ERR_INVALID_ARG, "problem is NULL");
   if (p->reserved != 0) return fail(STLITE_ERR_INVALID_ARG, "reserved field must be 0");
@@ -377,6 +379,11 @@ stlite_status stlite_validate(const stlite_problem* p) {
       const int64_t off = p->h_frame_meta[3 * f], r = p->h_frame_meta[3 * f + 1], c = p->h_frame_meta[3 * f + 2];
       if (r < 1 || c < 1) return fail(STLITE_ERR_INVALID_ARG, "frame %d has an empty grid (%lld x %lld)", f,
                                       (long long)r, (long long)c);
+      // A frame's keys are addressed by buffer descriptors of 32-bit byte
+      // counts (256 bytes per patch): 2^22 patches keep them below 2^30.
+      if (r * c > kMaxFramePatches)
+        return fail(STLITE_ERR_UNSUPPORTED, "frame %d has %lld patches; at most 2^22 are supported", f,
+                    (long long)(r * c));
       if (off < prev_end || off + r * c > b)
         return fail(STLITE_ERR_INVALID_ARG,
                     "frame %d [%lld, %lld) overlaps its predecessor or leaves sequence %d [%lld, %lld)", f,

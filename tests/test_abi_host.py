@@ -80,6 +80,13 @@ class HostProblem:
         return S.load().stlite_validate(ctypes.byref(self.c))
 
 
+def _one_huge_frame(p):
+    # a single 2049 x 2048 frame (2^22 + 2048 patches) in a sequence long enough to hold it
+    n = 2049 * 2048 + 40
+    q = HostProblem([0, n], [[(0, 2049, 2048)]], [n // 5])
+    p.__dict__.update(q.__dict__)
+
+
 def good():
     # two sequences: [frame 4x5 | 10 text | frame 4x5 | 12 text], [30 text]
     return HostProblem([0, 72, 102], [[(0, 4, 5), (30, 4, 5)], []], [14, 6])
@@ -113,6 +120,7 @@ def test_valid_problem_and_workspace_sizes():
     (lambda p: p.frame_meta.__setitem__((1, 0), 10), S.ERR_INVALID_ARG, "overlaps"),
     (lambda p: p.frame_meta.__setitem__((1, 1), 9), S.ERR_INVALID_ARG, "leaves sequence"),
     (lambda p: p.frame_meta.__setitem__((0, 2), 0), S.ERR_INVALID_ARG, "empty grid"),
+    (lambda p: _one_huge_frame(p), S.ERR_UNSUPPORTED, "at most 2^22"),
     (lambda p: p.cu_budget.__setitem__(1, 80), S.ERR_INVALID_ARG, "budget"),
     (lambda p: p.cu_frames.__setitem__(2, 1), S.ERR_INVALID_ARG, "cu_frames"),
 ])
@@ -121,6 +129,12 @@ def test_validation_rejects(mutate, status, text):
     mutate(p)
     assert p.validate() == status
     assert text in S.load().stlite_last_error().decode()
+
+
+def test_frame_of_exactly_2_22_patches_is_accepted():
+    n = 2048 * 2048 + 40
+    p = HostProblem([0, n], [[(0, 2048, 2048)]], [n // 5])
+    assert p.validate() == S.OK, S.load().stlite_last_error()
 
 
 def test_calls_fail_before_launch():
