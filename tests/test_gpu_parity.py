@@ -335,6 +335,29 @@ def test_selection_paths_agree(torch_cuda, monkeypatch, path):
             assert np.array_equal(got[key], ref[key], equal_nan=True), (name, path, key)
 
 
+@pytest.mark.parametrize("path", [None, "split"])
+@pytest.mark.parametrize("css, tsg", [(True, False), (False, True)], ids=["css_only", "tsg_only"])
+def test_component_ablations(torch_cuda, monkeypatch, path, css, tsg):
+    """The one-component variants of the procedure: CSS without the gate
+    (every visual token admitted, the top-B reads Phi and no gate) and the
+    gate without CSS (no Phi term, the top-B reads the gate and no Phi),
+    against the oracle with the same switches, under the default and the
+    splitter selection."""
+    H = _H()
+    if path:
+        monkeypatch.setenv("STLITE_SELECT_PATH", path)
+    else:
+        monkeypatch.delenv("STLITE_SELECT_PATH", raising=False)
+    for name in ("ragged", "dups", "gui"):
+        w = SMALL[name]
+        case = H.Case(w)
+        res = case.run(css=css, tsg=tsg)
+        for layer in range(w.n_layers):
+            for kv in range(w.n_kv_heads):
+                for s in range(case.lay.n_seqs):
+                    H.compare_unit(case, res, layer, kv, s, css=css, tsg=tsg)
+
+
 def test_split_tsg_matches_fused(torch_cuda):
     """stlite_tsg_rho followed by stlite_tsg_threshold reproduces stlite_tsg_gate
     bit for bit (rho, gate and tau)."""
