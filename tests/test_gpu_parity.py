@@ -189,11 +189,16 @@ STAGE_LAYOUTS = {
     # a 168,000-token segment, longer than the on-chip selection holds: every
     # segment of the call takes the splitter selection by default
     "long": ((80, (40, 50), 100), (5, (30, 37), 77)),
+    # a 336,000-token segment: about 9.7 % of it (32,600 keys at beta = 1/5, more at 1/2) lies
+    # between the splitters, more than one resolving batch (24,576), so resolve reloads the
+    # candidate list batch by batch
+    "huge": ((160, (40, 50), 100), (5, (30, 37), 77)),
 }
 
 # (layout, selection path forced through STLITE_SELECT_PATH; None = the default)
 STAGE_CASES = [("short", None), ("long", None), ("long", "four_pass"), ("long", "split_exact"),
-               ("short", "split"), ("short", "split_exact"), ("short", "four_pass")]
+               ("short", "split"), ("short", "split_exact"), ("short", "four_pass"),
+               ("huge", None), ("huge", "split_exact")]
 
 
 @pytest.mark.parametrize("layout,path", STAGE_CASES)
