@@ -193,12 +193,15 @@ STAGE_LAYOUTS = {
     # between the splitters, more than one resolving batch (24,576), so resolve reloads the
     # candidate list batch by batch
     "huge": ((160, (40, 50), 100), (5, (30, 37), 77)),
+    # a 1,050,000-token segment: more tiles (4,102) than resolve counts in LDS (4,096), so the
+    # taken counts per tile go through global atomics
+    "giant": ((500, (40, 50), 100), (5, (30, 37), 77)),
 }
 
 # (layout, selection path forced through STLITE_SELECT_PATH; None = the default)
 STAGE_CASES = [("short", None), ("long", None), ("long", "four_pass"), ("long", "split_exact"),
                ("short", "split"), ("short", "split_exact"), ("short", "four_pass"),
-               ("huge", None), ("huge", "split_exact")]
+               ("huge", None), ("huge", "split_exact"), ("giant", None)]
 
 
 @pytest.mark.parametrize("layout,path", STAGE_CASES)
