@@ -16,7 +16,7 @@ def torch_cuda():
     return torch
 
 
-@pytest.mark.parametrize("name", ["ragged", "tiles", "g1w1", "g8w64", "beta_tiny", "beta_one"])
+@pytest.mark.parametrize("name", ["ragged", "tiles", "g1w1", "g8w64", "g16w32", "beta_tiny", "beta_one"])
 def test_decode_small_all_units(torch_cuda, name):
     from tests import gpu_harness as H
     from tests.test_gpu_parity import SMALL

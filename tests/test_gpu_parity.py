@@ -88,6 +88,9 @@ SMALL = {
     # several key chunks per sequence, a short second sequence, and 28 padding rows in a split block
     "g7w64": _small([[(F, 20, 30), (T, 100)] * 4, [(T, 50), (F, 9, 10), (T, 77)]], G=7, Hkv=1, window=64, layers=1),
     "g7w60": _small([[(F, 20, 30), (T, 100)] * 3, [(F, 5, 6), (T, 300)]], G=7, Hkv=2, window=60, layers=1),
+    # the largest GQA group decode takes (16, no padded heads) at the largest window-row count (512)
+    "g16w32": _small([[(F, 10, 12), (T, 40), (F, 10, 12), (T, 60)], [(T, 20), (F, 6, 7), (T, 35)]],
+                     G=16, Hkv=2, window=32, layers=1),
     # more frames in one sequence than the selection kernels keep in LDS (1024)
     "many_frames": _small([[(F, 2, 3), (T, 1)] * 1100 + [(T, 20)]], G=2, Hkv=1, layers=1, beta=(1, 3)),
     # gui screens (flat textured panels and element patches): clusters of close Phi, rho and S values
