@@ -88,6 +88,8 @@ SMALL = {
     # several key chunks per sequence, a short second sequence, and 28 padding rows in a split block
     "g7w64": _small([[(F, 20, 30), (T, 100)] * 4, [(T, 50), (F, 9, 10), (T, 77)]], G=7, Hkv=1, window=64, layers=1),
     "g7w60": _small([[(F, 20, 30), (T, 100)] * 3, [(F, 5, 6), (T, 300)]], G=7, Hkv=2, window=60, layers=1),
+    # 13 row blocks: the only block count that takes the plain 7-wave layout
+    "g13w32": _small([[(F, 9, 10), (T, 30), (F, 9, 10), (T, 90)]], G=13, Hkv=1, window=32, layers=1),
     # the largest GQA group decode takes (16, no padded heads) at the largest window-row count (512)
     "g16w32": _small([[(F, 10, 12), (T, 40), (F, 10, 12), (T, 60)], [(T, 20), (F, 6, 7), (T, 35)]],
                      G=16, Hkv=2, window=32, layers=1),
