@@ -488,9 +488,17 @@ SPIKE_CASES = {
                              G=4, Hkv=3, window=16, beta=(3, 10), layers=1), 0),
     "g7w64": (lambda: _small([[(F, 20, 30), (T, 100)] * 4], G=7, Hkv=1, window=64, beta=(3, 10), layers=1), 6),
 }
+# The exact pass at the other wave layouts: one 32-row block (1 wave), 6 blocks (3 waves) and
+# 13 blocks (the plain 7-wave layout); key chunks of >= 1024 keys keep the spike keys
+# 200, 460 and 700 out of the first tile of their chunk.
+SPIKE_LAYOUTS = dict(SPIKE_CASES, **{
+    "g1w1": (lambda: _small([[(F, 20, 30), (T, 100)] * 2], G=1, Hkv=2, window=1, beta=(3, 10), layers=1), 0),
+    "g3w60": (lambda: _small([[(F, 20, 30), (T, 100)] * 2], G=3, Hkv=1, window=60, beta=(3, 10), layers=1), 2),
+    "g13w32": (lambda: _small([[(F, 20, 30), (T, 100)] * 2], G=13, Hkv=1, window=32, beta=(3, 10), layers=1), 12),
+})
 
 
-@pytest.mark.parametrize("name", list(SPIKE_CASES))
+@pytest.mark.parametrize("name", list(SPIKE_LAYOUTS))
 def test_logit_spike_takes_exact_pass(torch_cuda, name):
     """Keys aligned with a window query, far into a chunk, push that query's
     logits about 150 log2 units above the chunk's first tile, so that the lean
@@ -500,7 +508,7 @@ def test_logit_spike_takes_exact_pass(torch_cuda, name):
     H = _H()
     from oracle import stlite_oracle as O
     from paper_2603_00188_amd import workload as W2
-    make, head = SPIKE_CASES[name]
+    make, head = SPIKE_LAYOUTS[name]
     w = make()
     case = H.Case(w)
     q = O.bf16_to_f64(case.q[0, 0, head, 0])        # window position 0 of the head
