@@ -1310,12 +1310,14 @@ template <class Args>
 hipError_t launch_split(void (*sample)(Args), void (*classify)(Args), void (*resolve)(Args), void (*emit)(Args),
                         const Args& a_in, const Layout& lay, hipStream_t stream) {
   if (lay.n_units == 0 || lay.n_seqs == 0) return hipSuccess;
-  static int occupancy = 0;  // work-groups of the classify kernel per CU (-1: unknown)
-  if (occupancy == 0) {
+  // Work-groups of the classify kernel per CU (-1: unknown), queried on the
+  // first call; a function-local static is initialised once even when
+  // several host threads make that first call together.
+  static const int occupancy = [classify]() {
     int b = 0;
-    occupancy = hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, classify, kSpPassThreads, 0) == hipSuccess && b > 0
-                    ? b : -1;
-  }
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, classify, kSpPassThreads, 0) == hipSuccess && b > 0 ? b
+                                                                                                              : -1;
+  }();
   Args a = a_in;
   SelPlan& s = a.sel;
   if (occupancy > 0) {
