@@ -131,6 +131,41 @@ def test_validation_rejects(mutate, status, text):
     assert text in S.load().stlite_last_error().decode()
 
 
+def test_last_error_is_per_thread():
+    """Each host thread reads the message of its own last failure: several
+    threads validate differently broken problems at once (ctypes releases the
+    GIL during the calls) and each sees its own reason."""
+    import threading
+    cases = [(lambda p: setattr(p.c, "window", 0), "window"),
+             (lambda p: setattr(p.c, "head_dim", 64), "head_dim"),
+             (lambda p: setattr(p.c, "reserved", 1), "reserved"),
+             (lambda p: setattr(p.c, "total_tokens", 103), "total_tokens")]
+    lib = S.load()
+    seen, errors = {}, []
+    start = threading.Barrier(len(cases))
+
+    def run(i, mutate, text):
+        p = good()
+        mutate(p)
+        start.wait()
+        for _ in range(200):
+            if p.validate() == S.OK:
+                errors.append((i, "validated"))
+                return
+            msg = lib.stlite_last_error().decode()
+            if text not in msg:
+                errors.append((i, msg))
+                return
+        seen[i] = text
+
+    threads = [threading.Thread(target=run, args=(i, m, t)) for i, (m, t) in enumerate(cases)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors and len(seen) == len(cases), errors
+
+
 def test_frame_of_exactly_2_22_patches_is_accepted():
     n = 2048 * 2048 + 40
     p = HostProblem([0, n], [[(0, 2048, 2048)]], [n // 5])
