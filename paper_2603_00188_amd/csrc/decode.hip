@@ -183,9 +183,13 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_chunk_kernel(DecodeArgs
 }
 
 // Per (unit, sequence, query head): merge the chunks, out = O / L (0 for a
-// sequence without rows).  One output dimension per thread; the chunks are
-// merged in one pass with a running maximum M, rescaling L and O whenever it
-// rises, so the loads of successive chunks do not wait on each other.
+// sequence without rows).  One output dimension per thread.  The partials of
+// kCombineBatch chunks are loaded before any of them is merged, so a batch
+// costs one memory latency; the batch is weighed against its maximum (a chunk
+// that saw no row of the sequence has max -inf and weighs nothing) and merged
+// into the running (M, L, O).
+constexpr int kCombineBatch = 16;
+
 __global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(DecodeArgs a) {
   const int32_t s = blockIdx.x;
   const int unit = blockIdx.y, h = blockIdx.z;
@@ -196,15 +200,30 @@ __global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(DecodeArgs a) 
   const int32_t nch = (a.cu_rows[s + 1] - a.cu_rows[s] + a.chunk - 1) / a.chunk;
   const size_t c0 = size_t(unit) * a.total_chunks + first;
   float M = -INFINITY, L = 0.0f, O = 0.0f;
-#pragma unroll 4
-  for (int32_t c = 0; c < nch; ++c) {
-    const size_t ch = (c0 + c) * kDecHeads + h;
-    const float m = a.pm[ch], l = a.pl[ch], o = a.po[ch * kHeadDim + dim];
-    if (m == -INFINITY) continue;  // a chunk that saw no row of the sequence
-    const float mx = fmaxf(M, m);
-    const float sa = __builtin_amdgcn_exp2f(M - mx), sb = __builtin_amdgcn_exp2f(m - mx);
-    L = L * sa + l * sb;
-    O = O * sa + o * sb;
+  for (int32_t b0 = 0; b0 < nch; b0 += kCombineBatch) {
+    float m[kCombineBatch], l[kCombineBatch], o[kCombineBatch];
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) {
+      // slots past the sequence's last chunk re-read that chunk and weigh nothing
+      const size_t ch = (c0 + size_t(min(b0 + i, nch - 1))) * kDecHeads + h;
+      const float mv = a.pm[ch];
+      l[i] = a.pl[ch];
+      o[i] = a.po[ch * kHeadDim + dim];
+      m[i] = b0 + i < nch ? mv : -INFINITY;
+    }
+    float mx = M;
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) mx = fmaxf(mx, m[i]);
+    if (mx == -INFINITY) continue;  // no chunk so far saw a row of the sequence
+    const float sa = __builtin_amdgcn_exp2f(M - mx);  // 0 while M is still -inf
+    L *= sa;
+    O *= sa;
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) {
+      const float w = m[i] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m[i] - mx);
+      L += w * l[i];
+      O += w * o[i];
+    }
     M = mx;
   }
   a.out[((size_t(layer) * a.lay.n_seqs + s) * a.n_q_heads + size_t(kv) * a.group + h) * kHeadDim + dim] =
