@@ -93,3 +93,15 @@ def test_measured_traffic_follows_the_source_digest(bench, tmp_path, monkeypatch
         "# t\n\n- source_digest: `0000000000000000`\n- hbm_bytes_per_launch: 4701373011\n")
     assert bench.measured_traffic("rho_kernel", "w") is None          # sources changed
     assert bench.measured_traffic("compact_kernel", "w") is None      # no sources listed
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark measures one GPU: --gpus above 1 exits with a message
+    before touching any device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr or "single MI355X" in r.stderr
+    assert r.stdout == ""
