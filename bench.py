@@ -295,7 +295,9 @@ def measured_peaks(stream):
     kernels use, driven by stlite_probe_mfma with random operands that rotate
     per instruction, and the 32x32x16 shape carrying the window score's vector
     work (fma + exp2 + add per logit); a large hipBLASLt bf16 GEMM
-    (torch.matmul); and a device copy (torch copy_, bytes read + written)."""
+    (torch.matmul); a device copy (torch copy_, bytes read + written); and a
+    streaming read of 4 GiB through stlite_probe_read with the default and the
+    non-temporal cache policy."""
     import torch
     from paper_2603_00188_amd import stlite as S
 
@@ -333,7 +335,14 @@ def measured_peaks(stream):
     with torch.cuda.stream(stream):
         t = timed(lambda: dst.copy_(src), 10)
     out["device_copy_2gib_gbs"] = round(2.0 * src.numel() / t / 1e9, 1)
-    del a, b, src, dst, ops, sink
+    # a streaming read of 4 GiB (stlite_probe_read), default and non-temporal cache policy
+    rd = torch.empty(1 << 32, dtype=torch.uint8, device="cuda")
+    rd_groups = 8192
+    rd_sink = torch.empty(rd_groups * 256, dtype=torch.float32, device="cuda")
+    for name, nt in (("hbm_stream_read_4gib_gbs", False), ("hbm_stream_read_4gib_nontemporal_gbs", True)):
+        t = timed(lambda: S.stlite_probe_read(rd, rd.numel(), rd_sink, rd_groups, nt, stream), 10)
+        out[name] = round(rd.numel() / t / 1e9, 1)
+    del a, b, src, dst, ops, sink, rd, rd_sink
     log("measured peaks: " + ", ".join(f"{k} {v}" for k, v in out.items()))
     return out
 

@@ -1,7 +1,7 @@
 /*
- * stlite_probe.h -- throughput probes of the MI355X matrix cores, used by the
- * benchmark as a measured second denominator beside the published bf16 peak.
- * Not part of the compression method.
+ * stlite_probe.h -- throughput probes of the MI355X matrix cores and of its
+ * HBM read path, used by the benchmark as measured second denominators beside
+ * the published bf16 and bandwidth peaks.  Not part of the compression method.
  *
  * Each probe keeps every SIMD busy with independent MFMA chains whose
  * operands come from caller-supplied data and rotate among eight A and
@@ -49,6 +49,19 @@ typedef enum stlite_probe_shape {
  */
 stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint16_t* operands, float* sink,
                                 int32_t n_groups, int32_t iters, void* stream);
+
+/*
+ * Streaming read of `bytes` bytes at `src` (device), once, in 16-byte loads:
+ * n_groups work-groups of 256 threads, each lane reading every
+ * (n_groups * 256)-th 16-byte word, four loads in flight per lane; with
+ * `nontemporal` != 0 the loads carry the non-temporal cache policy.
+ *   src   device, 16-byte aligned, bytes a positive multiple of 16
+ *   sink  device, fp32, >= n_groups * 256 elements (written: keeps the loads)
+ * A NULL pointer, a misaligned or empty source, or n_groups < 1 is
+ * STLITE_ERR_INVALID_ARG.  Enqueues on `stream` only.
+ */
+stlite_status stlite_probe_read(const void* src, size_t bytes, float* sink, int32_t n_groups,
+                                int32_t nontemporal, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,4 +1,4 @@
-// Matrix-core throughput probes (measurement only; see stlite_probe.h).
+// Matrix-core and HBM read throughput probes (measurement only; see stlite_probe.h).
 #include <type_traits>
 
 #include "stlite_probe.h"
@@ -111,8 +111,45 @@ __global__ __launch_bounds__(kProbeThreads, 2) void probe_mfma_kernel(const uint
   sink[lane_id] = s;
 }
 
+typedef uint32_t probe_u32x4_t __attribute__((ext_vector_type(4)));
+
+// Streams n16 16-byte words once: each lane reads words i, i + stride, ...
+// four at a time (all four loads issued before they are combined), with the
+// default cache policy or non-temporal loads.  The XOR of what a lane read
+// goes to the sink, so no load can be dropped.
+template <bool NT>
+__global__ __launch_bounds__(kProbeThreads) void probe_read_kernel(const probe_u32x4_t* src, size_t n16, float* sink) {
+  const size_t stride = size_t(gridDim.x) * kProbeThreads;
+  size_t i = size_t(blockIdx.x) * kProbeThreads + threadIdx.x;
+  probe_u32x4_t acc = {0u, 0u, 0u, 0u};
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    probe_u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = NT ? __builtin_nontemporal_load(src + i + u * stride) : src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u];
+  }
+  for (; i < n16; i += stride) acc ^= NT ? __builtin_nontemporal_load(src + i) : src[i];
+  sink[size_t(blockIdx.x) * kProbeThreads + threadIdx.x] = __uint_as_float(acc.x ^ acc.y ^ acc.z ^ acc.w);
+}
+
 }  // namespace
 }  // namespace stlite
+
+extern "C" stlite_status stlite_probe_read(const void* src, size_t bytes, float* sink, int32_t n_groups,
+                                           int32_t nontemporal, void* stream) {
+  using namespace stlite;
+  if (!src || !sink || n_groups < 1 || bytes == 0 || bytes % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(src) % 16 != 0)
+    return STLITE_ERR_INVALID_ARG;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const probe_u32x4_t* words = static_cast<const probe_u32x4_t*>(src);
+  if (nontemporal)
+    hipLaunchKernelGGL(probe_read_kernel<true>, dim3(n_groups), dim3(kProbeThreads), 0, st, words, bytes / 16, sink);
+  else
+    hipLaunchKernelGGL(probe_read_kernel<false>, dim3(n_groups), dim3(kProbeThreads), 0, st, words, bytes / 16, sink);
+  return hipGetLastError() == hipSuccess ? STLITE_OK : STLITE_ERR_HIP;
+}
 
 extern "C" stlite_status stlite_probe_mfma(stlite_probe_shape shape, const uint16_t* operands, float* sink,
                                            int32_t n_groups, int32_t iters, void* stream) {

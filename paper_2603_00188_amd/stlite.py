@@ -26,7 +26,7 @@ EXPORTS = (
     "stlite_validate", "stlite_workspace_size", "stlite_score_window", "stlite_css_saliency",
     "stlite_tsg_gate", "stlite_tsg_rho", "stlite_tsg_threshold", "stlite_select_topk", "stlite_compact_kv",
     "stlite_decode_attention", "stlite_tsg_similarity", "stlite_tsg_fixed_gate",
-    "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma",
+    "stlite_css_saliency_nbhd", "stlite_kept_overlap", "stlite_probe_mfma", "stlite_probe_read",
     "stlite_layer_mean", "stlite_tsg_rho_concat", "stlite_css_saliency_concat", "stlite_compact_kv_layer",
     "stlite_select_topk_noalloc", "stlite_mean_attention",
 )
@@ -86,6 +86,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "stlite_css_saliency_nbhd": (st, [P, ctypes.c_int32, vp, vp, vp]),
         "stlite_kept_overlap": (st, [P, vp, vp, vp, vp]),
         "stlite_probe_mfma": (st, [st, vp, vp, ctypes.c_int32, ctypes.c_int32, vp]),
+        "stlite_probe_read": (st, [vp, sz, vp, ctypes.c_int32, ctypes.c_int32, vp]),
         "stlite_layer_mean": (st, [P, vp, vp, vp]),
         "stlite_mean_attention": (st, [P, vp, ctypes.c_int32, vp, vp]),
         "stlite_tsg_rho_concat": (st, [P, vp, vp, vp, sz, vp]),
@@ -307,6 +308,11 @@ PROBE_MFMAS_PER_ITER = {PROBE_MFMA_16X16X32: 8, PROBE_MFMA_32X32X16: 8, PROBE_MF
 def stlite_probe_mfma(shape: int, operands, sink, n_groups: int, iters: int, stream=None) -> None:
     _check(load().stlite_probe_mfma(int(shape), _ptr(operands), _ptr(sink), int(n_groups), int(iters),
                                     _stream(stream)), "stlite_probe_mfma")
+
+
+def stlite_probe_read(src, nbytes: int, sink, n_groups: int, nontemporal: bool, stream=None) -> None:
+    _check(load().stlite_probe_read(_ptr(src), int(nbytes), _ptr(sink), int(n_groups), 1 if nontemporal else 0,
+                                    _stream(stream)), "stlite_probe_read")
 
 
 def stlite_mean_attention(p: Problem, a_base, width: int, a_mean, stream=None) -> None:

@@ -304,6 +304,13 @@ def test_probe_rejections():
     assert lib.stlite_probe_mfma(1, FAKE_DEV, None, 1, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(0, FAKE_DEV, FAKE_DEV, 0, 1, None) == S.ERR_INVALID_ARG
     assert lib.stlite_probe_mfma(1, FAKE_DEV, FAKE_DEV, 4, 0, None) == S.ERR_INVALID_ARG
+    # the read probe: NULL pointers, an empty, unaligned or ragged source, no work-group
+    assert lib.stlite_probe_read(None, 1024, FAKE_DEV, 1, 0, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_read(FAKE_DEV, 1024, None, 1, 1, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_read(FAKE_DEV, 0, FAKE_DEV, 1, 0, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_read(FAKE_DEV, 1000, FAKE_DEV, 1, 0, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_read(FAKE_DEV + 8, 1024, FAKE_DEV, 1, 0, None) == S.ERR_INVALID_ARG
+    assert lib.stlite_probe_read(FAKE_DEV, 1024, FAKE_DEV, 0, 0, None) == S.ERR_INVALID_ARG
 
 
 
